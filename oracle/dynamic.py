@@ -1,0 +1,108 @@
+"""Sliding-window IHVP oracle: y = F^-1 x in float64 (test infrastructure only).
+
+Definition followed (Theorem 1, Section 3.2; sliding window of Section 4.2):
+    F = lambda * I_d + (1/m) * G^T G,   G = the m x d window, one gradient per row.
+The 1/m scale is the window capacity m, also while some slots still hold zero
+rows (a zero row adds nothing to F).
+
+Evaluation: the Woodbury identity (the closed form that the Sherman-Morrison
+recursion of Section 2 eq. 2 unrolls to)
+    F^-1 x = (x - G^T (G G^T + m*lambda*I)^-1 G x) / lambda,
+with K = G G^T accumulated in float64 from the exact fp32 rows, one LAPACK
+Cholesky of K + m*lambda*I and two triangular solves. The paper states the
+method is numerically equivalent to the direct computation (Section 2), so the
+plain definition is the oracle. Pinned in tests/test_oracle_dynamic.py against
+the dense d x d solve, the m = 1 Sherman-Morrison closed form, orthogonal rows,
+G = 0, the matrix-free residual F y = x, and the paper's D/B/q recursion.
+"""
+
+import numpy as np
+import scipy.linalg as sla
+
+_CHUNK = 1 << 18  # columns per fp64 chunk (bounds the fp64 temporaries)
+
+
+def _chunks(d, chunk=_CHUNK):
+    for j0 in range(0, d, chunk):
+        yield j0, min(d, j0 + chunk)
+
+
+def gram(G, chunk=_CHUNK):
+    """K = G G^T in float64 from fp32 rows, accumulated over column chunks."""
+    m, d = G.shape
+    K = np.zeros((m, m), np.float64)
+    for j0, j1 in _chunks(d, chunk):
+        Gc = G[:, j0:j1].astype(np.float64)
+        K += Gc @ Gc.T
+    return K
+
+
+def matvec(G, X, chunk=_CHUNK):
+    """P = G X^T (m x n) in float64; X is (n, d)."""
+    m, d = G.shape
+    P = np.zeros((m, X.shape[0]), np.float64)
+    for j0, j1 in _chunks(d, chunk):
+        P += G[:, j0:j1].astype(np.float64) @ X[:, j0:j1].astype(np.float64).T
+    return P
+
+
+class WindowOracle:
+    """The m x d window, its float64 Gram matrix, and exact IHVPs.
+
+    ``G0`` (m x d fp32) initialises the window; None starts with zero rows.
+    """
+
+    def __init__(self, d, m, lam, G0=None):
+        self.d, self.m, self.lam = int(d), int(m), float(lam)
+        if G0 is None:
+            self.G = np.zeros((m, d), np.float32)
+            self.K = np.zeros((m, m), np.float64)
+        else:
+            self.G = np.array(G0, dtype=np.float32, copy=True)
+            assert self.G.shape == (m, d)
+            self.K = gram(self.G)
+        self.steps = 0
+
+    def replace(self, slot, g):
+        """Overwrite row ``slot`` with g and refresh row and column slot of K.
+
+        Section 3.2 (initial precomputation and update): only the scalar
+        products of the new gradient with the window change.
+        """
+        g = np.asarray(g, dtype=np.float32)
+        self.G[slot] = g
+        p = matvec(self.G, g[None, :])[:, 0]
+        self.K[slot, :] = p
+        self.K[:, slot] = p
+        self.steps += 1
+        return p
+
+    def slide(self, g):
+        """Ring semantics: replace the oldest slot (steps mod m), return F^-1 g.
+
+        Section 4.2: the window drops its oldest gradient, takes the newest, and
+        the same newest gradient is then preconditioned.
+        """
+        slot = self.steps % self.m
+        self.replace(slot, g)
+        return self.ihvp(np.asarray(g, np.float32)[None, :])[0]
+
+    def coefficients(self, P):
+        """U = (K + m*lambda*I)^-1 P for P (m x n)."""
+        A = self.K + self.m * self.lam * np.eye(self.m)
+        c, low = sla.cho_factor(A, lower=True)
+        return sla.cho_solve((c, low), P)
+
+    def ihvp(self, X):
+        """F^-1 X for X of shape (d,) or (n, d); returns float64 of that shape."""
+        X = np.asarray(X, dtype=np.float32)
+        single = X.ndim == 1
+        if single:
+            X = X[None, :]
+        P = matvec(self.G, X)
+        U = self.coefficients(P)
+        Y = np.empty(X.shape, np.float64)
+        for j0, j1 in _chunks(self.d):
+            Gc = self.G[:, j0:j1].astype(np.float64)
+            Y[:, j0:j1] = (X[:, j0:j1].astype(np.float64) - U.T @ Gc) / self.lam
+        return Y[0] if single else Y

@@ -1,0 +1,68 @@
+"""The synthetic workloads, named by what they are.
+
+Each entry fixes the problem shape (d, m, lambda, block size), the gradient
+distribution and the run length. The gradient matrices stand in for the
+per-sample gradients of the paper's models (ResNet18 ~11.2M and ResNet50
+~25.6M parameters, Section 1 and Appendix on NF-ResNet50); no dataset or trained
+weight is used anywhere.
+
+Distributions:
+  "gauss"      entries N(0, 1/d)
+  "lognormal"  per-coordinate scale s_j ~ LogNormal(0, 1), fixed per seed;
+               entries s_j * N(0, 1) / sqrt(d)
+A fraction ``corr_frac`` of stream rows are made correlated with the previous
+stream row: g_r = 0.8 * g_{r-1} + 0.6 * noise_r (computed in fp64, stored fp32).
+"""
+
+from dataclasses import dataclass, replace
+from typing import Optional
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    kind: str            # "dynamic" or "static"
+    d: int
+    m: int
+    lam: float
+    dist: str            # "gauss" or "lognormal"
+    steps: int = 0       # sliding steps after the window is full (dynamic)
+    queries: int = 0     # extra IHVP queries fused into every step (dynamic)
+    corr_frac: float = 0.0
+    block: int = 0       # static: block size B (B divides d)
+    theta_std: float = 0.0
+    fill_by_replace: bool = False   # dynamic: start empty, fill with m replaces
+
+    def scaled(self, **kw) -> "Workload":
+        """Same recipe at another size (parity cases the oracle finishes in seconds)."""
+        return replace(self, **kw)
+
+
+WORKLOADS = {
+    # tiny sliding window; every step checked against the oracle
+    "dyn_tiny_d4096_m16": Workload(
+        "dyn_tiny_d4096_m16", "dynamic", d=4096, m=16, lam=1e-3, dist="gauss",
+        steps=32, fill_by_replace=True),
+    # mid-size window, coefficient phase comparable to the streaming passes
+    "dyn_d1m_m256": Workload(
+        "dyn_d1m_m256", "dynamic", d=1_048_576, m=256, lam=1e-4, dist="lognormal",
+        steps=100),
+    # ResNet18-sized window with 8 extra IHVP queries fused into each step
+    "dyn_resnet18_d11.2m_m1024_q8": Workload(
+        "dyn_resnet18_d11.2m_m1024_q8", "dynamic", d=11_200_000, m=1024, lam=1e-5,
+        dist="lognormal", steps=200, queries=8),
+    # ResNet50-sized window (~105 GB fp32 resident in HBM), 10% correlated rows
+    "dyn_resnet50_d25.6m_m1024": Workload(
+        "dyn_resnet50_d25.6m_m1024", "dynamic", d=25_600_000, m=1024, lam=1e-5,
+        dist="lognormal", steps=200, corr_frac=0.1),
+    # static block-wise pruning statistics: 2048 blocks of 2048 coordinates
+    "static_d4.19m_b2048_m1024": Workload(
+        "static_d4.19m_b2048_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
+        dist="lognormal", block=2048, theta_std=0.05),
+}
+
+HEADLINE = "dyn_resnet50_d25.6m_m1024"
+
+
+def get_workload(name: str) -> Workload:
+    return WORKLOADS[name]
