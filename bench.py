@@ -1,0 +1,251 @@
+"""Throughput of the M-FAC sliding-window step on one MI355X.
+
+A step is the whole dynamic hot path for one new gradient: write it into the
+oldest slot, refresh that row of the Gram matrix (pass 1 over the window),
+refactor the m x m coefficients, and return F^-1 g (pass 2 over the window).
+Default workload: d = 25,600,000, m = 1024, lambda = 1e-5, ResNet50-sized
+log-normal-scaled synthetic gradients with 10% correlated rows; the ~105 GB
+window and every step's gradient are resident in HBM before timing starts.
+
+Prints one JSON line (metric, value, ..., roofline, cpu_baseline).
+"""
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "IHVP steps/sec and achieved HBM GB/s at d=25.6M, m=1024 (1 GPU)"
+COUNTERS = os.path.join(ROOT, "profiles", "pass_kernels_hbm_counters.txt")
+PASS_SRC = os.path.join(ROOT, "paper_2107_03356_amd", "csrc", "pass.hip")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def pass_bytes(d, m):
+    """Algorithmic HBM bytes of one launch of each streaming pass (fp32).
+
+    pass 1: reads the m-1 other rows and the new gradient, writes the new row:
+            (m - 1) d + d + d = (m + 1) d floats
+    pass 2: reads all m rows, writes y: (m + 1) d floats
+    """
+    return 4 * (m + 1) * d, 4 * (m + 1) * d
+
+
+def read_counters(kernel):
+    """HBM traffic per launch from the committed rocprofv3 --pmc summary, if it
+    was taken on the current pass.hip (else None)."""
+    if not os.path.exists(COUNTERS):
+        return None
+    text = open(COUNTERS).read()
+    sha = hashlib.sha256(open(PASS_SRC, "rb").read()).hexdigest()[:16]
+    m = re.search(r"pass_src_sha256_16:\s*(\w+)", text)
+    if not m or m.group(1) != sha:
+        return None
+    m = re.search(rf"{kernel}_traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    return float(m.group(1)) if m else None
+
+
+def cpu_baseline(wl, seed, sample_div, nsteps):
+    """The fp64 oracle as it stands, on a column sample of the same workload.
+
+    Times `nsteps` oracle sliding steps on a window of m rows x d/sample_div
+    columns; the O(dm) part is scaled by sample_div to the full d, the O(m^3)
+    Cholesky part is timed separately and added once.
+    """
+    import numpy as np
+    import torch
+
+    from oracle.dynamic import WindowOracle
+    from synth import GradientStream
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    ds = wl.d // sample_div
+    swl = wl.scaled(d=ds, scale_d=wl.d)
+    gs = GradientStream(swl, seed=seed, device="cuda")
+    G0 = gs.window().cpu().numpy()
+    rows = [gs.step_row(t).cpu().numpy() for t in range(nsteps)]
+    orc = WindowOracle(ds, wl.m, wl.lam, G0=G0)
+    t0 = time.perf_counter()
+    for g in rows:
+        orc.slide(g)
+    t_steps = (time.perf_counter() - t0) / nsteps
+    P = np.zeros((wl.m, 1))
+    t0 = time.perf_counter()
+    for _ in range(nsteps):
+        orc.coefficients(P)
+    t_coef = (time.perf_counter() - t0) / nsteps
+    t_full = max(t_steps - t_coef, 0.0) * sample_div + t_coef
+    return {
+        "value": 1.0 / t_full,
+        "unit": "steps/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"{nsteps} oracle sliding steps (numpy fp64, Woodbury + LAPACK Cholesky) on a "
+                   f"{wl.m} x {ds} column sample (d/{sample_div}); O(dm) time x{sample_div} plus the "
+                   f"m^3 coefficient time ({t_coef * 1e3:.1f} ms)"),
+        "sec_per_step_full_d": t_full,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dyn_resnet50_d25.6m_m1024")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-div", type=int, default=64)
+    ap.add_argument("--cpu-steps", type=int, default=3)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the design for sharding d over GPUs is described in DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2107_03356_amd as P
+    from synth import GradientStream, get_workload
+
+    wl = get_workload(args.workload)
+    assert wl.kind == "dynamic"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    P.load()
+    d, m = wl.d, wl.m
+    nq = wl.queries
+    log(f"workload {wl.name}: d={d} m={m} lambda={wl.lam} queries={nq}")
+
+    # ---- setup (not timed): window rows and step gradients resident in HBM
+    t0 = time.perf_counter()
+    gs = GradientStream(wl, seed=args.seed, device=dev)
+    win = P.Window(d, m, wl.lam, max_queries=nq, device=dev)
+    batch = max(1, min(m, (4 << 30) // (4 * d)))
+    for r0 in range(0, m, batch):
+        n = min(batch, m - r0)
+        win.set_rows(r0, gs.rows(r0, n))
+    win.rebuild()
+    nsteps = args.warmup + args.steps
+    steps_g = torch.empty((nsteps, d), dtype=torch.float32, device=dev)
+    for t in range(nsteps):
+        steps_g[t] = gs.step_row(t)
+    Xq = None
+    if nq:
+        Xq = torch.empty((nsteps, nq, d), dtype=torch.float32, device=dev)
+        for t in range(nsteps):
+            Xq[t] = gs.queries(t, nq)
+    Yq = torch.empty((nq, d), dtype=torch.float32, device=dev) if nq else None
+    y = torch.empty(d, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    assert win.status() == 0
+    log(f"setup {time.perf_counter() - t0:.1f} s (window {win.storage.numel() / 1e9:.1f} GB)")
+
+    def step(t):
+        if nq:
+            win.replace(steps_g[t], y_out=y, X=Xq[t], Y=Yq)
+        else:
+            win.replace(steps_g[t], y_out=y)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    # ---- timed region: K steps, HIP events on the library's stream (torch's current stream)
+    win.trace_read()   # drop any earlier marks
+    win.trace(True)
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for t in range(args.warmup, nsteps):
+        step(t)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    win.trace(False)
+    ms_total = e0.elapsed_time(e1)
+    ph_ms, ph_cnt = win.trace_read()
+    st = win.status()
+    if st != 0:
+        log(f"device error after the timed steps: {P.status_string(st)}")
+        sys.exit(1)
+    log(f"timed {args.steps} steps: {ms_total:.1f} ms (wall {wall * 1e3:.1f} ms)")
+
+    ms_step = ms_total / args.steps
+    b1, b2 = pass_bytes(d, m)
+    if nq:
+        b1 += 4 * nq * d
+        b2 += 4 * 2 * nq * d
+    step_bytes = b1 + b2
+    avg = [ph_ms[i] / max(ph_cnt[i], 1) for i in range(3)]
+    gbs1 = b1 / (avg[0] * 1e-3) / 1e9
+    gbs2 = b2 / (avg[2] * 1e-3) / 1e9
+    dominant = 0 if ph_ms[0] >= ph_ms[2] else 2
+    kname = "k_pass1" if dominant == 0 else "k_pass2"
+    achieved = gbs1 if dominant == 0 else gbs2
+    traffic = read_counters(kname)
+
+    out = {
+        "metric": METRIC,
+        "value": 1000.0 / ms_step,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "d": d, "m": m, "lambda": wl.lam, "queries": nq,
+            "corr_frac": wl.corr_frac,
+            "step": "replace oldest row + Gram row + m x m coefficient refactor + IHVP of the new gradient",
+            "parallelism": "single GPU",
+        },
+        "achieved_hbm_gbs_step": step_bytes / (ms_step * 1e-3) / 1e9,
+        "phases_ms_per_step": {"pass1": avg[0], "coefficients": avg[1], "pass2": avg[2]},
+        "pass_gbs": {"k_pass1": gbs1, "k_pass2": gbs2},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": kname,
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        del steps_g, Xq, win
+        torch.cuda.empty_cache()
+        log("cpu baseline (oracle) ...")
+        t0 = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_sample_div, args.cpu_steps)
+        log(f"cpu baseline took {time.perf_counter() - t0:.1f} s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,206 @@
+/*
+ * mfac.h - C ABI of the MI355X M-FAC IHVP library (gfx950, HIP).
+ *
+ * Matrix-free inverse-Hessian-vector products under the damped empirical
+ * Fisher of a window of m gradients g_1..g_m in R^d (Frantar, Kurtic, Alistarh,
+ * "M-FAC: Efficient Matrix-Free Approximations of Second-Order Information"):
+ *
+ *     F = lambda * I_d + (1/m) * sum_i g_i g_i^T            (Theorem 1)
+ *
+ * Two families of calls:
+ *   - the dynamic sliding window (Section 3.2; optimizer of Section 4.2):
+ *     replace one gradient, refresh the Gram row, recompute the m x m
+ *     coefficients, and return F^-1 applied to the new gradient (and to up to
+ *     max_queries extra vectors in the same two passes over the window);
+ *   - the static block-wise precompute (Section 3.1, block-wise paragraph;
+ *     Appendix C) with the inverse-diagonal query and the OBD keep-mask
+ *     (Section 4.1).
+ *
+ * Conventions for every call:
+ *   - Pointers are HIP device pointers unless marked (host).
+ *   - Vectors of length d are fp32, contiguous, 16-byte aligned; a batch of n
+ *     vectors is n rows of length d with row stride d (row-major).
+ *   - The library never allocates or frees device memory. Window storage,
+ *     workspaces and outputs are owned by the caller and must outlive the
+ *     handle (storage/workspace) or the call's stream work (inputs/outputs).
+ *   - Calls only enqueue work on the handle's stream and return at once; the
+ *     *_status calls and mfac_window_get_rows synchronise that stream.
+ *   - Argument errors are detected on the host before anything is enqueued:
+ *     the call returns MFAC_EINVAL or MFAC_EWORKSPACE and the handle is
+ *     unchanged. A failed HIP launch returns MFAC_EHIP. A non-finite or
+ *     non-positive pivot met on the device latches an error word in the
+ *     workspace, reported as MFAC_ENONFINITE by the next *_status call.
+ *   - A handle is used by one host thread and one stream at a time.
+ */
+#ifndef MFAC_H
+#define MFAC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MFAC_OK = 0,
+    MFAC_EINVAL = -1,      /* invalid argument (null pointer, size, range, alignment) */
+    MFAC_EWORKSPACE = -2,  /* storage or workspace smaller than the *_bytes query   */
+    MFAC_EHIP = -3,        /* a HIP runtime call or kernel launch failed              */
+    MFAC_ENONFINITE = -4,  /* non-finite data or non-positive pivot seen on device    */
+    MFAC_ESTATE = -5       /* call not valid in the handle's current state            */
+} mfac_status;
+
+typedef struct mfac_window_s* mfac_window;
+typedef struct mfac_static_s* mfac_static;
+
+/* Text for a status code (static storage, never NULL). */
+const char* mfac_status_string(mfac_status s);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int32_t mfac_version(void);
+
+/* ======================================================================
+ * Dynamic sliding window (Section 3.2; Appendix B; Section 4.2)
+ * ====================================================================== */
+
+/* Bytes of window storage for an m x d window. The storage holds the m
+ * gradients in a library-chosen layout (column slabs of the window, each slab
+ * m rows x a fixed width, zero padded past d); read rows back with
+ * mfac_window_get_rows. Returns 0 for d < 1 or m < 1. */
+size_t mfac_window_storage_bytes(int64_t d, int32_t m);
+
+/* Bytes of device workspace for the window (Gram matrix and coefficient
+ * factor in fp64, per-call partial sums, error word). max_queries bounds the
+ * n of mfac_window_replace (n extra queries) and mfac_ihvp. Returns 0 on
+ * invalid sizes. */
+size_t mfac_window_workspace_bytes(int64_t d, int32_t m, int32_t max_queries);
+
+/* Create a window handle.
+ *   d >= 1, m >= 1, lambda > 0 finite (kept in fp64: the coefficient phase
+ *   runs in fp64), 0 <= max_queries <= 16,
+ *   m * (max_queries + 1) <= 16384.
+ *   storage:   >= mfac_window_storage_bytes(d, m), 256-byte aligned.
+ *   workspace: >= mfac_window_workspace_bytes(d, m, max_queries), 256-byte aligned.
+ *   G0:        m x d row-major initial gradients, or NULL for an empty window
+ *              (all rows zero; Theorem 1 keeps the 1/m scale for the capacity
+ *              m, so empty slots contribute nothing).
+ * Enqueues: copy of G0 into the storage (or zero fill), Gram K = G G^T
+ * (fp32 MFMA tiles, fp64 reduction), and the coefficient factor. The ring
+ * head starts at slot 0. *out receives a host-allocated handle. */
+mfac_status mfac_window_init(mfac_window* out, int64_t d, int32_t m, double lambda,
+                             int32_t max_queries, void* storage, size_t storage_bytes,
+                             void* workspace, size_t workspace_bytes,
+                             const float* G0, hipStream_t stream);
+
+/* Overwrite rows [first, first+count) of the window with count x d row-major
+ * rows (no Gram update: call mfac_window_rebuild after the last batch). */
+mfac_status mfac_window_set_rows(mfac_window w, int32_t first, int32_t count, const float* rows);
+
+/* Recompute the Gram matrix from the stored rows and refactor the
+ * coefficients (the O(d m^2 + m^3) setup of Section 3.2). Also the recovery
+ * path after a latched non-finite error once the data is fixed. */
+mfac_status mfac_window_rebuild(mfac_window w);
+
+/* The sliding step (Section 3.2 update and multiplication; Appendix B's
+ * combined update-multiply; Section 4.2's optimizer step):
+ *   1. slot k (k = slot, or the ring head if slot == -1) takes g_new;
+ *   2. p = G g_new gives row and column k of the Gram matrix;
+ *   3. the m x m coefficients are refactored from the Gram matrix;
+ *   4. y_out = F^-1 g_new for the window that now holds g_new, evaluated as
+ *      m * G^T (G G^T + m*lambda*I)^-1 e_k (free of the cancellation of the
+ *      direct form lambda^-1 g - G^T c), and Y = F^-1 X for the n extra rows.
+ * X/Y (n x d) are read/written in the same two passes over the window as g.
+ * y_out may be NULL (then only the window is updated); X and Y may be NULL iff
+ * n == 0. g_new, X must not alias the window storage or y_out/Y.
+ * When slot == -1 the ring head advances to (k + 1) mod m. */
+mfac_status mfac_window_replace(mfac_window w, int32_t slot, const float* g_new,
+                                float* y_out, int32_t n, const float* X, float* Y);
+
+/* Y = F^-1 X for n x d row-major X (Section 3.2 multiplication; Algorithm 2's
+ * role): two passes over the window and an O(m^2) solve with the cached
+ * factor. 1 <= n <= max_queries + 1 (the vectors one replace carries). */
+mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* Y);
+
+/* Copy rows [first, first+count) back as count x d row-major fp32 (device
+ * pointer). Synchronises the stream. */
+mfac_status mfac_window_get_rows(mfac_window w, int32_t first, int32_t count, float* rows_out);
+
+/* Current ring head (the slot the next replace with slot == -1 overwrites) and
+ * number of replaces so far (host values; no device access). */
+mfac_status mfac_window_info(mfac_window w, int32_t* head_out /* host */, int64_t* steps_out /* host */);
+
+/* Set the ring head and step count (resume from a checkpoint of the rows). */
+mfac_status mfac_window_set_head(mfac_window w, int32_t head, int64_t steps);
+
+/* Change the stream later calls enqueue on. */
+mfac_status mfac_window_set_stream(mfac_window w, hipStream_t stream);
+
+/* Phase timing with HIP events recorded on the handle's stream (a tracing aid,
+ * off by default). Phases: 0 = pass-1 kernel (G x and the row write),
+ * 1 = coefficient phase (partial-sum reduction, Gram row, factor, solves),
+ * 2 = pass-2 kernel (G^T c). enable != 0 starts recording around every
+ * replace and ihvp; 0 stops (recorded events are kept until read). */
+#define MFAC_NPHASES 3
+mfac_status mfac_window_trace(mfac_window w, int32_t enable);
+
+/* Synchronise the stream, add up the recorded phase times: ms_out and
+ * count_out (host arrays of MFAC_NPHASES) receive milliseconds and launch
+ * counts per phase; the recorded events are then released. */
+mfac_status mfac_window_trace_read(mfac_window w, double* ms_out /* host */, int64_t* count_out /* host */);
+
+/* Synchronise the stream and report (then clear) a latched device error. */
+mfac_status mfac_window_status(mfac_window w);
+
+/* Free the host handle (device buffers stay with the caller). NULL is a no-op. */
+mfac_status mfac_window_destroy(mfac_window w);
+
+/* ======================================================================
+ * Static block-wise precompute (Section 3.1; Appendix C) and OBD queries
+ * (Section 4.1)
+ * ====================================================================== */
+
+/* Bytes of workspace for the static path: per-block fp64 Gram/factor/inverse
+ * buffers for a batch of blocks processed together, plus the fp64 inverse
+ * diagonal (d values). block must divide d. Returns 0 on invalid sizes. */
+size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m);
+
+/* Precompute for the block-wise Fisher: d/B independent blocks, block b
+ * covering columns [bB, (b+1)B) with
+ *     F_b = lambda * I_B + (1/m) G_b^T G_b.
+ * G is the caller's m x d row-major gradient matrix; it is overwritten in
+ * place by W with W_b = R_b^-1 G_b, R_b the Cholesky factor of
+ * G_b G_b^T + m*lambda*I (the same role as the paper's V, which Algorithm 3
+ * also writes over G: V_i = sqrt(q_i / lambda) W_i). The inverse diagonal
+ * diag(F_b^-1) = (1 - sum_i W_b[i,:]^2) / lambda is formed in fp64 from the
+ * unrounded W and kept in the workspace.
+ * Requirements: 1 <= m, 1 <= block, block % 4 == 0, d % block == 0,
+ * lambda > 0 finite. */
+mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m,
+                                   double lambda, float* G, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/* diag(F^-1) for all d coordinates (Appendix C, row-selected extraction with
+ * the identity selection), rounded to fp32. */
+mfac_status mfac_inv_diag(mfac_static s, float* diag_out);
+
+/* Same, in fp64. */
+mfac_status mfac_inv_diag64(mfac_static s, double* diag_out);
+
+/* OBD saliency rho_j = theta_j^2 / (2 [F^-1]_jj) in fp64 (Section 4.1) and a
+ * global keep-mask over all blocks: keep_mask[j] = 1 for the `keep` largest
+ * rho, ties broken by the lower index; 0 <= keep <= d. scores_out may be
+ * NULL. Uses workspace scratch; output is exact given the fp64 diagonal. */
+mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t keep,
+                          double* scores_out, uint8_t* keep_mask_out);
+
+mfac_status mfac_static_set_stream(mfac_static s, hipStream_t stream);
+mfac_status mfac_static_status(mfac_static s);
+mfac_status mfac_static_destroy(mfac_static s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MFAC_H */

@@ -1,0 +1,545 @@
+// C ABI of libmfac (include/mfac.h): host-side validation, workspace layout
+// and the launch sequences of the dynamic and static paths. Nothing here
+// computes on the host; every step of the method runs in the kernels of
+// pass.hip, gram.hip, chol.hip and static.hip.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "../../include/mfac.h"
+#include "internal.h"
+
+#define MFAC_API extern "C" __attribute__((visibility("default")))
+
+using namespace mfac;
+
+namespace {
+
+constexpr int MAX_QUERIES = 16;
+constexpr int64_t MAX_MNV = 16384;  // m * (max_queries + 1), bounds the pass-1 LDS (64 KB)
+constexpr int64_t STATIC_BATCH_BYTES = int64_t(4) << 30;
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Carve {
+    char* base;
+    size_t off = 0;
+    template <typename T>
+    T* take(size_t count) {
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off += align256(count * sizeof(T));
+        return p;
+    }
+};
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool aligned4(const void* p) { return ((uintptr_t)p & 3u) == 0; }
+
+int64_t nslab_of(int64_t d) { return ceil_div(d, SLAB); }
+int padded_m(int m) { return (int)round_up(m, NB); }
+
+}  // namespace
+
+struct mfac_window_s {
+    int64_t d;
+    int m, mp, max_q;
+    double lambda;
+    int64_t nslab;
+    float* G;
+    hipStream_t st;
+    int* err;
+    double *K, *A, *Linv, *part, *p, *R, *U, *work, *gpart;
+    float* coef;
+    int head;
+    int64_t steps;
+    // phase tracing (host side): events recorded around the phases
+    bool trace;
+    struct Mark {
+        int phase;
+        hipEvent_t a, b;
+    };
+    std::vector<Mark>* marks;
+    hipEvent_t open_ev;
+};
+
+struct mfac_static_s {
+    int64_t d;
+    int B, m, mp, nblocks, batch;
+    double lambda;
+    float* G;
+    hipStream_t st;
+    int* err;
+    double *A, *Linv, *diag, *scores;
+    SelectScratch sel;
+};
+
+namespace {
+
+template <typename W>
+size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
+    const int mp = padded_m(m);
+    const int nvmax = 1 + max_q;
+    Carve c{base};
+    int* err = c.take<int>(64);
+    double* K = c.take<double>((size_t)m * m);
+    double* A = c.take<double>((size_t)mp * mp);
+    double* Linv = c.take<double>((size_t)mp * mp);
+    double* part = c.take<double>((size_t)PASS1_MAX_GRID * m * nvmax);
+    double* p = c.take<double>((size_t)m * nvmax);
+    double* R = c.take<double>((size_t)mp * nvmax);
+    double* U = c.take<double>((size_t)mp * nvmax);
+    double* work = c.take<double>((size_t)mp * nvmax);
+    float* coef = c.take<float>((size_t)m * nvmax);
+    double* gpart = c.take<double>((size_t)gram_window_part_doubles(m, nslab_of(d)));
+    if (w) {
+        w->err = err;
+        w->K = K;
+        w->A = A;
+        w->Linv = Linv;
+        w->part = part;
+        w->p = p;
+        w->R = R;
+        w->U = U;
+        w->work = work;
+        w->coef = coef;
+        w->gpart = gpart;
+    }
+    return c.off;
+}
+
+bool window_sizes_ok(int64_t d, int32_t m, int32_t max_q) {
+    return d >= 1 && m >= 1 && max_q >= 0 && max_q <= MAX_QUERIES && (int64_t)m * (max_q + 1) <= MAX_MNV &&
+           d <= (int64_t(1) << 40);
+}
+
+#define HIPCHK(x)                                  \
+    do {                                           \
+        hipError_t e_ = (x);                       \
+        if (e_ != hipSuccess) return MFAC_EHIP;    \
+    } while (0)
+
+// Tracing: mark_begin before a phase's first launch, mark_end after its last.
+hipError_t mark_begin(mfac_window w) {
+    if (!w->trace) return hipSuccess;
+    hipError_t e = hipEventCreate(&w->open_ev);
+    if (e != hipSuccess) return e;
+    return hipEventRecord(w->open_ev, w->st);
+}
+
+hipError_t mark_end(mfac_window w, int phase) {
+    if (!w->trace) return hipSuccess;
+    hipEvent_t b;
+    hipError_t e = hipEventCreate(&b);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, w->st);
+    w->marks->push_back({phase, w->open_ev, b});
+    return e;
+}
+
+mfac_status window_factor(mfac_window w, const double* p, int pstride, int k) {
+    HIPCHK(launch_assemble(w->K, w->m, p, pstride, k, (double)w->m * w->lambda, w->A, w->mp, w->err, w->st));
+    HIPCHK(launch_potrf(w->A, w->Linv, w->mp, 1, 0, w->err, w->st));
+    return MFAC_OK;
+}
+
+}  // namespace
+
+// ====================================================================== misc
+
+MFAC_API const char* mfac_status_string(mfac_status s) {
+    switch (s) {
+        case MFAC_OK: return "ok";
+        case MFAC_EINVAL: return "invalid argument";
+        case MFAC_EWORKSPACE: return "storage or workspace too small";
+        case MFAC_EHIP: return "HIP runtime or launch failure";
+        case MFAC_ENONFINITE: return "non-finite value or non-positive pivot on device";
+        case MFAC_ESTATE: return "call not valid in the current state";
+    }
+    return "unknown status";
+}
+
+MFAC_API int32_t mfac_version(void) { return 100; }
+
+// ====================================================================== window
+
+MFAC_API size_t mfac_window_storage_bytes(int64_t d, int32_t m) {
+    if (d < 1 || m < 1) return 0;
+    return (size_t)nslab_of(d) * (size_t)m * SLAB * sizeof(float);
+}
+
+MFAC_API size_t mfac_window_workspace_bytes(int64_t d, int32_t m, int32_t max_queries) {
+    if (!window_sizes_ok(d, m, max_queries)) return 0;
+    return window_layout<mfac_window_s>(d, m, max_queries, nullptr, nullptr);
+}
+
+MFAC_API mfac_status mfac_window_init(mfac_window* out, int64_t d, int32_t m, double lambda, int32_t max_queries,
+                                      void* storage, size_t storage_bytes, void* workspace, size_t workspace_bytes,
+                                      const float* G0, hipStream_t stream) {
+    if (!out) return MFAC_EINVAL;
+    *out = nullptr;
+    if (!window_sizes_ok(d, m, max_queries)) return MFAC_EINVAL;
+    if (!(lambda > 0.0) || !isfinite(lambda)) return MFAC_EINVAL;
+    if (!storage || !workspace) return MFAC_EINVAL;
+    if (((uintptr_t)storage & 255u) || ((uintptr_t)workspace & 255u)) return MFAC_EINVAL;
+    if (G0 && !aligned4(G0)) return MFAC_EINVAL;
+    if (storage_bytes < mfac_window_storage_bytes(d, m)) return MFAC_EWORKSPACE;
+    if (workspace_bytes < mfac_window_workspace_bytes(d, m, max_queries)) return MFAC_EWORKSPACE;
+
+    mfac_window w = (mfac_window)calloc(1, sizeof(mfac_window_s));
+    if (!w) return MFAC_EINVAL;
+    w->d = d;
+    w->m = m;
+    w->mp = padded_m(m);
+    w->max_q = max_queries;
+    w->lambda = lambda;
+    w->nslab = nslab_of(d);
+    w->G = (float*)storage;
+    w->st = stream;
+    window_layout<mfac_window_s>(d, m, max_queries, (char*)workspace, w);
+
+    mfac_status rc = MFAC_OK;
+    if (launch_fill_zero((float*)w->err, 1, w->st) != hipSuccess) rc = MFAC_EHIP;
+    if (rc == MFAC_OK) {
+        hipError_t e = G0 ? launch_set_rows(w->G, m, d, w->nslab, 0, m, G0, d, w->st)
+                          : launch_fill_zero(w->G, w->nslab * (int64_t)m * SLAB, w->st);
+        if (e != hipSuccess) rc = MFAC_EHIP;
+    }
+    if (rc == MFAC_OK) rc = mfac_window_rebuild(w);
+    if (rc != MFAC_OK) {
+        free(w);
+        return rc;
+    }
+    *out = w;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_set_rows(mfac_window w, int32_t first, int32_t count, const float* rows) {
+    if (!w || !rows || first < 0 || count < 1 || (int64_t)first + count > w->m || !aligned4(rows)) return MFAC_EINVAL;
+    HIPCHK(launch_set_rows(w->G, w->m, w->d, w->nslab, first, count, rows, w->d, w->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_rebuild(mfac_window w) {
+    if (!w) return MFAC_EINVAL;
+    HIPCHK(launch_gram_window(w->G, w->m, w->nslab, w->gpart, w->K, w->st));
+    return window_factor(w, nullptr, 0, -1);
+}
+
+MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const float* g_new, float* y_out, int32_t n,
+                                         const float* X, float* Y) {
+    if (!w || !g_new) return MFAC_EINVAL;
+    if (slot < -1 || slot >= w->m) return MFAC_EINVAL;
+    if (n < 0 || n > w->max_q) return MFAC_EINVAL;
+    if (n > 0 && (!X || !Y)) return MFAC_EINVAL;
+    if (!aligned4(g_new) || (y_out && !aligned4(y_out)) || (n > 0 && (!aligned4(X) || !aligned4(Y))))
+        return MFAC_EINVAL;
+    const int k = slot < 0 ? w->head : slot;
+    const int nv = 1 + n;
+    const int64_t d = w->d;
+
+    VecIn vin{};
+    vin.v[0] = g_new;
+    bool al = aligned16(g_new) && (y_out == nullptr || aligned16(y_out));
+    for (int q = 0; q < n; ++q) vin.v[1 + q] = X + (int64_t)q * d;
+    if (n > 0) al = al && aligned16(X) && aligned16(Y) && (d % 4 == 0);
+
+    int grid = 0;
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, nv, vin, al, w->G, k, w->part, &grid, w->st));
+    HIPCHK(mark_end(w, 0));
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_reduce_partials(w->part, grid, w->m * nv, w->p, w->st));
+    mfac_status rc = window_factor(w, w->p, nv, k);
+    if (rc != MFAC_OK) return rc;
+
+    if (y_out || n > 0) {
+        HIPCHK(launch_build_rhs(w->p, w->m, nv, k, w->R, w->mp, w->st));
+        HIPCHK(launch_chol_solve(w->A, w->Linv, w->mp, nv, w->R, w->U, w->work, w->st));
+        // column 0: c' = -m A^-1 e_k, so y = -G^T c' = m G^T A^-1 e_k;
+        // queries: C = lambda^-1 A^-1 P, y = x / lambda - G^T C
+        const double inv_lam = 1.0 / w->lambda;
+        VecOut vout{};
+        int v0 = 0;
+        if (!y_out) v0 = 1;  // skip the inserted-gradient column
+        int nv2 = 0;
+        for (int v = v0; v < nv; ++v, ++nv2) {
+            vout.x[nv2] = v == 0 ? nullptr : X + (int64_t)(v - 1) * d;
+            vout.y[nv2] = v == 0 ? y_out : Y + (int64_t)(v - 1) * d;
+            vout.alpha[nv2] = v == 0 ? 0.0f : (float)inv_lam;
+        }
+        if (v0 == 0) {
+            HIPCHK(launch_coef(w->U, w->m, w->mp, nv, -(double)w->m, inv_lam, w->coef, w->err, w->st));
+        } else {
+            // no y_out: coefficients of the queries only (columns 1..n of U)
+            HIPCHK(launch_coef(w->U + w->mp, w->m, w->mp, nv2, inv_lam, inv_lam, w->coef, w->err, w->st));
+        }
+        HIPCHK(mark_end(w, 1));
+        HIPCHK(mark_begin(w));
+        HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, nv2, w->coef, vout, al, w->st));
+        HIPCHK(mark_end(w, 2));
+    } else {
+        HIPCHK(mark_end(w, 1));
+    }
+    if (slot < 0) w->head = (k + 1) % w->m;
+    w->steps += 1;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* Y) {
+    if (!w || !X || !Y) return MFAC_EINVAL;
+    if (n < 1 || n > w->max_q + 1) return MFAC_EINVAL;
+    if (!aligned4(X) || !aligned4(Y)) return MFAC_EINVAL;
+    const int64_t d = w->d;
+    const bool al = aligned16(X) && aligned16(Y) && (n == 1 || d % 4 == 0);
+    VecIn vin{};
+    VecOut vout{};
+    const double inv_lam = 1.0 / w->lambda;
+    for (int q = 0; q < n; ++q) {
+        vin.v[q] = X + (int64_t)q * d;
+        vout.x[q] = X + (int64_t)q * d;
+        vout.y[q] = Y + (int64_t)q * d;
+        vout.alpha[q] = (float)inv_lam;
+    }
+    int grid = 0;
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, n, vin, al, nullptr, -1, w->part, &grid, w->st));
+    HIPCHK(mark_end(w, 0));
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_reduce_partials(w->part, grid, w->m * n, w->p, w->st));
+    HIPCHK(launch_build_rhs(w->p, w->m, n, -1, w->R, w->mp, w->st));
+    HIPCHK(launch_chol_solve(w->A, w->Linv, w->mp, n, w->R, w->U, w->work, w->st));
+    HIPCHK(launch_coef(w->U, w->m, w->mp, n, inv_lam, inv_lam, w->coef, w->err, w->st));
+    HIPCHK(mark_end(w, 1));
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, n, w->coef, vout, al, w->st));
+    HIPCHK(mark_end(w, 2));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_get_rows(mfac_window w, int32_t first, int32_t count, float* rows_out) {
+    if (!w || !rows_out || first < 0 || count < 1 || (int64_t)first + count > w->m || !aligned4(rows_out))
+        return MFAC_EINVAL;
+    HIPCHK(launch_get_rows(w->G, w->m, w->d, first, count, rows_out, w->d, w->st));
+    HIPCHK(hipStreamSynchronize(w->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_info(mfac_window w, int32_t* head_out, int64_t* steps_out) {
+    if (!w) return MFAC_EINVAL;
+    if (head_out) *head_out = w->head;
+    if (steps_out) *steps_out = w->steps;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_set_head(mfac_window w, int32_t head, int64_t steps) {
+    if (!w || head < 0 || head >= w->m || steps < 0) return MFAC_EINVAL;
+    w->head = head;
+    w->steps = steps;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_set_stream(mfac_window w, hipStream_t stream) {
+    if (!w) return MFAC_EINVAL;
+    w->st = stream;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_trace(mfac_window w, int32_t enable) {
+    if (!w) return MFAC_EINVAL;
+    if (enable && !w->marks) w->marks = new std::vector<mfac_window_s::Mark>();
+    w->trace = enable != 0;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_trace_read(mfac_window w, double* ms_out, int64_t* count_out) {
+    if (!w || !ms_out || !count_out) return MFAC_EINVAL;
+    for (int i = 0; i < MFAC_NPHASES; ++i) {
+        ms_out[i] = 0.0;
+        count_out[i] = 0;
+    }
+    if (!w->marks) return MFAC_OK;
+    HIPCHK(hipStreamSynchronize(w->st));
+    mfac_status rc = MFAC_OK;
+    for (auto& mk : *w->marks) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, mk.a, mk.b) != hipSuccess) rc = MFAC_EHIP;
+        ms_out[mk.phase] += ms;
+        count_out[mk.phase] += 1;
+        (void)hipEventDestroy(mk.a);
+        (void)hipEventDestroy(mk.b);
+    }
+    w->marks->clear();
+    return rc;
+}
+
+MFAC_API mfac_status mfac_window_status(mfac_window w) {
+    if (!w) return MFAC_EINVAL;
+    HIPCHK(hipStreamSynchronize(w->st));
+    int e = 0;
+    HIPCHK(hipMemcpy(&e, w->err, sizeof(int), hipMemcpyDeviceToHost));
+    if (e != 0) {
+        HIPCHK(launch_fill_zero((float*)w->err, 1, w->st));
+        HIPCHK(hipStreamSynchronize(w->st));
+        return MFAC_ENONFINITE;
+    }
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_destroy(mfac_window w) {
+    if (!w) return MFAC_OK;
+    if (w->marks) {
+        for (auto& mk : *w->marks) {
+            (void)hipEventDestroy(mk.a);
+            (void)hipEventDestroy(mk.b);
+        }
+        delete w->marks;
+    }
+    free(w);
+    return MFAC_OK;
+}
+
+// ====================================================================== static
+
+namespace {
+
+bool static_sizes_ok(int64_t d, int32_t B, int32_t m) {
+    return d >= 1 && B >= 4 && m >= 1 && (B % 4) == 0 && d % B == 0 && m <= 8192 && d <= (int64_t(1) << 40) &&
+           d / B <= (int64_t(1) << 30);
+}
+
+int static_batch(int64_t d, int B, int m) {
+    const int mp = padded_m(m);
+    const int64_t nblocks = d / B;
+    const int64_t per = (int64_t)mp * mp * 8 * 2;
+    int64_t b = STATIC_BATCH_BYTES / per;
+    // MFAC_STATIC_BATCH_BLOCKS caps the blocks processed per batch (tests use it
+    // to cover batch boundaries at small sizes); read by both the workspace
+    // query and the precompute, so keep it fixed between the two calls.
+    if (const char* env = getenv("MFAC_STATIC_BATCH_BLOCKS")) {
+        const long cap = strtol(env, nullptr, 10);
+        if (cap > 0 && cap < b) b = cap;
+    }
+    if (b < 1) b = 1;
+    if (b > 65535) b = 65535;
+    if (b > nblocks) b = nblocks;
+    return (int)b;
+}
+
+template <typename S>
+size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
+    const int mp = padded_m(m);
+    const int batch = static_batch(d, B, m);
+    Carve c{base};
+    int* err = c.take<int>(64);
+    double* diag = c.take<double>((size_t)d);
+    double* scores = c.take<double>((size_t)d);
+    char* sel = c.take<char>((size_t)select_scratch_bytes(d));
+    double* A = c.take<double>((size_t)batch * mp * mp);
+    double* Linv = c.take<double>((size_t)batch * mp * mp);
+    if (s) {
+        s->err = err;
+        s->diag = diag;
+        s->scores = scores;
+        s->sel = select_scratch_carve(sel, d);
+        s->A = A;
+        s->Linv = Linv;
+        s->batch = batch;
+    }
+    return c.off;
+}
+
+}  // namespace
+
+MFAC_API size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m) {
+    if (!static_sizes_ok(d, block, m)) return 0;
+    return static_layout<mfac_static_s>(d, block, m, nullptr, nullptr);
+}
+
+MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m, double lambda,
+                                            float* G, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!out) return MFAC_EINVAL;
+    *out = nullptr;
+    if (!static_sizes_ok(d, block, m)) return MFAC_EINVAL;
+    if (!(lambda > 0.0) || !isfinite(lambda)) return MFAC_EINVAL;
+    if (!G || !workspace || !aligned16(G) || ((uintptr_t)workspace & 255u)) return MFAC_EINVAL;
+    if (workspace_bytes < mfac_static_workspace_bytes(d, block, m)) return MFAC_EWORKSPACE;
+
+    mfac_static s = (mfac_static)calloc(1, sizeof(mfac_static_s));
+    if (!s) return MFAC_EINVAL;
+    s->d = d;
+    s->B = block;
+    s->m = m;
+    s->mp = padded_m(m);
+    s->nblocks = (int)(d / block);
+    s->lambda = lambda;
+    s->G = G;
+    s->st = stream;
+    static_layout<mfac_static_s>(d, block, m, (char*)workspace, s);
+
+    const int64_t bstride = (int64_t)s->mp * s->mp;
+    const double mu = (double)m * lambda;
+    auto fail = [&]() {
+        free(s);
+        return MFAC_EHIP;
+    };
+    if (launch_fill_zero((float*)s->err, 1, s->st) != hipSuccess) return fail();
+    for (int b0 = 0; b0 < s->nblocks; b0 += s->batch) {
+        const int nb = (s->nblocks - b0) < s->batch ? (s->nblocks - b0) : s->batch;
+        if (launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->st) != hipSuccess) return fail();
+        if (launch_potrf(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st) != hipSuccess) return fail();
+        if (launch_trtri(s->A, s->Linv, s->mp, nb, bstride, s->st) != hipSuccess) return fail();
+        if (launch_trmm_diag(s->Linv, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, s->st) !=
+            hipSuccess)
+            return fail();
+    }
+    *out = s;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_inv_diag(mfac_static s, float* diag_out) {
+    if (!s || !diag_out || !aligned4(diag_out)) return MFAC_EINVAL;
+    HIPCHK(launch_diag_to_f32(s->diag, s->d, diag_out, s->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_inv_diag64(mfac_static s, double* diag_out) {
+    if (!s || !diag_out || ((uintptr_t)diag_out & 7u)) return MFAC_EINVAL;
+    HIPCHK(hipMemcpyAsync(diag_out, s->diag, (size_t)s->d * sizeof(double), hipMemcpyDeviceToDevice, s->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t keep, double* scores_out,
+                                   uint8_t* keep_mask_out) {
+    if (!s || !theta || !keep_mask_out || keep < 0 || keep > s->d || !aligned4(theta)) return MFAC_EINVAL;
+    if (scores_out && ((uintptr_t)scores_out & 7u)) return MFAC_EINVAL;
+    double* sc = scores_out ? scores_out : s->scores;
+    HIPCHK(launch_scores(theta, s->diag, s->d, sc, s->err, s->st));
+    HIPCHK(launch_topk_mask(sc, s->d, keep, s->sel, keep_mask_out, s->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_static_set_stream(mfac_static s, hipStream_t stream) {
+    if (!s) return MFAC_EINVAL;
+    s->st = stream;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_static_status(mfac_static s) {
+    if (!s) return MFAC_EINVAL;
+    HIPCHK(hipStreamSynchronize(s->st));
+    int e = 0;
+    HIPCHK(hipMemcpy(&e, s->err, sizeof(int), hipMemcpyDeviceToHost));
+    if (e != 0) {
+        HIPCHK(launch_fill_zero((float*)s->err, 1, s->st));
+        HIPCHK(hipStreamSynchronize(s->st));
+        return MFAC_ENONFINITE;
+    }
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_static_destroy(mfac_static s) {
+    free(s);
+    return MFAC_OK;
+}

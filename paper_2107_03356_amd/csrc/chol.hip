@@ -1,0 +1,391 @@
+// The m x m coefficient phase, in fp64.
+//
+// The paper's D (Section 3.2) is the upper LU factor, without pivoting, of
+// K/lambda + m I minus m I (Appendix B); equivalently D and B come from the
+// Cholesky factor R of A = K + m*lambda*I: A = lambda * Ru Ru^T with
+// D = diag(Ru) Ru^T - m I and B = lambda^-1 (Ru diag(Ru)^-1)^-1. The
+// coefficients of Theorem 1 are then c = lambda^-1 A^-1 G x. This file keeps
+// that factor explicitly: a blocked right-looking Cholesky of A in NB = 64
+// tiles (the paper's remark that a modified Cholesky kernel would beat its
+// LU), the inverses of the diagonal tiles, optionally the full L^-1, and
+// blocked triangular solves. A is padded to a multiple of 64 with an
+// identity block so no kernel needs edge handling.
+//
+// Dense 64 x 64 x 64 tile products run on fp64 MFMA (v_mfma_f64_16x16x4f64):
+// 4 waves, each a 32 x 32 quadrant of 2 x 2 16x16 tiles, operands from LDS.
+// All products are written as C[r][c] = sum_k a[r][k] * b[c][k]; a tile that
+// enters as b[k][c] is transposed while it is staged.
+#include "internal.h"
+
+namespace mfac {
+namespace {
+
+typedef double v4d __attribute__((ext_vector_type(4)));
+constexpr int P = 68;  // LDS pitch of a 64 x 64 fp64 tile
+
+__device__ __forceinline__ void stage_tile(double (*S)[P], const double* __restrict__ src, int64_t ld) {
+    for (int e = threadIdx.x; e < 64 * 16; e += blockDim.x) {
+        const int r = e >> 4, c = (e & 15) * 4;
+        const double* s = src + (int64_t)r * ld + c;
+        S[r][c] = s[0];
+        S[r][c + 1] = s[1];
+        S[r][c + 2] = s[2];
+        S[r][c + 3] = s[3];
+    }
+}
+
+__device__ __forceinline__ void stage_tile_t(double (*S)[P], const double* __restrict__ src, int64_t ld) {
+    for (int e = threadIdx.x; e < 64 * 64; e += blockDim.x) {
+        const int r = e >> 6, c = e & 63;
+        S[c][r] = src[(int64_t)r * ld + c];
+    }
+}
+
+__device__ __forceinline__ void zero_acc(v4d (&acc)[2][2]) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
+}
+
+// acc += a * b^T over k in [0, 64) for this wave's quadrant (256 threads).
+__device__ __forceinline__ void mma_nt(const double (*a)[P], const double (*b)[P], v4d (&acc)[2][2]) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int rl = lane & 15, kl = lane >> 4;
+#pragma unroll 4
+    for (int kk = 0; kk < 16; ++kk) {
+        double av[2], bv[2];
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            av[s] = a[wr * 32 + s * 16 + rl][kk * 4 + kl];
+            bv[s] = b[wc * 32 + s * 16 + rl][kk * 4 + kl];
+        }
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y)
+                acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+    }
+}
+
+// Visit this thread's accumulator entries: f(row, col, value). In the fp64
+// 16x16x4 MFMA result, lane l register r holds row (l/16) + 4r, column l%16.
+template <typename F>
+__device__ __forceinline__ void for_acc(v4d (&acc)[2][2], F f) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int rl = lane & 15, kl = lane >> 4;
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) f(wr * 32 + x * 16 + kl + 4 * r, wc * 32 + y * 16 + rl, acc[x][y][r]);
+}
+
+// ------------------------------------------------------------------ assemble
+__global__ __launch_bounds__(256) void k_assemble(double* __restrict__ K, int m,
+                                                  const double* __restrict__ p, int pstride, int k,
+                                                  double mu, double* __restrict__ A, int mp,
+                                                  int* __restrict__ err) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= (int64_t)mp * mp) return;
+    const int i = (int)(e / mp), j = (int)(e % mp);
+    double v;
+    if (i < m && j < m) {
+        if (k >= 0 && i == k)
+            v = p[(int64_t)j * pstride];
+        else if (k >= 0 && j == k)
+            v = p[(int64_t)i * pstride];
+        else
+            v = K[(int64_t)i * m + j];
+        if (k >= 0 && i == k) {
+            K[(int64_t)k * m + j] = v;
+            K[(int64_t)j * m + k] = v;
+            if (!isfinite(v)) atomicOr(err, 1);
+        }
+        if (i == j) v += mu;
+    } else {
+        v = (i == j) ? 1.0 : 0.0;
+    }
+    A[e] = v;
+}
+
+// ------------------------------------------------------------------ potrf
+// One 64-thread wave per batch item: factor diagonal tile t in place (lower)
+// and write its inverse into the diagonal tile of Linv.
+__global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, double* __restrict__ Linv,
+                                                   int mp, int64_t bstride, int t, int* __restrict__ err) {
+    __shared__ double T[64][65];
+    __shared__ double I[64][65];
+    double* Ab = A + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
+    double* Lb = Linv + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
+    const int i = threadIdx.x;
+    for (int c = 0; c < 64; ++c) T[i][c] = Ab[(int64_t)i * mp + c];
+    __syncthreads();
+    int bad = 0;
+    for (int j = 0; j < 64; ++j) {
+        if (i == j) {
+            double piv = T[j][j];
+            if (!(piv > 0.0) || !isfinite(piv)) {
+                bad = 1;
+                piv = 1.0;
+            }
+            T[j][j] = sqrt(piv);
+        }
+        __syncthreads();
+        const double djj = T[j][j];
+        if (i > j) T[i][j] /= djj;
+        __syncthreads();
+        if (i > j) {
+            const double lij = T[i][j];
+            for (int c = j + 1; c <= i; ++c) T[i][c] -= lij * T[c][j];
+        }
+        __syncthreads();
+    }
+    if (bad) atomicOr(err, 2);
+    // column i of the inverse of the lower factor, by forward substitution
+    for (int r = 0; r < 64; ++r) I[r][i] = 0.0;
+    {
+        const int c = i;
+        I[c][c] = 1.0 / T[c][c];
+        for (int r = c + 1; r < 64; ++r) {
+            double s = 0.0;
+            for (int l = c; l < r; ++l) s += T[r][l] * I[l][c];
+            I[r][c] = -s / T[r][r];
+        }
+    }
+    __syncthreads();
+    for (int c = 0; c < 64; ++c) {
+        Ab[(int64_t)i * mp + c] = (c <= i) ? T[i][c] : 0.0;
+        Lb[(int64_t)i * mp + c] = I[i][c];
+    }
+}
+
+// Panel: A[r,t] <- A[r,t] * Linv[t,t]^T for r > t. grid (T-1-t, nbatch).
+__global__ __launch_bounds__(256) void k_trsm_panel(double* __restrict__ A, const double* __restrict__ Linv,
+                                                    int mp, int64_t bstride, int t) {
+    __shared__ double Sa[64][P];
+    __shared__ double Sb[64][P];
+    const int r = t + 1 + blockIdx.x;
+    double* Ab = A + (int64_t)blockIdx.y * bstride;
+    const double* Lb = Linv + (int64_t)blockIdx.y * bstride;
+    double* Art = Ab + (int64_t)r * 64 * mp + t * 64;
+    stage_tile(Sa, Art, mp);
+    stage_tile(Sb, Lb + (int64_t)t * 64 * mp + t * 64, mp);
+    __syncthreads();
+    v4d acc[2][2];
+    zero_acc(acc);
+    mma_nt(Sa, Sb, acc);
+    for_acc(acc, [&](int row, int col, double v) { Art[(int64_t)row * mp + col] = v; });
+}
+
+// Trailing update: A[r,s] -= A[r,t] A[s,t]^T for t < s <= r. grid (npairs, nbatch).
+__global__ __launch_bounds__(256) void k_syrk_update(double* __restrict__ A, int mp, int64_t bstride, int t) {
+    __shared__ double Sa[64][P];
+    __shared__ double Sb[64][P];
+    // pair index -> (r, s) over the lower triangle of the trailing tiles
+    const int idx = blockIdx.x;
+    int rr = (int)((sqrtf(8.0f * (float)idx + 1.0f) - 1.0f) * 0.5f);
+    while ((rr + 1) * (rr + 2) / 2 <= idx) ++rr;
+    while (rr * (rr + 1) / 2 > idx) --rr;
+    const int ss = idx - rr * (rr + 1) / 2;
+    const int r = t + 1 + rr, s = t + 1 + ss;
+    double* Ab = A + (int64_t)blockIdx.y * bstride;
+    stage_tile(Sa, Ab + (int64_t)r * 64 * mp + t * 64, mp);
+    if (r != s) stage_tile(Sb, Ab + (int64_t)s * 64 * mp + t * 64, mp);
+    __syncthreads();
+    v4d acc[2][2];
+    zero_acc(acc);
+    mma_nt(Sa, r != s ? Sb : Sa, acc);
+    double* C = Ab + (int64_t)r * 64 * mp + s * 64;
+    for_acc(acc, [&](int row, int col, double v) { C[(int64_t)row * mp + col] -= v; });
+}
+
+// ------------------------------------------------------------------ trtri
+// Linv[i,j] = -Linv[i,i] * sum_{k=j}^{i-1} L[i,k] Linv[k,j], i = j + step.
+// grid (T - step, nbatch).
+__global__ __launch_bounds__(256) void k_trtri_step(const double* __restrict__ L, double* __restrict__ Linv,
+                                                    int mp, int64_t bstride, int step) {
+    __shared__ double Sa[64][P];
+    __shared__ double Sb[64][P];
+    const int j = blockIdx.x, i = j + step;
+    const double* Lb = L + (int64_t)blockIdx.y * bstride;
+    double* Ib = Linv + (int64_t)blockIdx.y * bstride;
+    v4d acc[2][2];
+    zero_acc(acc);
+    for (int k = j; k < i; ++k) {
+        stage_tile(Sa, Lb + (int64_t)i * 64 * mp + k * 64, mp);
+        stage_tile_t(Sb, Ib + (int64_t)k * 64 * mp + j * 64, mp);
+        __syncthreads();
+        mma_nt(Sa, Sb, acc);
+        __syncthreads();
+    }
+    // X = acc; stage X^T into Sb, Linv[i,i] into Sa, then -Linv[i,i] X
+    for_acc(acc, [&](int row, int col, double v) { Sb[col][row] = v; });
+    stage_tile(Sa, Ib + (int64_t)i * 64 * mp + i * 64, mp);
+    __syncthreads();
+    zero_acc(acc);
+    mma_nt(Sa, Sb, acc);
+    double* C = Ib + (int64_t)i * 64 * mp + j * 64;
+    for_acc(acc, [&](int row, int col, double v) { C[(int64_t)row * mp + col] = -v; });
+}
+
+__global__ __launch_bounds__(256) void k_zero_upper(double* __restrict__ Linv, int mp, int64_t bstride) {
+    // zero the strictly-upper tiles of Linv (tile (i, j) with j > i); grid (T*T, nbatch)
+    const int T = mp / 64;
+    const int ti = blockIdx.x / T, tj = blockIdx.x % T;
+    if (tj <= ti) return;
+    double* C = Linv + (int64_t)blockIdx.y * bstride + (int64_t)ti * 64 * mp + tj * 64;
+    for (int e = threadIdx.x; e < 4096; e += 256) C[(int64_t)(e >> 6) * mp + (e & 63)] = 0.0;
+}
+
+// ------------------------------------------------------------------ solves
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+// One work-group per right-hand side: U[:,c] = (L L^T)^-1 R[:,c].
+// Forward z = L^-1 r by tile rows (wave per row of the off-diagonal
+// product, lanes along the row), then backward u = L^-T z by tile columns
+// (lanes along columns). Diagonal tiles use the stored inverses.
+__global__ __launch_bounds__(256) void k_chol_solve(const double* __restrict__ L,
+                                                    const double* __restrict__ Linv, int mp,
+                                                    const double* __restrict__ R, double* __restrict__ U,
+                                                    double* __restrict__ work) {
+    __shared__ double v[64];
+    __shared__ double part[4][64];
+    const int c = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int T = mp / 64;
+    const double* r = R + (int64_t)c * mp;
+    double* z = work + (int64_t)c * mp;
+    double* u = U + (int64_t)c * mp;
+
+    for (int t = 0; t < T; ++t) {
+        // v = r_t - L[t, <t] z_<t
+        for (int rr = wave; rr < 64; rr += 4) {
+            const int row = t * 64 + rr;
+            double s = 0.0;
+            for (int k = lane; k < t * 64; k += 64) s += L[(int64_t)row * mp + k] * z[k];
+            s = wave_sum_d(s);
+            if (lane == 0) v[rr] = r[row] - s;
+        }
+        __syncthreads();
+        // z_t = Linv[t,t] v
+        for (int rr = wave; rr < 64; rr += 4) {
+            const int row = t * 64 + rr;
+            double s = Linv[(int64_t)row * mp + t * 64 + lane] * v[lane];
+            s = wave_sum_d(s);
+            if (lane == 0) z[row] = s;
+        }
+        __threadfence_block();
+        __syncthreads();
+    }
+    for (int t = T - 1; t >= 0; --t) {
+        // w = z_t - L[>t, t]^T u_>t   (lanes over the 64 columns of tile column t)
+        double s = 0.0;
+        for (int row = (t + 1) * 64 + wave; row < mp; row += 4) s += L[(int64_t)row * mp + t * 64 + lane] * u[row];
+        part[wave][lane] = s;
+        __syncthreads();
+        if (wave == 0) v[lane] = z[t * 64 + lane] - (part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane]);
+        __syncthreads();
+        // u_t = Linv[t,t]^T w
+        if (wave == 0) {
+            double a = 0.0;
+            for (int k = 0; k < 64; ++k) a += Linv[(int64_t)(t * 64 + k) * mp + t * 64 + lane] * v[k];
+            u[t * 64 + lane] = a;
+        }
+        __threadfence_block();
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(256) void k_build_rhs(const double* __restrict__ p, int m, int nv, int k,
+                                                   double* __restrict__ R, int mp) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= (int64_t)mp * nv) return;
+    const int v = (int)(e / mp), i = (int)(e % mp);
+    double x;
+    if (k >= 0 && v == 0)
+        x = (i == k) ? 1.0 : 0.0;
+    else
+        x = (i < m) ? p[(int64_t)i * nv + v] : 0.0;
+    R[e] = x;
+}
+
+__global__ __launch_bounds__(256) void k_coef(const double* __restrict__ U, int m, int mp, int nv, double s0,
+                                              double s1, float* __restrict__ coef, int* __restrict__ err) {
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= m * nv) return;
+    const int i = e / nv, v = e % nv;
+    const double x = U[(int64_t)v * mp + i] * (v == 0 ? s0 : s1);
+    if (!isfinite(x)) atomicOr(err, 4);
+    coef[e] = (float)x;
+}
+
+}  // namespace
+
+hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k, double mu, double* A,
+                           int mp, int* err, hipStream_t st) {
+    const int64_t n = (int64_t)mp * mp;
+    hipLaunchKernelGGL(k_assemble, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, st, K, m, p, pstride, k,
+                       mu, A, mp, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_potrf(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                        hipStream_t st) {
+    const int T = mp / 64;
+    for (int t = 0; t < T; ++t) {
+        hipLaunchKernelGGL(k_potrf_diag, dim3(nbatch), dim3(64), 0, st, A, Linv, mp, bstride, t, err);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int n = T - 1 - t;
+        if (n == 0) break;
+        hipLaunchKernelGGL(k_trsm_panel, dim3(n, nbatch), dim3(256), 0, st, A, Linv, mp, bstride, t);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_syrk_update, dim3(n * (n + 1) / 2, nbatch), dim3(256), 0, st, A, mp, bstride, t);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_trtri(const double* L, double* Linv, int mp, int nbatch, int64_t bstride, hipStream_t st) {
+    const int T = mp / 64;
+    hipLaunchKernelGGL(k_zero_upper, dim3(T * T, nbatch), dim3(256), 0, st, Linv, mp, bstride);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    for (int s = 1; s < T; ++s) {
+        hipLaunchKernelGGL(k_trtri_step, dim3(T - s, nbatch), dim3(256), 0, st, L, Linv, mp, bstride, s);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_chol_solve(const double* L, const double* Linv, int mp, int nrhs, const double* R,
+                             double* U, double* work, hipStream_t st) {
+    hipLaunchKernelGGL(k_chol_solve, dim3(nrhs), dim3(256), 0, st, L, Linv, mp, R, U, work);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_rhs(const double* p, int m, int nv, int k, double* R, int mp, hipStream_t st) {
+    const int64_t n = (int64_t)mp * nv;
+    hipLaunchKernelGGL(k_build_rhs, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, st, p, m, nv, k, R, mp);
+    return hipGetLastError();
+}
+
+hipError_t launch_coef(const double* U, int m, int mp, int nv, double s0, double s1, float* coef, int* err,
+                       hipStream_t st) {
+    hipLaunchKernelGGL(k_coef, dim3((unsigned)ceil_div((int64_t)m * nv, 256)), dim3(256), 0, st, U, m, mp, nv,
+                       s0, s1, coef, err);
+    return hipGetLastError();
+}
+
+}  // namespace mfac

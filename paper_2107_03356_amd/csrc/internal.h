@@ -1,0 +1,107 @@
+// Internal declarations shared by the HIP translation units of libmfac.
+// Not part of the public ABI (include/mfac.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mfac {
+
+// Window storage: the m x d window is kept as column slabs of SLAB floats;
+// slab s holds columns [s*SLAB, (s+1)*SLAB) of all m rows, row i of the slab
+// at offset i*SLAB (so one slab is a contiguous m*SLAB block). Columns past d
+// in the last slab are zero.
+constexpr int SLAB = 2048;
+// Coefficient matrices are padded to a multiple of NB with an identity block.
+constexpr int NB = 64;
+constexpr int MAXNV = 17;  // 1 inserted gradient + up to 16 extra queries
+constexpr int PASS1_MAX_GRID = 512;
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Pointer/scale sets for the multi-vector passes (passed by value).
+struct VecIn {
+    const float* v[MAXNV];
+};
+struct VecOut {
+    const float* x[MAXNV];  // x_v, or nullptr when alpha_v == 0
+    float* y[MAXNV];
+    float alpha[MAXNV];
+};
+
+// ---------------------------------------------------------------- passes
+// Fill n floats with zero.
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t st);
+// rows (count x d, row-major, leading dimension ld) -> window rows [first, first+count)
+hipError_t launch_set_rows(float* G, int m, int64_t d, int64_t nslab, int first, int count,
+                           const float* rows, int64_t ld, hipStream_t st);
+hipError_t launch_get_rows(const float* G, int m, int64_t d, int first, int count,
+                           float* rows, int64_t ld, hipStream_t st);
+// Pass 1: part[b][i*nv+v] = partial sums of G[i,:] . vec_v over the chunks of
+// work-group b; optionally writes vec_0 into row wslot first. Returns grid size.
+hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv,
+                        const VecIn& vin, bool aligned, float* Gw, int wslot,
+                        double* part, int* grid_out, hipStream_t st);
+// p[t] = sum_b part[b][t] for t < mnv (fixed order, fp64)
+hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double* p,
+                                  hipStream_t st);
+// Pass 2: y_v = alpha_v x_v - sum_i coef[i*nv+v] G[i,:]
+hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv,
+                        const float* coef, const VecOut& vout, bool aligned, hipStream_t st);
+
+// ---------------------------------------------------------------- Gram
+// Window Gram: K (m x m, fp64, full symmetric) = sum over slabs of G_s G_s^T,
+// fp32 MFMA tiles with fp64 flushes; part must hold gram_window_part_doubles().
+int64_t gram_window_part_doubles(int m, int64_t nslab);
+hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part, double* K,
+                              hipStream_t st);
+// Static blocks: A_b = G_b G_b^T + mu I (fp64 MFMA), padded to mp with identity;
+// blocks [b0, b0+nb) of the m x d row-major G, block width B.
+hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb,
+                              double mu, double* A, int mp, hipStream_t st);
+
+// ---------------------------------------------------------------- coefficients
+// A (mp x mp) = K (m x m) + mu I, identity padding; optionally first replaces
+// row/column k of K with p (dynamic replace).
+hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k, double mu,
+                           double* A, int mp, int* err, hipStream_t st);
+// In-place lower Cholesky of nbatch matrices (mp x mp, batch stride) and the
+// inverses of its diagonal NB x NB blocks into Linv's diagonal blocks.
+hipError_t launch_potrf(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                        hipStream_t st);
+// Off-diagonal blocks of Linv = L^-1 (diagonal blocks from launch_potrf).
+hipError_t launch_trtri(const double* L, double* Linv, int mp, int nbatch, int64_t bstride,
+                        hipStream_t st);
+// Solve L L^T U = R for nrhs columns (R and U: mp x nrhs, column c at c*mp).
+hipError_t launch_chol_solve(const double* L, const double* Linv, int mp, int nrhs,
+                             const double* R, double* U, double* work, hipStream_t st);
+// Dynamic right-hand sides and coefficients:
+// rhs column 0 = e_k (if k >= 0), columns v >= v0: p[:, v] (mp x nv layout).
+hipError_t launch_build_rhs(const double* p, int m, int nv, int k, double* R, int mp,
+                            hipStream_t st);
+// coef[i*nv+v] = scale_v * U[v*mp+i]  (fp32)
+hipError_t launch_coef(const double* U, int m, int mp, int nv, double s0, double s1,
+                       float* coef, int* err, hipStream_t st);
+
+// ---------------------------------------------------------------- static
+// W_b = Linv_b G_b in place over G (fp32), colsum of squares in fp64 -> diag
+hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* G, int m,
+                            int64_t d, int B, int b0, int nb, double lam, double* diag,
+                            hipStream_t st);
+hipError_t launch_diag_to_f32(const double* diag, int64_t d, float* out, hipStream_t st);
+hipError_t launch_scores(const float* theta, const double* diag, int64_t d, double* scores,
+                         int* err, hipStream_t st);
+// Radix selection of the keep-th largest score and the keep-mask
+struct SelectScratch {
+    unsigned int* hist;       // 256 bins
+    unsigned long long* state;  // prefix, mask, remaining rank, (unused)
+    unsigned int* chunk_cnt;  // per-chunk tie counts
+    int nchunk;
+};
+int64_t select_scratch_bytes(int64_t d);
+SelectScratch select_scratch_carve(void* base, int64_t d);
+hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, SelectScratch sc,
+                            uint8_t* mask, hipStream_t st);
+
+}  // namespace mfac

@@ -1,0 +1,339 @@
+// Streaming passes over the window (the two O(dm) matrix-vector products of
+// the dynamic algorithm, Section 3.2 complexity analysis; Appendix B: the
+// update reuses p = G g for both the Gram row and the IHVP).
+//
+// Both passes are HBM-bound (0.5 flop per byte). The window is stored as
+// column slabs (internal.h), so every wave reads rows of 8 KB contiguous and
+// all rows of a slab lie in one contiguous m*8 KB region.
+//
+// Pass 1: every work-group owns a set of column chunks and keeps per-row
+// running sums in LDS. For each row a wave loads U float4 per lane (128-bit
+// coalesced loads), multiplies with the register-resident vector chunks and
+// reduces across the wave with lane shuffles. The replaced row is never read:
+// the new gradient is taken from registers and written into the slot in the
+// same pass. Work-group partials go to a [grid][m*nv] fp64 buffer, summed in
+// a fixed order by the reduce kernel (deterministic, no float atomics).
+//
+// Pass 2: each wave owns one column chunk of the output and walks all m rows,
+// accumulating coef[i] * G[i, chunk] in registers; no cross-lane traffic.
+#include "internal.h"
+
+namespace mfac {
+namespace {
+
+__device__ __forceinline__ float4 ld4(const float* __restrict__ p, int64_t j, int64_t d, int aligned) {
+    if (aligned && j + 3 < d) return *reinterpret_cast<const float4*>(p + j);
+    float4 r;
+    r.x = (j < d) ? p[j] : 0.f;
+    r.y = (j + 1 < d) ? p[j + 1] : 0.f;
+    r.z = (j + 2 < d) ? p[j + 2] : 0.f;
+    r.w = (j + 3 < d) ? p[j + 3] : 0.f;
+    return r;
+}
+
+__device__ __forceinline__ void st4(float* __restrict__ p, int64_t j, int64_t d, int aligned, float4 v) {
+    if (aligned && j + 3 < d) {
+        *reinterpret_cast<float4*>(p + j) = v;
+        return;
+    }
+    if (j < d) p[j] = v.x;
+    if (j + 1 < d) p[j + 1] = v.y;
+    if (j + 2 < d) p[j + 2] = v.z;
+    if (j + 3 < d) p[j + 3] = v.w;
+}
+
+__device__ __forceinline__ float dot4(float4 a, float4 b, float s) {
+    s = fmaf(a.x, b.x, s);
+    s = fmaf(a.y, b.y, s);
+    s = fmaf(a.z, b.z, s);
+    s = fmaf(a.w, b.w, s);
+    return s;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+__global__ void k_fill_zero(float* __restrict__ p, int64_t n) {
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride) p[i] = 0.f;
+}
+
+__global__ __launch_bounds__(256) void k_set_rows(float* __restrict__ G, int m, int64_t d,
+                                                  int64_t ncolpad, int first,
+                                                  const float* __restrict__ rows, int64_t ld,
+                                                  int aligned) {
+    const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (j >= ncolpad) return;
+    const int r = blockIdx.y;
+    const float4 v = ld4(rows + (int64_t)r * ld, j, d, aligned);
+    const int64_t slab = j / SLAB;
+    const int64_t off = j - slab * SLAB;
+    *reinterpret_cast<float4*>(G + slab * (int64_t)m * SLAB + (int64_t)(first + r) * SLAB + off) = v;
+}
+
+__global__ __launch_bounds__(256) void k_get_rows(const float* __restrict__ G, int m, int64_t d,
+                                                  int first, float* __restrict__ rows, int64_t ld,
+                                                  int aligned) {
+    const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (j >= d) return;
+    const int r = blockIdx.y;
+    const int64_t slab = j / SLAB;
+    const int64_t off = j - slab * SLAB;
+    const float4 v =
+        *reinterpret_cast<const float4*>(G + slab * (int64_t)m * SLAB + (int64_t)(first + r) * SLAB + off);
+    st4(rows + (int64_t)r * ld, j, d, aligned, v);
+}
+
+template <int NV, int U>
+__global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int m, int64_t d,
+                                               int64_t nchunk, VecIn vin, int aligned,
+                                               float* __restrict__ Gw, int wslot,
+                                               double* __restrict__ part) {
+    extern __shared__ float acc[];  // m * NV running sums
+    constexpr int CW = 256 * U;     // chunk width (floats): 64 lanes x float4 x U
+    constexpr int CPS = SLAB / CW;  // chunks per slab
+    static_assert(SLAB % CW == 0, "chunk must tile the slab");
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int mnv = m * NV;
+    for (int t = threadIdx.x; t < mnv; t += 256) acc[t] = 0.f;
+    __syncthreads();
+
+    for (int64_t c = blockIdx.x; c < nchunk; c += gridDim.x) {
+        const int64_t slab = c / CPS;
+        const int off = (int)(c - slab * CPS) * CW;
+        const int64_t j0 = slab * SLAB + off;
+        const float* Gs = G + slab * (int64_t)m * SLAB + off + lane * 4;
+
+        float4 vr[NV][U];
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int u = 0; u < U; ++u) vr[v][u] = ld4(vin.v[v], j0 + u * 256 + lane * 4, d, aligned);
+
+        if (wslot >= 0 && wave == 0) {
+            float* dst = Gw + slab * (int64_t)m * SLAB + (int64_t)wslot * SLAB + off + lane * 4;
+#pragma unroll
+            for (int u = 0; u < U; ++u) *reinterpret_cast<float4*>(dst + u * 256) = vr[0][u];
+        }
+
+        // two rows per iteration: rows i and i + 4 handled by this wave
+        for (int i = wave; i < m; i += 8) {
+            const int i2 = i + 4;
+            const bool has2 = i2 < m;
+            float4 ga[U], gb[U];
+            if (i != wslot) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    ga[u] = *reinterpret_cast<const float4*>(Gs + (int64_t)i * SLAB + u * 256);
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) ga[u] = vr[0][u];
+            }
+            if (has2 && i2 != wslot) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    gb[u] = *reinterpret_cast<const float4*>(Gs + (int64_t)i2 * SLAB + u * 256);
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) gb[u] = vr[0][u];
+            }
+            float sa[NV], sb[NV];
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                float a = 0.f, b = 0.f;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    a = dot4(ga[u], vr[v][u], a);
+                    b = dot4(gb[u], vr[v][u], b);
+                }
+                sa[v] = wave_sum(a);
+                sb[v] = wave_sum(b);
+            }
+            if (lane == 0) {
+#pragma unroll
+                for (int v = 0; v < NV; ++v) {
+                    acc[i * NV + v] += sa[v];
+                    if (has2) acc[i2 * NV + v] += sb[v];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    double* out = part + (int64_t)blockIdx.x * mnv;
+    for (int t = threadIdx.x; t < mnv; t += 256) out[t] = (double)acc[t];
+}
+
+__global__ __launch_bounds__(256) void k_reduce_partials(const double* __restrict__ part, int grid,
+                                                         int mnv, double* __restrict__ p) {
+    __shared__ double red[16][17];
+    const int to = threadIdx.x & 15;
+    const int bg = threadIdx.x >> 4;
+    const int t = blockIdx.x * 16 + to;
+    double s = 0.0;
+    if (t < mnv)
+        for (int b = bg; b < grid; b += 16) s += part[(int64_t)b * mnv + t];
+    red[bg][to] = s;
+    __syncthreads();
+    if (bg == 0 && t < mnv) {
+        double r = 0.0;
+        for (int k = 0; k < 16; ++k) r += red[k][to];
+        p[t] = r;
+    }
+}
+
+template <int NV, int U>
+__global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int m, int64_t d,
+                                               int64_t nwchunk, const float* __restrict__ coef,
+                                               VecOut vout, int aligned) {
+    constexpr int WCW = 256 * U;  // wave chunk width (floats)
+    constexpr int CPS = SLAB / WCW;
+    static_assert(SLAB % WCW == 0, "chunk must tile the slab");
+    const int lane = threadIdx.x & 63;
+    const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (c >= nwchunk) return;
+    const int64_t slab = c / CPS;
+    const int off = (int)(c - slab * CPS) * WCW;
+    const int64_t j0 = slab * SLAB + off;
+    const float* Gs = G + slab * (int64_t)m * SLAB + off + lane * 4;
+
+    float4 acc[NV][U];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[v][u] = make_float4(0.f, 0.f, 0.f, 0.f);
+
+#pragma unroll 2
+    for (int i = 0; i < m; ++i) {
+        float4 g[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) g[u] = *reinterpret_cast<const float4*>(Gs + (int64_t)i * SLAB + u * 256);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const float cv = coef[i * NV + v];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                acc[v][u].x = fmaf(cv, g[u].x, acc[v][u].x);
+                acc[v][u].y = fmaf(cv, g[u].y, acc[v][u].y);
+                acc[v][u].z = fmaf(cv, g[u].z, acc[v][u].z);
+                acc[v][u].w = fmaf(cv, g[u].w, acc[v][u].w);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        const float a = vout.alpha[v];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t j = j0 + u * 256 + lane * 4;
+            float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (a != 0.f) x = ld4(vout.x[v], j, d, aligned);
+            float4 y;
+            y.x = a * x.x - acc[v][u].x;
+            y.y = a * x.y - acc[v][u].y;
+            y.z = a * x.z - acc[v][u].z;
+            y.w = a * x.w - acc[v][u].w;
+            st4(vout.y[v], j, d, aligned, y);
+        }
+    }
+}
+
+template <int NV>
+struct PassCfg {
+    // floats per lane per row: keep the register-resident vectors at <= ~72 VGPRs
+    static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 8 ? 2 : 1;
+    static constexpr int U2 = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 4 ? 2 : 1;
+};
+
+template <int NV>
+hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn& vin, bool aligned,
+                    float* Gw, int wslot, double* part, int* grid_out, hipStream_t st) {
+    constexpr int U = PassCfg<NV>::U;
+    const int64_t nchunk = nslab * (SLAB / (256 * U));
+    const int grid = (int)(nchunk < PASS1_MAX_GRID ? nchunk : PASS1_MAX_GRID);
+    const size_t lds = (size_t)m * NV * sizeof(float);
+    hipLaunchKernelGGL((k_pass1<NV, U>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
+                       aligned ? 1 : 0, Gw, wslot, part);
+    *grid_out = grid;
+    return hipGetLastError();
+}
+
+template <int NV>
+hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const float* coef,
+                    const VecOut& vout, bool aligned, hipStream_t st) {
+    constexpr int U = PassCfg<NV>::U2;
+    const int64_t nwchunk = nslab * (SLAB / (256 * U));
+    const int64_t grid = ceil_div(nwchunk, 4);
+    hipLaunchKernelGGL((k_pass2<NV, U>), dim3((unsigned)grid), dim3(256), 0, st, G, m, d, nwchunk,
+                       coef, vout, aligned ? 1 : 0);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t st) {
+    int64_t blocks = ceil_div(n, 256);
+    if (blocks > 65536) blocks = 65536;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, st, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_set_rows(float* G, int m, int64_t d, int64_t nslab, int first, int count,
+                           const float* rows, int64_t ld, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    const int64_t ncolpad = nslab * SLAB;
+    const bool aligned = ((uintptr_t)rows % 16 == 0) && (ld % 4 == 0);
+    dim3 grid((unsigned)ceil_div(ncolpad / 4, 256), (unsigned)count);
+    hipLaunchKernelGGL(k_set_rows, grid, dim3(256), 0, st, G, m, d, ncolpad, first, rows, ld,
+                       aligned ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_get_rows(const float* G, int m, int64_t d, int first, int count, float* rows,
+                           int64_t ld, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    const bool aligned = ((uintptr_t)rows % 16 == 0) && (ld % 4 == 0);
+    dim3 grid((unsigned)ceil_div(ceil_div(d, 4), 256), (unsigned)count);
+    hipLaunchKernelGGL(k_get_rows, grid, dim3(256), 0, st, G, m, d, first, rows, ld, aligned ? 1 : 0);
+    return hipGetLastError();
+}
+
+#define MFAC_NV_CASES(X) \
+    X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16) X(17)
+
+hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv, const VecIn& vin,
+                        bool aligned, float* Gw, int wslot, double* part, int* grid_out,
+                        hipStream_t st) {
+    switch (nv) {
+#define CASE(N) \
+    case N: return pass1_nv<N>(G, m, d, nslab, vin, aligned, Gw, wslot, part, grid_out, st);
+        MFAC_NV_CASES(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double* p, hipStream_t st) {
+    hipLaunchKernelGGL(k_reduce_partials, dim3((unsigned)ceil_div(mnv, 16)), dim3(256), 0, st, part,
+                       grid, mnv, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv, const float* coef,
+                        const VecOut& vout, bool aligned, hipStream_t st) {
+    switch (nv) {
+#define CASE(N) \
+    case N: return pass2_nv<N>(G, m, d, nslab, coef, vout, aligned, st);
+        MFAC_NV_CASES(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace mfac

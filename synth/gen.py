@@ -76,7 +76,7 @@ class GradientStream:
         z64 = z.to(torch.float64)
         if s is not None:
             z64 *= s
-        z64 /= math.sqrt(d)
+        z64 /= math.sqrt(self.wl.scale_d or d)
         return z64.to(torch.float32)
 
     def is_correlated(self, r: int) -> bool:

@@ -32,6 +32,8 @@ class Workload:
     block: int = 0       # static: block size B (B divides d)
     theta_std: float = 0.0
     fill_by_replace: bool = False   # dynamic: start empty, fill with m replaces
+    scale_d: int = 0     # d in the 1/sqrt(d) entry scale (0: the workload's own d);
+                         # reduced-size parity cases keep the full-size scale
 
     def scaled(self, **kw) -> "Workload":
         """Same recipe at another size (parity cases the oracle finishes in seconds)."""

@@ -1,0 +1,214 @@
+"""GPU parity of the dynamic sliding-window path against the fp64 oracle.
+
+Every case draws its rows once (synth), hands the same fp32 values to the HIP
+path (through the C ABI) and to oracle.dynamic.WindowOracle, and compares
+F^-1 g_new (and the fused extra queries) element by element in relative L2.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import REL_TOL, rel_l2, require_gpu, say
+from oracle.dynamic import WindowOracle
+from synth import GradientStream, get_workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def _sliding(dev, wl, seed, nsteps, queries=0, fill_by_replace=False, check=lambda t: True):
+    from paper_2107_03356_amd import Window
+    gs = GradientStream(wl, seed=seed, device="cpu")
+    d, m = wl.d, wl.m
+    if fill_by_replace:
+        win = Window(d, m, wl.lam, max_queries=queries, device=dev)
+        orc = WindowOracle(d, m, wl.lam)
+        rows = range(0, m + nsteps)
+    else:
+        G0 = gs.window()
+        win = Window(d, m, wl.lam, max_queries=queries, G0=G0.to(dev), device=dev)
+        orc = WindowOracle(d, m, wl.lam, G0=G0.numpy())
+        rows = range(m, m + nsteps)
+    errs, outs = [], []
+    for t, r in enumerate(rows):
+        g = gs.row(r)
+        if queries:
+            X = gs.queries(t, queries)
+            y, Y = win.replace(g.to(dev), X=X.to(dev))
+        else:
+            y = win.replace(g.to(dev))
+        slot_before = orc.steps % m
+        yo = orc.slide(g.numpy())
+        if check(t):
+            torch.cuda.synchronize()
+            e = rel_l2(y.cpu().numpy(), yo)
+            errs.append(e)
+            if queries:
+                Yo = orc.ihvp(X.numpy())
+                for q in range(queries):
+                    errs.append(rel_l2(Y[q].cpu().numpy(), Yo[q]))
+            assert max(errs[-(1 + queries):]) < REL_TOL, (t, slot_before, errs[-(1 + queries):])
+        outs.append(y)
+    assert win.status() == 0
+    return win, orc, errs, outs
+
+
+def test_tiny_fill_by_replace_every_step(dev):
+    wl = get_workload("dyn_tiny_d4096_m16")
+    say("tiny fill_by_replace", wl.d, wl.m)
+    win, orc, errs, outs = _sliding(dev, wl, seed=1, nsteps=wl.steps, fill_by_replace=True)
+    assert len(errs) == wl.m + wl.steps
+    assert max(errs) < 1e-5, max(errs)
+    assert win.info() == (0, wl.m + wl.steps)
+
+
+def test_tiny_init_equals_fill(dev):
+    """R2: an empty window filled by m replaces equals init with those rows."""
+    wl = get_workload("dyn_tiny_d4096_m16")
+    say("tiny init vs fill")
+    _, _, errs_a, outs_a = _sliding(dev, wl, seed=2, nsteps=wl.steps, fill_by_replace=True)
+    _, _, errs_b, outs_b = _sliding(dev, wl, seed=2, nsteps=wl.steps, fill_by_replace=False)
+    assert max(errs_b) < 1e-5
+    for ya, yb in zip(outs_a[wl.m:], outs_b):
+        assert rel_l2(ya.cpu().numpy(), yb.cpu().numpy()) < 1e-5
+
+
+@pytest.mark.parametrize("d,m,lam,q,dist", [
+    (3 * 2048 + 777, 40, 1e-3, 3, "gauss"),        # ragged d (d % 4 != 0), m not a multiple of 64
+    (20000, 200, 1e-4, 2, "lognormal"),            # several 64-row tiles in the factor
+    (40968, 1024, 1e-5, 8, "lognormal"),           # m = 1024 with 8 fused queries (ResNet18 recipe)
+    (2048, 1, 1e-2, 1, "gauss"),                   # m = 1 (Sherman-Morrison)
+    (5, 3, 1e-1, 1, "gauss"),                      # d smaller than one float4 group row
+])
+def test_ragged_and_multitile_with_queries(dev, d, m, lam, q, dist):
+    base = get_workload("dyn_resnet18_d11.2m_m1024_q8")
+    wl = base.scaled(d=d, m=m, lam=lam, dist=dist, queries=q, scale_d=(base.d if dist == "lognormal" else 0))
+    say("ragged", d, m, lam, q)
+    nsteps = 6 if m >= 1024 else 12
+    _, _, errs, _ = _sliding(dev, wl, seed=3, nsteps=nsteps, queries=q)
+    assert max(errs) < REL_TOL
+
+
+def test_d1m_m256_full_size(dev):
+    """The d = 1,048,576, m = 256 workload at full size (a few sliding steps)."""
+    wl = get_workload("dyn_d1m_m256")
+    say("d1m m256 full size")
+    _, _, errs, _ = _sliding(dev, wl, seed=0, nsteps=4)
+    assert max(errs) < REL_TOL
+
+
+def test_correlated_rows_resnet50_recipe_small(dev):
+    """10% correlated rows (ResNet50 recipe) at reduced d, full m = 1024."""
+    base = get_workload("dyn_resnet50_d25.6m_m1024")
+    wl = base.scaled(d=65536, scale_d=base.d)
+    say("resnet50 recipe small")
+    _, _, errs, _ = _sliding(dev, wl, seed=0, nsteps=4)
+    assert max(errs) < REL_TOL
+
+
+def test_ihvp_and_explicit_slots(dev):
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=30000, m=96, scale_d=base.d)
+    gs = GradientStream(wl, seed=5)
+    G0 = gs.window()
+    say("ihvp + explicit slots")
+    win = Window(wl.d, wl.m, wl.lam, max_queries=4, G0=G0.to(dev), device=dev)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    X = gs.queries(0, 4)
+    Y = win.ihvp(X.to(dev))
+    Yo = orc.ihvp(X.numpy())
+    for q in range(4):
+        assert rel_l2(Y[q].cpu().numpy(), Yo[q]) < REL_TOL
+    # explicit slots, in a non-ring order; ring head must not move
+    for t, slot in enumerate([17, 3, 95, 3, 0]):
+        g = gs.row(wl.m + t)
+        y = win.replace(g.to(dev), slot=slot)
+        orc.replace(slot, g.numpy())
+        assert rel_l2(y.cpu().numpy(), orc.ihvp(g.numpy())) < REL_TOL
+    assert win.info() == (0, 5)
+    np.testing.assert_array_equal(win.get_rows().cpu().numpy(), orc.G)
+    Y = win.ihvp(X[:1].to(dev).contiguous())
+    assert rel_l2(Y[0].cpu().numpy(), orc.ihvp(X[0].numpy())) < REL_TOL
+
+
+def test_replace_without_output_and_queries_only(dev):
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=12345 * 4, m=70, scale_d=base.d)
+    gs = GradientStream(wl, seed=6)
+    G0 = gs.window()
+    say("replace without y_out")
+    win = Window(wl.d, wl.m, wl.lam, max_queries=2, G0=G0.to(dev), device=dev)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    g = gs.row(wl.m)
+    win.replace(g.to(dev), want_y=False)          # window update only
+    orc.slide(g.numpy())
+    g2 = gs.row(wl.m + 1)
+    X = gs.queries(1, 2)
+    _, Y = win.replace(g2.to(dev), X=X.to(dev), want_y=False)   # queries but no y_out
+    orc.slide(g2.numpy())
+    Yo = orc.ihvp(X.numpy())
+    for q in range(2):
+        assert rel_l2(Y[q].cpu().numpy(), Yo[q]) < REL_TOL
+
+
+def test_deterministic_bitwise(dev):
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=50000, m=128, scale_d=base.d)
+    say("determinism")
+    _, _, _, a = _sliding(dev, wl, seed=7, nsteps=5, queries=0, check=lambda t: False)
+    _, _, _, b = _sliding(dev, wl, seed=7, nsteps=5, queries=0, check=lambda t: False)
+    for ya, yb in zip(a, b):
+        assert torch.equal(ya, yb)
+
+
+def test_checkpoint_resume(dev):
+    """Resume = init from the saved rows + head; continues like the original."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=40000, m=64, scale_d=base.d)
+    gs = GradientStream(wl, seed=8)
+    G0 = gs.window()
+    say("checkpoint/resume")
+    win = Window(wl.d, wl.m, wl.lam, G0=G0.to(dev), device=dev)
+    for t in range(5):
+        win.replace(gs.row(wl.m + t).to(dev))
+    rows = win.get_rows()
+    head, steps = win.info()
+    win2 = Window(wl.d, wl.m, wl.lam, G0=rows, device=dev)
+    win2.set_head(head, steps)
+    for t in range(5, 9):
+        g = gs.row(wl.m + t).to(dev)
+        ya, yb = win.replace(g), win2.replace(g)
+        assert rel_l2(ya.cpu().numpy(), yb.cpu().numpy()) < 1e-5
+    assert win.info() == win2.info()
+
+
+def test_nonfinite_latched_and_rebuild_recovers(dev):
+    from paper_2107_03356_amd import MFAC_ENONFINITE, Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=8192, m=32, scale_d=base.d)
+    gs = GradientStream(wl, seed=9)
+    G0 = gs.window()
+    say("non-finite latch")
+    win = Window(wl.d, wl.m, wl.lam, G0=G0.to(dev), device=dev)   # max_queries = 0: ihvp still takes 1 vector
+    bad = gs.row(wl.m).clone()
+    bad[100] = float("nan")
+    win.replace(bad.to(dev), slot=4)
+    assert win.status() == MFAC_ENONFINITE
+    assert win.status() == 0          # cleared after being reported
+    good = gs.row(wl.m + 1)
+    win.set_rows(4, good[None, :].to(dev).contiguous())
+    win.rebuild()
+    assert win.status() == 0
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    orc.replace(4, good.numpy())
+    x = gs.queries(0, 1)
+    y = win.ihvp(x.to(dev))
+    assert rel_l2(y[0].cpu().numpy(), orc.ihvp(x[0].numpy())) < REL_TOL

@@ -1,0 +1,106 @@
+"""GPU parity of the static block-wise path: inverse diagonal, W, scores, mask."""
+
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg as sla
+import torch
+
+from gpu_common import rel_l2, require_gpu, say
+from oracle import mask as omask
+from oracle import static as ostatic
+from synth import GradientStream, get_workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def _oracle_W(G, lam, B):
+    """W_b = R_b^-1 G_b per block (fp64), the quantity written over G."""
+    m, d = G.shape
+    out = np.empty((m, d))
+    for b in range(d // B):
+        Gb = G[:, b * B:(b + 1) * B].astype(np.float64)
+        R = np.linalg.cholesky(Gb @ Gb.T + m * lam * np.eye(m))
+        out[:, b * B:(b + 1) * B] = sla.solve_triangular(R, Gb, lower=True)
+    return out
+
+
+def _run(dev, G, B, lam, theta, keep):
+    from paper_2107_03356_amd import StaticBlocks
+    Gd = G.to(dev).contiguous()
+    sb = StaticBlocks(Gd, B, lam)
+    diag64 = sb.inv_diag(fp64=True)
+    diag32 = sb.inv_diag()
+    mask, scores = sb.obs_mask(theta.to(dev), keep)
+    torch.cuda.synchronize()
+    assert sb.status() == 0
+    return (Gd.cpu().numpy(), diag64.cpu().numpy(), diag32.cpu().numpy(), mask.cpu().numpy(),
+            scores.cpu().numpy())
+
+
+@pytest.mark.parametrize("m,B,nb,lam,batch_cap", [
+    (100, 256, 6, 1e-3, None),     # m padded to 128 inside
+    (64, 512, 3, 1e-4, 2),         # batch boundary inside the block loop
+    (1, 64, 4, 1e-2, None),        # m = 1 closed form
+    (200, 2048, 2, 1e-4, None),    # the pruning block width
+])
+def test_static_small(dev, m, B, nb, lam, batch_cap, monkeypatch):
+    if batch_cap:
+        monkeypatch.setenv("MFAC_STATIC_BATCH_BLOCKS", str(batch_cap))
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=B * nb, m=m, block=B, lam=lam, scale_d=B)   # per-block scale: Fisher term well above m*lam
+    gs = GradientStream(wl, seed=11)
+    G = gs.rows(0, m)
+    theta = gs.theta()
+    keep = wl.d // 2
+    say("static small", m, B, nb, lam, batch_cap)
+    W, d64, d32, mk, sc = _run(dev, G, B, lam, theta, keep)
+    Gn = G.numpy()
+    dref = ostatic.inv_diag(Gn, lam, B)
+    assert rel_l2(d64, dref) < 1e-11
+    assert rel_l2(d32, dref) < 1e-6
+    assert rel_l2(W, _oracle_W(Gn, lam, B)) < 1e-6
+    sref = omask.scores(theta.numpy(), dref)
+    assert rel_l2(sc, sref) < 1e-11
+    np.testing.assert_array_equal(mk, omask.keep_mask(sref, keep))
+
+
+def test_static_pruning_recipe_reduced_blocks(dev):
+    """m = 1024, B = 2048 with the full-size entry scale (1/sqrt(4,194,304)), 3 blocks."""
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=3 * 2048, scale_d=base.d)
+    gs = GradientStream(wl, seed=0)
+    G = gs.rows(0, wl.m)
+    theta = gs.theta()
+    keep = wl.d // 2
+    say("static pruning recipe, 3 blocks")
+    W, d64, d32, mk, sc = _run(dev, G, wl.block, wl.lam, theta, keep)
+    dref = ostatic.inv_diag(G.numpy(), wl.lam, wl.block)
+    assert rel_l2(d64, dref) < 1e-11
+    sref = omask.scores(theta.numpy(), dref)
+    np.testing.assert_array_equal(mk, omask.keep_mask(sref, keep))
+
+
+@pytest.mark.parametrize("keep_frac", [0.0, 1.0, 1e-4, 0.5, 0.7])
+def test_mask_edges_and_ties(dev, keep_frac):
+    """keep = 0, d, 1, and cuts inside a band of exactly tied (zero) scores."""
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=8 * 256, m=48, block=256, lam=1e-3, scale_d=256)
+    gs = GradientStream(wl, seed=12)
+    G = gs.rows(0, wl.m)
+    theta = gs.theta()
+    theta[::3] = 0.0            # a third of the scores are exactly 0: ties at the cut for keep > 2/3 d
+    theta[1::7] = -0.0
+    keep = int(round(wl.d * keep_frac))
+    say("mask edges", keep)
+    W, d64, d32, mk, sc = _run(dev, G, wl.block, wl.lam, theta, keep)
+    dref = ostatic.inv_diag(G.numpy(), wl.lam, wl.block)
+    sref = omask.scores(theta.numpy(), dref)
+    np.testing.assert_array_equal(mk, omask.keep_mask(sref, keep))
+    assert int(mk.sum()) == keep
