@@ -220,7 +220,7 @@ def main():
         "config": {
             "workload": wl.name, "d": d, "m": m, "lambda": wl.lam, "queries": nq,
             "corr_frac": wl.corr_frac,
-            "step": "replace oldest row + Gram row + m x m coefficient refactor + IHVP of the new gradient",
+            "step": "replace oldest row + Gram row + O(m^2) update of the fp64 inverse of G G^T + m lambda I (full refactor every R replaces) + IHVP of the new gradient",
             "parallelism": "single GPU",
         },
         "achieved_hbm_gbs_step": step_bytes / (ms_step * 1e-3) / 1e9,

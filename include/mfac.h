@@ -134,6 +134,18 @@ mfac_status mfac_window_info(mfac_window w, int32_t* head_out /* host */, int64_
 /* Set the ring head and step count (resume from a checkpoint of the rows). */
 mfac_status mfac_window_set_head(mfac_window w, int32_t head, int64_t steps);
 
+/* How the m x m coefficients follow a replace. The library keeps the explicit
+ * fp64 inverse of A = G G^T + m*lambda*I.
+ *   period == 0: refactor A from the Gram matrix on every replace (blocked
+ *                Cholesky, triangular inverse, L^-T L^-1: the O(m^3) per-replace
+ *                cost of Section 3.2's complexity analysis);
+ *   period >= 1: O(m^2) update of the inverse on a replace (slot k's old
+ *                pivot removed through its Schur complement, the new column
+ *                inserted), with a full refactor from the Gram matrix every
+ *                `period` replaces to bound rounding drift.
+ * Default: max(m, 1024). */
+mfac_status mfac_window_set_refactor_period(mfac_window w, int32_t period);
+
 /* Change the stream later calls enqueue on. */
 mfac_status mfac_window_set_stream(mfac_window w, hipStream_t stream);
 

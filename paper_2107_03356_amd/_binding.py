@@ -41,6 +41,7 @@ SIGNATURES = {
     "mfac_window_get_rows": (_c.c_int, [_VP, _I32, _I32, _VP]),
     "mfac_window_info": (_c.c_int, [_VP, _c.POINTER(_I32), _c.POINTER(_I64)]),
     "mfac_window_set_head": (_c.c_int, [_VP, _I32, _I64]),
+    "mfac_window_set_refactor_period": (_c.c_int, [_VP, _I32]),
     "mfac_window_set_stream": (_c.c_int, [_VP, _VP]),
     "mfac_window_trace": (_c.c_int, [_VP, _I32]),
     "mfac_window_trace_read": (_c.c_int, [_VP, _c.POINTER(_F64), _c.POINTER(_I64)]),
@@ -202,6 +203,9 @@ class Window:
 
     def set_head(self, head, steps):
         _check("mfac_window_set_head", load().mfac_window_set_head(self.handle, int(head), int(steps)))
+
+    def set_refactor_period(self, period):
+        _check("mfac_window_set_refactor_period", load().mfac_window_set_refactor_period(self.handle, int(period)))
 
     def trace(self, enable=True):
         _check("mfac_window_trace", load().mfac_window_trace(self.handle, 1 if enable else 0))

@@ -50,10 +50,14 @@ struct mfac_window_s {
     float* G;
     hipStream_t st;
     int* err;
-    double *K, *A, *Linv, *part, *p, *R, *U, *work, *gpart;
+    double *K, *A, *Linv, *Ainv, *part, *p, *zv, *gpart;
     float* coef;
     int head;
     int64_t steps;
+    // coefficient policy: 0 = refactor from K on every replace; R > 0 = O(m^2)
+    // update of the explicit inverse, refactored from K every R replaces
+    int32_t period;
+    int32_t since_refactor;
     // phase tracing (host side): events recorded around the phases
     bool trace;
     struct Mark {
@@ -87,10 +91,9 @@ size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
     double* A = c.take<double>((size_t)mp * mp);
     double* Linv = c.take<double>((size_t)mp * mp);
     double* part = c.take<double>((size_t)PASS1_MAX_GRID * m * nvmax);
+    double* Ainv = c.take<double>((size_t)mp * mp);
     double* p = c.take<double>((size_t)m * nvmax);
-    double* R = c.take<double>((size_t)mp * nvmax);
-    double* U = c.take<double>((size_t)mp * nvmax);
-    double* work = c.take<double>((size_t)mp * nvmax);
+    double* zv = c.take<double>((size_t)mp * 2);
     float* coef = c.take<float>((size_t)m * nvmax);
     double* gpart = c.take<double>((size_t)gram_window_part_doubles(m, nslab_of(d)));
     if (w) {
@@ -99,10 +102,9 @@ size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
         w->A = A;
         w->Linv = Linv;
         w->part = part;
+        w->Ainv = Ainv;
         w->p = p;
-        w->R = R;
-        w->U = U;
-        w->work = work;
+        w->zv = zv;
         w->coef = coef;
         w->gpart = gpart;
     }
@@ -138,9 +140,24 @@ hipError_t mark_end(mfac_window w, int phase) {
     return e;
 }
 
+// Full refactor from K (optionally after replacing row/column k with p):
+// A = K + m*lambda*I, A = L L^T, Linv = L^-1, Ainv = Linv^T Linv.
 mfac_status window_factor(mfac_window w, const double* p, int pstride, int k) {
     HIPCHK(launch_assemble(w->K, w->m, p, pstride, k, (double)w->m * w->lambda, w->A, w->mp, w->err, w->st));
     HIPCHK(launch_potrf(w->A, w->Linv, w->mp, 1, 0, w->err, w->st));
+    HIPCHK(launch_trtri(w->A, w->Linv, w->mp, 1, 0, w->st));
+    HIPCHK(launch_lauum(w->Linv, w->Ainv, w->mp, 1, 0, w->st));
+    w->since_refactor = 0;
+    return MFAC_OK;
+}
+
+// Coefficients after slot k took a gradient with Gram column p: O(m^2) update
+// of the inverse, or a full refactor when the policy asks for one.
+mfac_status window_slot_update(mfac_window w, int pstride, int k) {
+    if (w->period == 0 || w->since_refactor + 1 >= w->period) return window_factor(w, w->p, pstride, k);
+    HIPCHK(launch_inv_replace(w->K, w->m, w->p, pstride, k, (double)w->m * w->lambda, w->Ainv, w->mp, w->zv,
+                              w->zv + w->mp, w->err, w->st));
+    w->since_refactor += 1;
     return MFAC_OK;
 }
 
@@ -197,6 +214,7 @@ MFAC_API mfac_status mfac_window_init(mfac_window* out, int64_t d, int32_t m, do
     w->nslab = nslab_of(d);
     w->G = (float*)storage;
     w->st = stream;
+    w->period = m > 1024 ? m : 1024;
     window_layout<mfac_window_s>(d, m, max_queries, (char*)workspace, w);
 
     mfac_status rc = MFAC_OK;
@@ -251,12 +269,10 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
     HIPCHK(launch_reduce_partials(w->part, grid, w->m * nv, w->p, w->st));
-    mfac_status rc = window_factor(w, w->p, nv, k);
+    mfac_status rc = window_slot_update(w, nv, k);
     if (rc != MFAC_OK) return rc;
 
     if (y_out || n > 0) {
-        HIPCHK(launch_build_rhs(w->p, w->m, nv, k, w->R, w->mp, w->st));
-        HIPCHK(launch_chol_solve(w->A, w->Linv, w->mp, nv, w->R, w->U, w->work, w->st));
         // column 0: c' = -m A^-1 e_k, so y = -G^T c' = m G^T A^-1 e_k;
         // queries: C = lambda^-1 A^-1 P, y = x / lambda - G^T C
         const double inv_lam = 1.0 / w->lambda;
@@ -270,10 +286,12 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
             vout.alpha[nv2] = v == 0 ? 0.0f : (float)inv_lam;
         }
         if (v0 == 0) {
-            HIPCHK(launch_coef(w->U, w->m, w->mp, nv, -(double)w->m, inv_lam, w->coef, w->err, w->st));
+            HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p, nv, nv, k, -(double)w->m, inv_lam, w->coef,
+                                        w->err, w->st));
         } else {
-            // no y_out: coefficients of the queries only (columns 1..n of U)
-            HIPCHK(launch_coef(w->U + w->mp, w->m, w->mp, nv2, inv_lam, inv_lam, w->coef, w->err, w->st));
+            // no y_out: coefficients of the queries only (columns 1..n of p)
+            HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p + 1, nv, nv2, -1, inv_lam, inv_lam, w->coef,
+                                        w->err, w->st));
         }
         HIPCHK(mark_end(w, 1));
         HIPCHK(mark_begin(w));
@@ -308,9 +326,7 @@ MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* 
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
     HIPCHK(launch_reduce_partials(w->part, grid, w->m * n, w->p, w->st));
-    HIPCHK(launch_build_rhs(w->p, w->m, n, -1, w->R, w->mp, w->st));
-    HIPCHK(launch_chol_solve(w->A, w->Linv, w->mp, n, w->R, w->U, w->work, w->st));
-    HIPCHK(launch_coef(w->U, w->m, w->mp, n, inv_lam, inv_lam, w->coef, w->err, w->st));
+    HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p, n, n, -1, inv_lam, inv_lam, w->coef, w->err, w->st));
     HIPCHK(mark_end(w, 1));
     HIPCHK(mark_begin(w));
     HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, n, w->coef, vout, al, w->st));
@@ -337,6 +353,12 @@ MFAC_API mfac_status mfac_window_set_head(mfac_window w, int32_t head, int64_t s
     if (!w || head < 0 || head >= w->m || steps < 0) return MFAC_EINVAL;
     w->head = head;
     w->steps = steps;
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_window_set_refactor_period(mfac_window w, int32_t period) {
+    if (!w || period < 0) return MFAC_EINVAL;
+    w->period = period;
     return MFAC_OK;
 }
 

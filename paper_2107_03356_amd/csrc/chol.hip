@@ -145,16 +145,29 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
         __syncthreads();
     }
     if (bad) atomicOr(err, 2);
-    // column i of the inverse of the lower factor, by forward substitution
-    for (int r = 0; r < 64; ++r) I[r][i] = 0.0;
+    // Column i of the inverse of the lower factor by forward substitution,
+    // kept in registers: x_r = (delta_ri - sum_{l<r} T[r][l] x_l) / T[r][r].
+    // Rows above i come out as exact zeros. Reads of T[r][l] are the same
+    // address across the wave (LDS broadcast); the dot products use four
+    // partial sums so consecutive FMAs do not wait on each other.
     {
-        const int c = i;
-        I[c][c] = 1.0 / T[c][c];
-        for (int r = c + 1; r < 64; ++r) {
-            double s = 0.0;
-            for (int l = c; l < r; ++l) s += T[r][l] * I[l][c];
-            I[r][c] = -s / T[r][r];
+        double x[64];
+#pragma unroll
+        for (int r = 0; r < 64; ++r) {
+            double s0 = (r == i) ? 1.0 : 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+#pragma unroll
+            for (int l = 0; l + 3 < r; l += 4) {
+                s0 -= T[r][l] * x[l];
+                s1 -= T[r][l + 1] * x[l + 1];
+                s2 -= T[r][l + 2] * x[l + 2];
+                s3 -= T[r][l + 3] * x[l + 3];
+            }
+#pragma unroll
+            for (int l = r & ~3; l < r; ++l) s0 -= T[r][l] * x[l];
+            x[r] = ((s0 + s1) + (s2 + s3)) / T[r][r];
         }
+#pragma unroll
+        for (int r = 0; r < 64; ++r) I[r][i] = x[r];
     }
     __syncthreads();
     for (int c = 0; c < 64; ++c) {
@@ -241,90 +254,134 @@ __global__ __launch_bounds__(256) void k_zero_upper(double* __restrict__ Linv, i
     for (int e = threadIdx.x; e < 4096; e += 256) C[(int64_t)(e >> 6) * mp + (e & 63)] = 0.0;
 }
 
-// ------------------------------------------------------------------ solves
+// ------------------------------------------------------------------ explicit inverse
+// Ainv = (A)^-1 = Linv^T Linv, tile (I, J) = sum_{K >= max(I,J)} Linv[K,I]^T Linv[K,J].
+// grid (T*T, nbatch).
+__global__ __launch_bounds__(256) void k_lauum(const double* __restrict__ Linv, double* __restrict__ Ainv, int mp,
+                                               int64_t bstride) {
+    __shared__ double Sa[64][P];
+    __shared__ double Sb[64][P];
+    const int T = mp / 64;
+    const int I = blockIdx.x / T, J = blockIdx.x % T;
+    const double* Lb = Linv + (int64_t)blockIdx.y * bstride;
+    v4d acc[2][2];
+    zero_acc(acc);
+    for (int K = (I > J ? I : J); K < T; ++K) {
+        stage_tile_t(Sa, Lb + (int64_t)K * 64 * mp + I * 64, mp);
+        stage_tile_t(Sb, Lb + (int64_t)K * 64 * mp + J * 64, mp);
+        __syncthreads();
+        mma_nt(Sa, Sb, acc);
+        __syncthreads();
+    }
+    double* C = Ainv + (int64_t)blockIdx.y * bstride + (int64_t)I * 64 * mp + J * 64;
+    for_acc(acc, [&](int row, int col, double v) { C[(int64_t)row * mp + col] = v; });
+}
+
 __device__ __forceinline__ double wave_sum_d(double x) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
     return x;
 }
 
-// One work-group per right-hand side: U[:,c] = (L L^T)^-1 R[:,c].
-// Forward z = L^-1 r by tile rows (wave per row of the off-diagonal
-// product, lanes along the row), then backward u = L^-T z by tile columns
-// (lanes along columns). Diagonal tiles use the stored inverses.
-__global__ __launch_bounds__(256) void k_chol_solve(const double* __restrict__ L,
-                                                    const double* __restrict__ Linv, int mp,
-                                                    const double* __restrict__ R, double* __restrict__ U,
-                                                    double* __restrict__ work) {
-    __shared__ double v[64];
-    __shared__ double part[4][64];
-    const int c = blockIdx.x;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// Slot k takes a new gradient whose Gram column is p (p[j*pstride], p_k = |g|^2).
+// Writes row/column k of K, z = Ainv b (b = p off slot k, 0 at k) and
+// v = row k of Ainv (the old inverse's column k). One wave per row of Ainv.
+__global__ __launch_bounds__(256) void k_inv_gemv(double* __restrict__ K, int m, const double* __restrict__ p,
+                                                  int pstride, int k, const double* __restrict__ Ainv, int mp,
+                                                  double* __restrict__ z, double* __restrict__ v,
+                                                  int* __restrict__ err) {
+    const int lane = threadIdx.x & 63;
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= mp) return;
+    const double* row = Ainv + (int64_t)i * mp;
+    double s = 0.0;
+    for (int j = lane; j < m; j += 64)
+        if (j != k) s += row[j] * p[(int64_t)j * pstride];
+    s = wave_sum_d(s);
+    if (lane == 0) z[i] = s;
+    if (i == k) {
+        for (int j = lane; j < mp; j += 64) v[j] = row[j];
+    }
+    if (i < m && lane == 0) {
+        const double pi = p[(int64_t)i * pstride];
+        K[(int64_t)k * m + i] = pi;
+        K[(int64_t)i * m + k] = pi;
+        if (!isfinite(pi)) atomicOr(err, 1);
+    }
+}
+
+// Block-wide scalars of the slot update, computed identically by every
+// work-group (fixed order): t = v_k, zk = z_k, s = c - b^T u with
+// u = z - v zk / t and c = p_k + mu.
+__device__ void inv_update_scalars(const double* __restrict__ p, int pstride, int k, int m, double mu,
+                                   const double* __restrict__ z, const double* __restrict__ v, double* sh,
+                                   double& t, double& zk, double& s) {
+    t = v[k];
+    zk = z[k];
+    double acc = 0.0;
+    for (int j = threadIdx.x; j < m; j += 256)
+        if (j != k) acc += p[(int64_t)j * pstride] * (z[j] - v[j] * (zk / t));
+    acc = wave_sum_d(acc);
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    const double bu = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+    s = p[(int64_t)k * pstride] + mu - bu;
+}
+
+// Ainv <- Ainv - v v^T / v_k + w w^T / s,  w = u - e_k, u = z - v z_k / v_k:
+// the inverse with slot k removed (Schur complement of its old pivot) plus
+// the new column inserted (new pivot s >= m*lambda). grid (T*T).
+__global__ __launch_bounds__(256) void k_inv_update(const double* __restrict__ p, int pstride, int k, int m,
+                                                    double mu, const double* __restrict__ z,
+                                                    const double* __restrict__ v, double* __restrict__ Ainv,
+                                                    int mp, int* __restrict__ err) {
+    __shared__ double sh[4];
+    double t, zk, s;
+    inv_update_scalars(p, pstride, k, m, mu, z, v, sh, t, zk, s);
+    if (blockIdx.x == 0 && threadIdx.x == 0 && (!(s > 0.0) || !isfinite(s) || !(t > 0.0))) atomicOr(err, 16);
     const int T = mp / 64;
-    const double* r = R + (int64_t)c * mp;
-    double* z = work + (int64_t)c * mp;
-    double* u = U + (int64_t)c * mp;
-
-    for (int t = 0; t < T; ++t) {
-        // v = r_t - L[t, <t] z_<t
-        for (int rr = wave; rr < 64; rr += 4) {
-            const int row = t * 64 + rr;
-            double s = 0.0;
-            for (int k = lane; k < t * 64; k += 64) s += L[(int64_t)row * mp + k] * z[k];
-            s = wave_sum_d(s);
-            if (lane == 0) v[rr] = r[row] - s;
-        }
-        __syncthreads();
-        // z_t = Linv[t,t] v
-        for (int rr = wave; rr < 64; rr += 4) {
-            const int row = t * 64 + rr;
-            double s = Linv[(int64_t)row * mp + t * 64 + lane] * v[lane];
-            s = wave_sum_d(s);
-            if (lane == 0) z[row] = s;
-        }
-        __threadfence_block();
-        __syncthreads();
-    }
-    for (int t = T - 1; t >= 0; --t) {
-        // w = z_t - L[>t, t]^T u_>t   (lanes over the 64 columns of tile column t)
-        double s = 0.0;
-        for (int row = (t + 1) * 64 + wave; row < mp; row += 4) s += L[(int64_t)row * mp + t * 64 + lane] * u[row];
-        part[wave][lane] = s;
-        __syncthreads();
-        if (wave == 0) v[lane] = z[t * 64 + lane] - (part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane]);
-        __syncthreads();
-        // u_t = Linv[t,t]^T w
-        if (wave == 0) {
-            double a = 0.0;
-            for (int k = 0; k < 64; ++k) a += Linv[(int64_t)(t * 64 + k) * mp + t * 64 + lane] * v[k];
-            u[t * 64 + lane] = a;
-        }
-        __threadfence_block();
-        __syncthreads();
+    const int I = blockIdx.x / T, J = blockIdx.x % T;
+    const double r = zk / t, it = 1.0 / t, is = 1.0 / s;
+    for (int e = threadIdx.x; e < 4096; e += 256) {
+        const int i = I * 64 + (e >> 6), j = J * 64 + (e & 63);
+        const double wi = z[i] - v[i] * r - (i == k ? 1.0 : 0.0);
+        const double wj = z[j] - v[j] * r - (j == k ? 1.0 : 0.0);
+        double* a = Ainv + (int64_t)i * mp + j;
+        *a = *a - v[i] * v[j] * it + wi * wj * is;
     }
 }
 
-__global__ __launch_bounds__(256) void k_build_rhs(const double* __restrict__ p, int m, int nv, int k,
-                                                   double* __restrict__ R, int mp) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= (int64_t)mp * nv) return;
-    const int v = (int)(e / mp), i = (int)(e % mp);
-    double x;
-    if (k >= 0 && v == 0)
-        x = (i == k) ? 1.0 : 0.0;
-    else
-        x = (i < m) ? p[(int64_t)i * nv + v] : 0.0;
-    R[e] = x;
-}
-
-__global__ __launch_bounds__(256) void k_coef(const double* __restrict__ U, int m, int mp, int nv, double s0,
-                                              double s1, float* __restrict__ coef, int* __restrict__ err) {
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    if (e >= m * nv) return;
-    const int i = e / nv, v = e % nv;
-    const double x = U[(int64_t)v * mp + i] * (v == 0 ? s0 : s1);
-    if (!isfinite(x)) atomicOr(err, 4);
-    coef[e] = (float)x;
+// coef[i*nv + c] = scale_c * (Ainv rhs_c)_i with rhs_0 = e_k when k >= 0,
+// the other columns p[j*pstride + c]; one wave per row i, lanes along the row.
+__global__ __launch_bounds__(256) void k_coef_from_inv(const double* __restrict__ Ainv, int mp, int m,
+                                                       const double* __restrict__ p, int pstride, int nv, int k,
+                                                       double s0, double s1, float* __restrict__ coef,
+                                                       int* __restrict__ err) {
+    const int lane = threadIdx.x & 63;
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= m) return;
+    const double* row = Ainv + (int64_t)i * mp;
+    double acc[MAXNV];
+#pragma unroll
+    for (int c = 0; c < MAXNV; ++c) acc[c] = 0.0;
+    const int c0 = k >= 0 ? 1 : 0;
+    for (int j = lane; j < m; j += 64) {
+        const double a = row[j];
+#pragma unroll
+        for (int c = 0; c < MAXNV; ++c)
+            if (c >= c0 && c < nv) acc[c] += a * p[(int64_t)j * pstride + c];
+    }
+#pragma unroll
+    for (int c = 0; c < MAXNV; ++c) {
+        if (c < nv) {
+            double x = (c < c0) ? row[k] : wave_sum_d(acc[c]);
+            x *= (c == 0 ? s0 : s1);
+            if (lane == 0) {
+                if (!isfinite(x)) atomicOr(err, 4);
+                coef[i * nv + c] = (float)x;
+            }
+        }
+    }
 }
 
 }  // namespace
@@ -369,22 +426,27 @@ hipError_t launch_trtri(const double* L, double* Linv, int mp, int nbatch, int64
     return hipSuccess;
 }
 
-hipError_t launch_chol_solve(const double* L, const double* Linv, int mp, int nrhs, const double* R,
-                             double* U, double* work, hipStream_t st) {
-    hipLaunchKernelGGL(k_chol_solve, dim3(nrhs), dim3(256), 0, st, L, Linv, mp, R, U, work);
+hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, int64_t bstride, hipStream_t st) {
+    const int T = mp / 64;
+    hipLaunchKernelGGL(k_lauum, dim3(T * T, nbatch), dim3(256), 0, st, Linv, Ainv, mp, bstride);
     return hipGetLastError();
 }
 
-hipError_t launch_build_rhs(const double* p, int m, int nv, int k, double* R, int mp, hipStream_t st) {
-    const int64_t n = (int64_t)mp * nv;
-    hipLaunchKernelGGL(k_build_rhs, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, st, p, m, nv, k, R, mp);
+hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, int k, double mu, double* Ainv,
+                              int mp, double* z, double* v, int* err, hipStream_t st) {
+    hipLaunchKernelGGL(k_inv_gemv, dim3((unsigned)ceil_div(mp, 4)), dim3(256), 0, st, K, m, p, pstride, k, Ainv, mp,
+                       z, v, err);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int T = mp / 64;
+    hipLaunchKernelGGL(k_inv_update, dim3(T * T), dim3(256), 0, st, p, pstride, k, m, mu, z, v, Ainv, mp, err);
     return hipGetLastError();
 }
 
-hipError_t launch_coef(const double* U, int m, int mp, int nv, double s0, double s1, float* coef, int* err,
-                       hipStream_t st) {
-    hipLaunchKernelGGL(k_coef, dim3((unsigned)ceil_div((int64_t)m * nv, 256)), dim3(256), 0, st, U, m, mp, nv,
-                       s0, s1, coef, err);
+hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double* p, int pstride, int nv, int k,
+                                double s0, double s1, float* coef, int* err, hipStream_t st) {
+    hipLaunchKernelGGL(k_coef_from_inv, dim3((unsigned)ceil_div(m, 4)), dim3(256), 0, st, Ainv, mp, m, p, pstride, nv,
+                       k, s0, s1, coef, err);
     return hipGetLastError();
 }
 

@@ -73,16 +73,16 @@ hipError_t launch_potrf(double* A, double* Linv, int mp, int nbatch, int64_t bst
 // Off-diagonal blocks of Linv = L^-1 (diagonal blocks from launch_potrf).
 hipError_t launch_trtri(const double* L, double* Linv, int mp, int nbatch, int64_t bstride,
                         hipStream_t st);
-// Solve L L^T U = R for nrhs columns (R and U: mp x nrhs, column c at c*mp).
-hipError_t launch_chol_solve(const double* L, const double* Linv, int mp, int nrhs,
-                             const double* R, double* U, double* work, hipStream_t st);
-// Dynamic right-hand sides and coefficients:
-// rhs column 0 = e_k (if k >= 0), columns v >= v0: p[:, v] (mp x nv layout).
-hipError_t launch_build_rhs(const double* p, int m, int nv, int k, double* R, int mp,
-                            hipStream_t st);
-// coef[i*nv+v] = scale_v * U[v*mp+i]  (fp32)
-hipError_t launch_coef(const double* U, int m, int mp, int nv, double s0, double s1,
-                       float* coef, int* err, hipStream_t st);
+// Ainv = Linv^T Linv (the explicit inverse of A = L L^T), full mp x mp.
+hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, int64_t bstride, hipStream_t st);
+// O(m^2) slot replacement: K row/column k <- p and Ainv <- (A with column k
+// replaced)^-1; z, v: mp-double scratch vectors.
+hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, int k, double mu, double* Ainv,
+                              int mp, double* z, double* v, int* err, hipStream_t st);
+// coef[i*nv+c] = scale_c (Ainv rhs_c)_i: rhs_0 = e_k if k >= 0 (scale s0); the
+// other columns rhs_c[j] = p[j*pstride + c] (scale s1; also column 0 if k < 0).
+hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double* p, int pstride, int nv, int k,
+                                double s0, double s1, float* coef, int* err, hipStream_t st);
 
 // ---------------------------------------------------------------- static
 // W_b = Linv_b G_b in place over G (fp32), colsum of squares in fp64 -> diag

@@ -212,3 +212,48 @@ def test_nonfinite_latched_and_rebuild_recovers(dev):
     x = gs.queries(0, 1)
     y = win.ihvp(x.to(dev))
     assert rel_l2(y[0].cpu().numpy(), orc.ihvp(x[0].numpy())) < REL_TOL
+
+
+@pytest.mark.parametrize("period", [0, 1, 3])
+def test_refactor_policies(dev, period):
+    """Per-replace refactor (period 0/1) and a refactor every 3 replaces agree with the oracle."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=9000, m=80, scale_d=base.d)
+    gs = GradientStream(wl, seed=13)
+    G0 = gs.window()
+    say("refactor policy", period)
+    win = Window(wl.d, wl.m, wl.lam, max_queries=2, G0=G0.to(dev), device=dev)
+    win.set_refactor_period(period)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    for t in range(10):
+        g = gs.row(wl.m + t)
+        X = gs.queries(t, 2)
+        y, Y = win.replace(g.to(dev), X=X.to(dev))
+        yo = orc.slide(g.numpy())
+        Yo = orc.ihvp(X.numpy())
+        assert rel_l2(y.cpu().numpy(), yo) < REL_TOL
+        assert max(rel_l2(Y[q].cpu().numpy(), Yo[q]) for q in range(2)) < REL_TOL
+    assert win.status() == 0
+
+
+def test_long_run_inverse_updates_do_not_drift(dev):
+    """400 O(m^2) inverse updates (over six trips round a 64-slot ring) without a refactor."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_resnet50_d25.6m_m1024")
+    wl = base.scaled(d=16384, m=64, lam=1e-4, scale_d=base.d // 64)
+    gs = GradientStream(wl, seed=14)
+    G0 = gs.window()
+    say("long run drift")
+    win = Window(wl.d, wl.m, wl.lam, G0=G0.to(dev), device=dev)
+    win.set_refactor_period(100000)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    errs = []
+    for t in range(400):
+        g = gs.row(wl.m + t)
+        y = win.replace(g.to(dev))
+        yo = orc.slide(g.numpy())
+        if t % 25 == 24:
+            errs.append(rel_l2(y.cpu().numpy(), yo))
+    assert win.status() == 0
+    assert max(errs) < 1e-5, errs
