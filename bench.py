@@ -33,13 +33,13 @@ def log(*a):
 
 
 def pass_bytes(d, m):
-    """Algorithmic HBM bytes of one launch of each streaming pass (fp32).
+    """Algorithmic HBM bytes of one launch of each step kernel that touches d (fp32).
 
-    pass 1: reads the m-1 other rows and the new gradient, writes the new row:
-            (m - 1) d + d + d = (m + 1) d floats
-    pass 2: reads all m rows, writes y: (m + 1) d floats
+    row write: reads g, writes it into the slot: 2 d floats
+    pass 1:    reads all m rows and g: (m + 1) d floats
+    pass 2:    reads all m rows, writes y: (m + 1) d floats
     """
-    return 4 * (m + 1) * d, 4 * (m + 1) * d
+    return 4 * (m + 1) * d, 4 * (m + 1) * d, 4 * 2 * d
 
 
 def read_counters(kernel):
@@ -141,7 +141,9 @@ def main():
     for r0 in range(0, m, batch):
         n = min(batch, m - r0)
         win.set_rows(r0, gs.rows(r0, n))
+        log(f"window rows {r0 + n}/{m}")
     win.rebuild()
+    log("Gram + factor done")
     nsteps = args.warmup + args.steps
     steps_g = torch.empty((nsteps, d), dtype=torch.float32, device=dev)
     for t in range(nsteps):
@@ -167,6 +169,11 @@ def main():
         step(t)
     torch.cuda.synchronize()
     log("warmup done")
+    # a plain copy of known size (k_get_rows: 8 window rows -> row-major, 8*d*4
+    # bytes read and written); HBM counter runs use it to scale FETCH/WRITE_SIZE
+    calib_rows = min(m, 8)
+    del_rows = win.get_rows(0, calib_rows)
+    del del_rows
 
     # ---- timed region: K steps, HIP events on the library's stream (torch's current stream)
     win.trace_read()   # drop any earlier marks
@@ -191,12 +198,12 @@ def main():
     log(f"timed {args.steps} steps: {ms_total:.1f} ms (wall {wall * 1e3:.1f} ms)")
 
     ms_step = ms_total / args.steps
-    b1, b2 = pass_bytes(d, m)
+    b1, b2, bw = pass_bytes(d, m)
     if nq:
         b1 += 4 * nq * d
         b2 += 4 * 2 * nq * d
-    step_bytes = b1 + b2
-    avg = [ph_ms[i] / max(ph_cnt[i], 1) for i in range(3)]
+    step_bytes = b1 + b2 + bw
+    avg = [ph_ms[i] / max(ph_cnt[i], 1) for i in range(4)]
     gbs1 = b1 / (avg[0] * 1e-3) / 1e9
     gbs2 = b2 / (avg[2] * 1e-3) / 1e9
     dominant = 0 if ph_ms[0] >= ph_ms[2] else 2
@@ -224,7 +231,7 @@ def main():
             "parallelism": "single GPU",
         },
         "achieved_hbm_gbs_step": step_bytes / (ms_step * 1e-3) / 1e9,
-        "phases_ms_per_step": {"pass1": avg[0], "coefficients": avg[1], "pass2": avg[2]},
+        "phases_ms_per_step": {"row_write": avg[3], "pass1": avg[0], "coefficients": avg[1], "pass2": avg[2]},
         "pass_gbs": {"k_pass1": gbs1, "k_pass2": gbs2},
         "roofline": {
             "bound": "hbm",
@@ -236,6 +243,7 @@ def main():
             "traffic": traffic,
         },
         "cpu_baseline": None,
+        "calib_copy": {"kernel": "k_get_rows", "bytes_read": 4 * calib_rows * d, "bytes_written": 4 * calib_rows * d},
     }
     if not args.no_cpu_baseline:
         del steps_g, Xq, win

@@ -150,11 +150,12 @@ mfac_status mfac_window_set_refactor_period(mfac_window w, int32_t period);
 mfac_status mfac_window_set_stream(mfac_window w, hipStream_t stream);
 
 /* Phase timing with HIP events recorded on the handle's stream (a tracing aid,
- * off by default). Phases: 0 = pass-1 kernel (G x and the row write),
- * 1 = coefficient phase (partial-sum reduction, Gram row, factor, solves),
- * 2 = pass-2 kernel (G^T c). enable != 0 starts recording around every
- * replace and ihvp; 0 stops (recorded events are kept until read). */
-#define MFAC_NPHASES 3
+ * off by default). Phases: 0 = pass-1 kernel (G x), 1 = coefficient phase
+ * (partial-sum reduction, Gram row, inverse update or refactor, coefficients),
+ * 2 = pass-2 kernel (G^T c), 3 = the write of the new gradient into its slot.
+ * enable != 0 starts recording around every replace and ihvp; 0 stops
+ * (recorded events are kept until read). */
+#define MFAC_NPHASES 4
 mfac_status mfac_window_trace(mfac_window w, int32_t enable);
 
 /* Synchronise the stream, add up the recorded phase times: ms_out and

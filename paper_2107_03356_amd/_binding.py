@@ -211,9 +211,10 @@ class Window:
         _check("mfac_window_trace", load().mfac_window_trace(self.handle, 1 if enable else 0))
 
     def trace_read(self):
-        """(ms per phase, launches per phase) since the last read; phases: pass 1, coefficients, pass 2."""
-        ms = (ctypes.c_double * 3)()
-        cnt = (ctypes.c_int64 * 3)()
+        """(ms per phase, launches per phase) since the last read; phases: pass 1,
+        coefficients, pass 2, row write."""
+        ms = (ctypes.c_double * 4)()
+        cnt = (ctypes.c_int64 * 4)()
         _check("mfac_window_trace_read", load().mfac_window_trace_read(self.handle, ms, cnt))
         return list(ms), list(cnt)
 

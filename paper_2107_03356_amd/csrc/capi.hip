@@ -265,7 +265,10 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
 
     int grid = 0;
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, nv, vin, al, w->G, k, w->part, &grid, w->st));
+    HIPCHK(launch_write_row(w->G, w->m, d, w->nslab, k, g_new, w->st));
+    HIPCHK(mark_end(w, 3));
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, nv, vin, al, w->part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
     HIPCHK(launch_reduce_partials(w->part, grid, w->m * nv, w->p, w->st));
@@ -322,7 +325,7 @@ MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* 
     }
     int grid = 0;
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, n, vin, al, nullptr, -1, w->part, &grid, w->st));
+    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, n, vin, al, w->part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
     HIPCHK(launch_reduce_partials(w->part, grid, w->m * n, w->p, w->st));

@@ -38,11 +38,12 @@ hipError_t launch_set_rows(float* G, int m, int64_t d, int64_t nslab, int first,
                            const float* rows, int64_t ld, hipStream_t st);
 hipError_t launch_get_rows(const float* G, int m, int64_t d, int first, int count,
                            float* rows, int64_t ld, hipStream_t st);
+// Row k of the window <- g (d floats; zero padding past d).
+hipError_t launch_write_row(float* G, int m, int64_t d, int64_t nslab, int k, const float* g, hipStream_t st);
 // Pass 1: part[b][i*nv+v] = partial sums of G[i,:] . vec_v over the chunks of
-// work-group b; optionally writes vec_0 into row wslot first. Returns grid size.
+// work-group b. Returns the grid size.
 hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv,
-                        const VecIn& vin, bool aligned, float* Gw, int wslot,
-                        double* part, int* grid_out, hipStream_t st);
+                        const VecIn& vin, bool aligned, double* part, int* grid_out, hipStream_t st);
 // p[t] = sum_b part[b][t] for t < mnv (fixed order, fp64)
 hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double* p,
                                   hipStream_t st);

@@ -6,20 +6,33 @@
 // column slabs (internal.h), so every wave reads rows of 8 KB contiguous and
 // all rows of a slab lie in one contiguous m*8 KB region.
 //
+// A replace first writes the new gradient into its slot (k_write_row, 2 d
+// floats of traffic), so both passes below are pure read streams: interleaving
+// that write with pass 1's reads cost ~8% of pass 1's bandwidth on gfx950.
+//
 // Pass 1: every work-group owns a set of column chunks and keeps per-row
 // running sums in LDS. For each row a wave loads U float4 per lane (128-bit
 // coalesced loads), multiplies with the register-resident vector chunks and
-// reduces across the wave with lane shuffles. The replaced row is never read:
-// the new gradient is taken from registers and written into the slot in the
-// same pass. Work-group partials go to a [grid][m*nv] fp64 buffer, summed in
-// a fixed order by the reduce kernel (deterministic, no float atomics).
+// reduces across the wave with lane shuffles. Work-group partials go to a
+// [grid][m*nv] fp64 buffer, summed in a fixed order by the reduce kernel
+// (deterministic, no float atomics).
 //
 // Pass 2: each wave owns one column chunk of the output and walks all m rows,
-// accumulating coef[i] * G[i, chunk] in registers; no cross-lane traffic.
+// accumulating coef[i] * G[i, chunk] in registers (coefficients staged in LDS);
+// no cross-lane traffic.
 #include "internal.h"
 
 namespace mfac {
 namespace {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// Window rows are read exactly once per pass: nontemporal loads stream them
+// past the caches (measured +15-20% HBM throughput on gfx950 for these passes).
+__device__ __forceinline__ float4 ld_stream(const float* __restrict__ p) {
+    const f4v v = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
 
 __device__ __forceinline__ float4 ld4(const float* __restrict__ p, int64_t j, int64_t d, int aligned) {
     if (aligned && j + 3 < d) return *reinterpret_cast<const float4*>(p + j);
@@ -54,6 +67,49 @@ __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
     return x;
+}
+
+// Sum N per-lane values over the 64 lanes of a wave in about N + 5 shuffles
+// (instead of 6 N): at each halving step a lane keeps half of its pending sums
+// and trades the other half with its partner lane (lane ^ O), so the number of
+// pending values halves while the lanes covered double. Once one value is
+// left, plain butterfly steps finish the sum. On return the lane holds the
+// total of value `base`; exactly one lane per value has writer == true.
+template <int N, int C, int O>
+struct WaveReduceMany {
+    static __device__ __forceinline__ void run(float (&s)[N], int lane, int& base, int& creal, bool& dup) {
+        if constexpr (O > 0) {
+            const bool up = (lane & O) != 0;
+            if constexpr (C > 1) {
+                constexpr int H = (C + 1) / 2;
+#pragma unroll
+                for (int j = 0; j < H; ++j) {
+                    const float lo = s[j];
+                    const float hi = (H + j < C) ? s[(H + j < N) ? H + j : N - 1] : 0.f;
+                    const float send = up ? lo : hi;
+                    const float keep = up ? hi : lo;
+                    s[j] = keep + __shfl_xor(send, O, 64);
+                }
+                base += up ? H : 0;
+                creal = up ? (creal > H ? creal - H : 0) : (creal < H ? creal : H);
+                WaveReduceMany<N, H, O / 2>::run(s, lane, base, creal, dup);
+            } else {
+                s[0] += __shfl_xor(s[0], O, 64);
+                dup = dup || up;
+                WaveReduceMany<N, 1, O / 2>::run(s, lane, base, creal, dup);
+            }
+        }
+    }
+};
+
+template <int N>
+__device__ __forceinline__ float wave_reduce_many(float (&s)[N], int lane, int& base, bool& writer) {
+    base = 0;
+    int creal = N;
+    bool dup = false;
+    WaveReduceMany<N, N, 32>::run(s, lane, base, creal, dup);
+    writer = !dup && creal > 0;
+    return s[0];
 }
 
 __global__ void k_fill_zero(float* __restrict__ p, int64_t n) {
@@ -91,7 +147,6 @@ __global__ __launch_bounds__(256) void k_get_rows(const float* __restrict__ G, i
 template <int NV, int U>
 __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int m, int64_t d,
                                                int64_t nchunk, VecIn vin, int aligned,
-                                               float* __restrict__ Gw, int wslot,
                                                double* __restrict__ part) {
     extern __shared__ float acc[];  // m * NV running sums
     constexpr int CW = 256 * U;     // chunk width (floats): 64 lanes x float4 x U
@@ -115,34 +170,21 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
 #pragma unroll
             for (int u = 0; u < U; ++u) vr[v][u] = ld4(vin.v[v], j0 + u * 256 + lane * 4, d, aligned);
 
-        if (wslot >= 0 && wave == 0) {
-            float* dst = Gw + slab * (int64_t)m * SLAB + (int64_t)wslot * SLAB + off + lane * 4;
-#pragma unroll
-            for (int u = 0; u < U; ++u) *reinterpret_cast<float4*>(dst + u * 256) = vr[0][u];
-        }
-
-        // two rows per iteration: rows i and i + 4 handled by this wave
+        // two rows per iteration: rows i and i + 4 of this wave; a missing
+        // second row re-reads row i and its sum is dropped (no branch around loads)
         for (int i = wave; i < m; i += 8) {
-            const int i2 = i + 4;
-            const bool has2 = i2 < m;
+            const bool has2 = i + 4 < m;
+            const int i2 = has2 ? i + 4 : i;
             float4 ga[U], gb[U];
-            if (i != wslot) {
 #pragma unroll
-                for (int u = 0; u < U; ++u)
-                    ga[u] = *reinterpret_cast<const float4*>(Gs + (int64_t)i * SLAB + u * 256);
-            } else {
+            for (int u = 0; u < U; ++u) ga[u] = ld_stream(Gs + (int64_t)i * SLAB + u * 256);
 #pragma unroll
-                for (int u = 0; u < U; ++u) ga[u] = vr[0][u];
-            }
-            if (has2 && i2 != wslot) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    gb[u] = *reinterpret_cast<const float4*>(Gs + (int64_t)i2 * SLAB + u * 256);
-            } else {
-#pragma unroll
-                for (int u = 0; u < U; ++u) gb[u] = vr[0][u];
-            }
-            float sa[NV], sb[NV];
+            for (int u = 0; u < U; ++u) gb[u] = ld_stream(Gs + (int64_t)i2 * SLAB + u * 256);
+            // keep all 2U loads in flight before the first use (the scheduler
+            // otherwise recycles a few load registers and waits on each load)
+            __builtin_amdgcn_sched_barrier(0);
+            // per-lane partial dots: rows i (values 0..NV-1) and i2 (NV..2NV-1)
+            float sv[2 * NV];
 #pragma unroll
             for (int v = 0; v < NV; ++v) {
                 float a = 0.f, b = 0.f;
@@ -151,15 +193,17 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
                     a = dot4(ga[u], vr[v][u], a);
                     b = dot4(gb[u], vr[v][u], b);
                 }
-                sa[v] = wave_sum(a);
-                sb[v] = wave_sum(b);
+                sv[v] = a;
+                sv[NV + v] = b;
             }
-            if (lane == 0) {
-#pragma unroll
-                for (int v = 0; v < NV; ++v) {
-                    acc[i * NV + v] += sa[v];
-                    if (has2) acc[i2 * NV + v] += sb[v];
-                }
+            int idx;
+            bool writer;
+            const float tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
+            if (writer) {
+                if (idx < NV)
+                    acc[i * NV + idx] += tot;
+                else if (has2)
+                    acc[i2 * NV + (idx - NV)] += tot;
             }
         }
     }
@@ -190,9 +234,12 @@ template <int NV, int U>
 __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int m, int64_t d,
                                                int64_t nwchunk, const float* __restrict__ coef,
                                                VecOut vout, int aligned) {
-    constexpr int WCW = 256 * U;  // wave chunk width (floats)
+    extern __shared__ float cl[];  // m * NV coefficients
+    constexpr int WCW = 256 * U;   // wave chunk width (floats)
     constexpr int CPS = SLAB / WCW;
     static_assert(SLAB % WCW == 0, "chunk must tile the slab");
+    for (int t = threadIdx.x; t < m * NV; t += 256) cl[t] = coef[t];
+    __syncthreads();
     const int lane = threadIdx.x & 63;
     const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (c >= nwchunk) return;
@@ -207,14 +254,37 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
 #pragma unroll
         for (int u = 0; u < U; ++u) acc[v][u] = make_float4(0.f, 0.f, 0.f, 0.f);
 
-#pragma unroll 2
-    for (int i = 0; i < m; ++i) {
+    // RB rows per batch: all RB*U loads are issued before the first FMA
+    constexpr int RB = 8;
+    int i = 0;
+    for (; i + RB <= m; i += RB) {
+        float4 g[RB][U];
+#pragma unroll
+        for (int r = 0; r < RB; ++r)
+#pragma unroll
+            for (int u = 0; u < U; ++u) g[r][u] = ld_stream(Gs + (int64_t)(i + r) * SLAB + u * 256);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int r = 0; r < RB; ++r)
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                const float cv = cl[(i + r) * NV + v];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    acc[v][u].x = fmaf(cv, g[r][u].x, acc[v][u].x);
+                    acc[v][u].y = fmaf(cv, g[r][u].y, acc[v][u].y);
+                    acc[v][u].z = fmaf(cv, g[r][u].z, acc[v][u].z);
+                    acc[v][u].w = fmaf(cv, g[r][u].w, acc[v][u].w);
+                }
+            }
+    }
+    for (; i < m; ++i) {
         float4 g[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) g[u] = *reinterpret_cast<const float4*>(Gs + (int64_t)i * SLAB + u * 256);
+        for (int u = 0; u < U; ++u) g[u] = ld_stream(Gs + (int64_t)i * SLAB + u * 256);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-            const float cv = coef[i * NV + v];
+            const float cv = cl[i * NV + v];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 acc[v][u].x = fmaf(cv, g[u].x, acc[v][u].x);
@@ -243,22 +313,34 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
     }
 }
 
+// The new gradient into row k of the window (padding past d stays zero).
+__global__ __launch_bounds__(256) void k_write_row(float* __restrict__ G, int m, int64_t d, int64_t ncolpad,
+                                                   int k, const float* __restrict__ g, int aligned) {
+    const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (j >= ncolpad) return;
+    const float4 v = ld4(g, j, d, aligned);
+    const int64_t slab = j / SLAB;
+    *reinterpret_cast<float4*>(G + slab * (int64_t)m * SLAB + (int64_t)k * SLAB + (j - slab * SLAB)) = v;
+}
+
 template <int NV>
 struct PassCfg {
-    // floats per lane per row: keep the register-resident vectors at <= ~72 VGPRs
-    static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 8 ? 2 : 1;
-    static constexpr int U2 = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 4 ? 2 : 1;
+    // float4 per lane per row. Pass 1 keeps the vector chunks in registers
+    // (<= ~72 VGPRs); pass 2 uses narrow 512-column wave chunks with 8 rows in
+    // flight, which measured fastest on the 105 GB window.
+    static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 9 ? 2 : 1;
+    static constexpr int U2 = NV <= 2 ? 2 : 1;
 };
 
 template <int NV>
 hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn& vin, bool aligned,
-                    float* Gw, int wslot, double* part, int* grid_out, hipStream_t st) {
+                    double* part, int* grid_out, hipStream_t st) {
     constexpr int U = PassCfg<NV>::U;
     const int64_t nchunk = nslab * (SLAB / (256 * U));
     const int grid = (int)(nchunk < PASS1_MAX_GRID ? nchunk : PASS1_MAX_GRID);
     const size_t lds = (size_t)m * NV * sizeof(float);
     hipLaunchKernelGGL((k_pass1<NV, U>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
-                       aligned ? 1 : 0, Gw, wslot, part);
+                       aligned ? 1 : 0, part);
     *grid_out = grid;
     return hipGetLastError();
 }
@@ -269,7 +351,8 @@ hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const float
     constexpr int U = PassCfg<NV>::U2;
     const int64_t nwchunk = nslab * (SLAB / (256 * U));
     const int64_t grid = ceil_div(nwchunk, 4);
-    hipLaunchKernelGGL((k_pass2<NV, U>), dim3((unsigned)grid), dim3(256), 0, st, G, m, d, nwchunk,
+    const size_t lds = (size_t)m * NV * sizeof(float);
+    hipLaunchKernelGGL((k_pass2<NV, U>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk,
                        coef, vout, aligned ? 1 : 0);
     return hipGetLastError();
 }
@@ -307,12 +390,19 @@ hipError_t launch_get_rows(const float* G, int m, int64_t d, int first, int coun
 #define MFAC_NV_CASES(X) \
     X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16) X(17)
 
+hipError_t launch_write_row(float* G, int m, int64_t d, int64_t nslab, int k, const float* g, hipStream_t st) {
+    const int64_t ncolpad = nslab * SLAB;
+    const bool aligned = ((uintptr_t)g % 16) == 0;
+    hipLaunchKernelGGL(k_write_row, dim3((unsigned)ceil_div(ncolpad / 4, 256)), dim3(256), 0, st, G, m, d, ncolpad,
+                       k, g, aligned ? 1 : 0);
+    return hipGetLastError();
+}
+
 hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv, const VecIn& vin,
-                        bool aligned, float* Gw, int wslot, double* part, int* grid_out,
-                        hipStream_t st) {
+                        bool aligned, double* part, int* grid_out, hipStream_t st) {
     switch (nv) {
 #define CASE(N) \
-    case N: return pass1_nv<N>(G, m, d, nslab, vin, aligned, Gw, wslot, part, grid_out, st);
+    case N: return pass1_nv<N>(G, m, d, nslab, vin, aligned, part, grid_out, st);
         MFAC_NV_CASES(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;
