@@ -18,6 +18,7 @@ G = 0, the matrix-free residual F y = x, and the paper's D/B/q recursion.
 
 import numpy as np
 import scipy.linalg as sla
+import torch
 
 _CHUNK = 1 << 18  # columns per fp64 chunk (bounds the fp64 temporaries)
 
@@ -27,22 +28,46 @@ def _chunks(d, chunk=_CHUNK):
         yield j0, min(d, j0 + chunk)
 
 
+class _F64Chunks:
+    """Column chunks of an fp32 matrix converted to float64 in one reused buffer.
+
+    The conversion is exact (every fp32 value is a float64 value); torch's
+    CPU copy does it with all threads and without fresh page faults.
+    """
+
+    def __init__(self, rows, chunk=_CHUNK):
+        self.buf = np.empty((rows, chunk), np.float64)
+        self.chunk = chunk
+
+    def __call__(self, A):
+        d = A.shape[1]
+        for j0, j1 in _chunks(d, self.chunk):
+            b = self.buf[:A.shape[0], :j1 - j0]
+            torch.from_numpy(b).copy_(torch.from_numpy(A[:, j0:j1]))
+            yield j0, j1, b
+
+
 def gram(G, chunk=_CHUNK):
-    """K = G G^T in float64 from fp32 rows, accumulated over column chunks."""
+    """K = G G^T in float64 from fp32 rows, accumulated over column chunks.
+
+    Each chunk's product is the BLAS symmetric rank-k update (dsyrk) of the
+    chunk in float64; only its lower triangle is formed, then mirrored.
+    """
     m, d = G.shape
-    K = np.zeros((m, m), np.float64)
-    for j0, j1 in _chunks(d, chunk):
-        Gc = G[:, j0:j1].astype(np.float64)
-        K += Gc @ Gc.T
-    return K
+    K = np.zeros((m, m), np.float64, order="F")
+    for _, _, b in _F64Chunks(m, chunk)(G):
+        K = sla.blas.dsyrk(1.0, b.T, beta=1.0, c=K, trans=1, lower=1, overwrite_c=1)
+    K = np.tril(K)
+    return np.ascontiguousarray(K + np.tril(K, -1).T)
 
 
 def matvec(G, X, chunk=_CHUNK):
-    """P = G X^T (m x n) in float64; X is (n, d)."""
+    """P = G X^T (m x n) in float64; X is (n, d) fp32."""
     m, d = G.shape
     P = np.zeros((m, X.shape[0]), np.float64)
-    for j0, j1 in _chunks(d, chunk):
-        P += G[:, j0:j1].astype(np.float64) @ X[:, j0:j1].astype(np.float64).T
+    conv = _F64Chunks(m, chunk)
+    for j0, j1, b in conv(G):
+        P += b @ X[:, j0:j1].astype(np.float64).T
     return P
 
 
@@ -81,11 +106,13 @@ class WindowOracle:
         """Ring semantics: replace the oldest slot (steps mod m), return F^-1 g.
 
         Section 4.2: the window drops its oldest gradient, takes the newest, and
-        the same newest gradient is then preconditioned.
+        the same newest gradient is then preconditioned. G g after the insert is
+        the Gram column the replace just computed (Appendix B reuses it the same
+        way), so it is passed on instead of being recomputed.
         """
         slot = self.steps % self.m
-        self.replace(slot, g)
-        return self.ihvp(np.asarray(g, np.float32)[None, :])[0]
+        p = self.replace(slot, g)
+        return self.ihvp(np.asarray(g, np.float32)[None, :], P=p[:, None])[0]
 
     def coefficients(self, P):
         """U = (K + m*lambda*I)^-1 P for P (m x n)."""
@@ -93,16 +120,19 @@ class WindowOracle:
         c, low = sla.cho_factor(A, lower=True)
         return sla.cho_solve((c, low), P)
 
-    def ihvp(self, X):
-        """F^-1 X for X of shape (d,) or (n, d); returns float64 of that shape."""
+    def ihvp(self, X, P=None):
+        """F^-1 X for X of shape (d,) or (n, d); returns float64 of that shape.
+
+        P = G X^T may be passed when already known.
+        """
         X = np.asarray(X, dtype=np.float32)
         single = X.ndim == 1
         if single:
             X = X[None, :]
-        P = matvec(self.G, X)
+        if P is None:
+            P = matvec(self.G, X)
         U = self.coefficients(P)
         Y = np.empty(X.shape, np.float64)
-        for j0, j1 in _chunks(self.d):
-            Gc = self.G[:, j0:j1].astype(np.float64)
-            Y[:, j0:j1] = (X[:, j0:j1].astype(np.float64) - U.T @ Gc) / self.lam
+        for j0, j1, b in _F64Chunks(self.m)(self.G):
+            Y[:, j0:j1] = (X[:, j0:j1].astype(np.float64) - U.T @ b) / self.lam
         return Y[0] if single else Y
