@@ -115,7 +115,9 @@ def bench_static(args, wl, dev):
 
     P.load()
     d, m, B = wl.d, wl.m, wl.block
-    flops = 2.0 * m * m * d + m ** 3 * (d // B) / 3.0 * 2 + 2.0 * m * m * d / 2
+    # algorithmic flops per run: symmetric Gram m^2 B and triangular W = L^-1 G_b
+    # m^2 B per block (2 m^2 d together), Cholesky and triangular inverse m^3/3 each
+    flops = 2.0 * m * m * d + 2.0 * (m ** 3 / 3.0) * (d // B)
     t0 = time.perf_counter()
     gs = GradientStream(wl, seed=args.seed, device=dev)
     G0 = torch.empty((m, d), dtype=torch.float32, device=dev)
@@ -153,7 +155,8 @@ def bench_static(args, wl, dev):
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep},
-        "algorithmic_tflops": flops / (ms * 1e-3) / 1e12,
+        "roofline": {"bound": "mfma", "achieved": flops / (ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
+                     "frac": flops / (ms * 1e-3) / 1e12 / 78.6, "traffic": None},
     }
     print(json.dumps(out), flush=True)
 
