@@ -208,6 +208,27 @@ mfac_status mfac_inv_diag64(mfac_static s, double* diag_out);
 mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t keep,
                           double* scores_out, uint8_t* keep_mask_out);
 
+/* Y = F^-1 X for the block-wise Fisher, n x d row-major fp32 X and Y,
+ * 1 <= n <= 4 (Appendix C eq. 9; with W in place of V and q:
+ * F_b^-1 x_b = (x_b - W_b^T (W_b x_b)) / lambda). Two passes over W (the
+ * precompute's output in G's storage). X and Y must not alias G. */
+mfac_status mfac_static_ihvp(mfac_static s, int32_t n, const float* X, float* Y);
+
+/* Element queries [F^-1]_ij, O(m) each (Section 3.1, eq. 5):
+ * (delta_ij - sum_k W[k,i] W[k,j]) / lambda when i and j share a block, 0
+ * otherwise; fp64 sums of the fp32 W. ij: device array of 2*nq int64 indices
+ * (i_0, j_0, i_1, j_1, ...); out: nq fp64 values. An index outside [0, d)
+ * yields NaN and latches MFAC_ENONFINITE. */
+mfac_status mfac_static_element(mfac_static s, int64_t nq, const int64_t* ij, double* out);
+
+/* OBS correction (Section 4.1) for removing every coordinate j with
+ * keep_mask[j] == 0 at once: delta = -F^-1 x with x_j = theta_j / [F^-1]_jj on
+ * removed coordinates and 0 elsewhere, i.e. the sum of the single-weight OBS
+ * updates -theta_j F^-1 e_j / [F^-1]_jj (the paper's approximate
+ * multi-weight OBS). theta + delta zeroes a removed weight that is the only
+ * removed one in its block. theta, delta_out: d fp32; keep_mask: d uint8. */
+mfac_status mfac_obs_update(mfac_static s, const float* theta, const uint8_t* keep_mask, float* delta_out);
+
 mfac_status mfac_static_set_stream(mfac_static s, hipStream_t stream);
 mfac_status mfac_static_status(mfac_static s);
 mfac_status mfac_static_destroy(mfac_static s);

@@ -52,6 +52,9 @@ SIGNATURES = {
     "mfac_inv_diag": (_c.c_int, [_VP, _VP]),
     "mfac_inv_diag64": (_c.c_int, [_VP, _VP]),
     "mfac_obs_mask": (_c.c_int, [_VP, _VP, _I64, _VP, _VP]),
+    "mfac_static_ihvp": (_c.c_int, [_VP, _I32, _VP, _VP]),
+    "mfac_static_element": (_c.c_int, [_VP, _I64, _VP, _VP]),
+    "mfac_obs_update": (_c.c_int, [_VP, _VP, _VP, _VP]),
     "mfac_static_set_stream": (_c.c_int, [_VP, _VP]),
     "mfac_static_status": (_c.c_int, [_VP]),
     "mfac_static_destroy": (_c.c_int, [_VP]),
@@ -276,6 +279,31 @@ class StaticBlocks:
         mask = t.empty(self.d, dtype=t.uint8, device=self.device)
         _check("mfac_obs_mask", load().mfac_obs_mask(self.handle, _ptr(theta), int(keep), _ptr(sc), _ptr(mask)))
         return mask, sc
+
+    def ihvp(self, X, Y=None):
+        """F^-1 X for the block-wise Fisher (n <= 4 rows of length d)."""
+        t = self.torch
+        n = X.shape[0] if X.dim() == 2 else 1
+        assert X.dtype == t.float32 and X.is_contiguous() and X.numel() == n * self.d
+        Y = t.empty_like(X) if Y is None else Y
+        _check("mfac_static_ihvp", load().mfac_static_ihvp(self.handle, n, _ptr(X), _ptr(Y)))
+        return Y
+
+    def element(self, ij):
+        """[F^-1]_ij for an (nq, 2) int64 tensor of index pairs; returns nq fp64."""
+        t = self.torch
+        ij = ij.to(device=self.device, dtype=t.int64).contiguous()
+        out = t.empty(ij.shape[0], dtype=t.float64, device=self.device)
+        _check("mfac_static_element", load().mfac_static_element(self.handle, ij.shape[0], _ptr(ij), _ptr(out)))
+        return out
+
+    def obs_update(self, theta, keep_mask):
+        """OBS correction delta (fp32, d) for removing the coordinates outside keep_mask."""
+        t = self.torch
+        assert theta.dtype == t.float32 and keep_mask.dtype == t.uint8
+        delta = t.empty(self.d, dtype=t.float32, device=self.device)
+        _check("mfac_obs_update", load().mfac_obs_update(self.handle, _ptr(theta), _ptr(keep_mask), _ptr(delta)))
+        return delta
 
     def status(self):
         return load().mfac_static_status(self.handle)

@@ -75,7 +75,8 @@ struct mfac_static_s {
     float* G;
     hipStream_t st;
     int* err;
-    double *A, *Linv, *diag, *scores;
+    double *A, *Linv, *diag, *scores, *qpart;
+    float *qcoef, *xobs;
     SelectScratch sel;
 };
 
@@ -463,7 +464,13 @@ size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
     char* sel = c.take<char>((size_t)select_scratch_bytes(d));
     double* A = c.take<double>((size_t)batch * mp * mp);
     double* Linv = c.take<double>((size_t)batch * mp * mp);
+    double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
+    float* qcoef = c.take<float>((size_t)(d / B) * m * 4);
+    float* xobs = c.take<float>((size_t)d);
     if (s) {
+        s->qpart = qpart;
+        s->qcoef = qcoef;
+        s->xobs = xobs;
         s->err = err;
         s->diag = diag;
         s->scores = scores;
@@ -542,6 +549,30 @@ MFAC_API mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t ke
     double* sc = scores_out ? scores_out : s->scores;
     HIPCHK(launch_scores(theta, s->diag, s->d, sc, s->err, s->st));
     HIPCHK(launch_topk_mask(sc, s->d, keep, s->sel, keep_mask_out, s->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_static_ihvp(mfac_static s, int32_t n, const float* X, float* Y) {
+    if (!s || !X || !Y || n < 1 || n > 4 || !aligned16(X) || !aligned16(Y)) return MFAC_EINVAL;
+    const double inv_lam = 1.0 / s->lambda;
+    HIPCHK(launch_static_ihvp(s->G, s->m, s->d, s->B, n, X, (float)inv_lam, inv_lam, Y, s->qpart, s->qcoef, s->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_static_element(mfac_static s, int64_t nq, const int64_t* ij, double* out) {
+    if (!s || nq < 0 || (nq > 0 && (!ij || !out)) || ((uintptr_t)ij & 7u) || ((uintptr_t)out & 7u))
+        return MFAC_EINVAL;
+    HIPCHK(launch_static_element(s->G, s->m, s->d, s->B, nq, ij, s->lambda, out, s->err, s->st));
+    return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_obs_update(mfac_static s, const float* theta, const uint8_t* keep_mask, float* delta_out) {
+    if (!s || !theta || !keep_mask || !delta_out || !aligned4(theta) || !aligned16(delta_out)) return MFAC_EINVAL;
+    const double inv_lam = 1.0 / s->lambda;
+    HIPCHK(launch_obs_x(theta, keep_mask, s->diag, s->d, s->xobs, s->st));
+    // delta = -F^-1 x = -x / lambda + W^T (W x) / lambda
+    HIPCHK(launch_static_ihvp(s->G, s->m, s->d, s->B, 1, s->xobs, (float)-inv_lam, -inv_lam, delta_out, s->qpart,
+                              s->qcoef, s->st));
     return MFAC_OK;
 }
 

@@ -1,0 +1,237 @@
+// Queries of the static block-wise path over W (W_b = R_b^-1 G_b, written over
+// G by the precompute; row-major m x d).
+//
+// IHVP (Appendix C eq. 9 with W for V and q): F_b^-1 x_b = (x_b - W_b^T W_b x_b)/lambda,
+// in two passes over W like the dynamic path: pass 1 forms p_b = W_b x_b per
+// column chunk (partial dots per chunk, reduced per block in fp64), pass 2
+// forms alpha x - W_b^T c_b with c_b = scale * p_b. The OBS correction of
+// Section 4.1 is the IHVP of x_j = theta_j / [F^-1]_jj on removed coordinates,
+// negated. Element queries (eq. 5) are O(m) gathers of two W columns.
+#include "device_util.h"
+#include "internal.h"
+
+namespace mfac {
+namespace {
+
+// Pass 1: one work-group per column chunk of width 256*U inside one block.
+// part[c][i*NV + v] = sum_{j in chunk c} W[i, j] x_v[j].
+template <int NV, int U>
+__global__ __launch_bounds__(256) void k_sq_pass1(const float* __restrict__ W, int m, int64_t d, int B, int cpb,
+                                                  const float* __restrict__ X, double* __restrict__ part) {
+    extern __shared__ float acc[];
+    constexpr int CW = 256 * U;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int mnv = m * NV;
+    const int c = blockIdx.x;
+    const int b = c / cpb, cb = c - (c / cpb) * cpb;
+    const int64_t j0 = (int64_t)b * B + (int64_t)cb * CW;
+    int64_t jend = (int64_t)(b + 1) * B;
+    if (jend > j0 + CW) jend = j0 + CW;
+    for (int t = threadIdx.x; t < mnv; t += 256) acc[t] = 0.f;
+
+    float4 vr[NV][U];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int u = 0; u < U; ++u) vr[v][u] = ld4(X + (int64_t)v * d, j0 + u * 256 + lane * 4, jend, 1);
+    __syncthreads();
+
+    for (int i = wave; i < m; i += 8) {
+        const bool has2 = i + 4 < m;
+        const int i2 = has2 ? i + 4 : i;
+        float4 ga[U], gb[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t j = j0 + u * 256 + lane * 4;
+            ga[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+            gb[u] = (j < jend) ? ld_stream(W + (int64_t)i2 * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        float sv[2 * NV];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            float a = 0.f, bb = 0.f;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                a = dot4(ga[u], vr[v][u], a);
+                bb = dot4(gb[u], vr[v][u], bb);
+            }
+            sv[v] = a;
+            sv[NV + v] = bb;
+        }
+        int idx;
+        bool writer;
+        const float tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
+        if (writer) {
+            if (idx < NV)
+                acc[i * NV + idx] += tot;
+            else if (has2)
+                acc[i2 * NV + (idx - NV)] += tot;
+        }
+    }
+    __syncthreads();
+    double* out = part + (int64_t)c * mnv;
+    for (int t = threadIdx.x; t < mnv; t += 256) out[t] = (double)acc[t];
+}
+
+// coef[b][t] = scale * sum_{cb < cpb} part[b*cpb + cb][t]   (fixed order, fp64)
+__global__ __launch_bounds__(256) void k_sq_reduce(const double* __restrict__ part, int cpb, int mnv, double scale,
+                                                   float* __restrict__ coef) {
+    const int b = blockIdx.y;
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t >= mnv) return;
+    double s = 0.0;
+    for (int cb = 0; cb < cpb; ++cb) s += part[((int64_t)b * cpb + cb) * mnv + t];
+    coef[(int64_t)b * mnv + t] = (float)(scale * s);
+}
+
+// Pass 2: one wave per 256*U-column chunk of one block:
+// y_v[j] = alpha * x_v[j] - sum_i coef[b][i*NV + v] W[i, j].
+template <int NV, int U>
+__global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, int m, int64_t d, int B, int cpb2,
+                                                  int64_t nwchunk, const float* __restrict__ coef,
+                                                  const float* __restrict__ X, float alpha, float* __restrict__ Y) {
+    constexpr int WCW = 256 * U;
+    const int lane = threadIdx.x & 63;
+    const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (c >= nwchunk) return;
+    const int b = (int)(c / cpb2), cb = (int)(c - (c / cpb2) * cpb2);
+    const int64_t j0 = (int64_t)b * B + (int64_t)cb * WCW;
+    int64_t jend = (int64_t)(b + 1) * B;
+    if (jend > j0 + WCW) jend = j0 + WCW;
+    const float* cf = coef + (int64_t)b * m * NV;
+
+    float4 acc[NV][U];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[v][u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < m; ++i) {
+        float4 g[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t j = j0 + u * 256 + lane * 4;
+            g[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const float cv = cf[i * NV + v];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                acc[v][u].x = fmaf(cv, g[u].x, acc[v][u].x);
+                acc[v][u].y = fmaf(cv, g[u].y, acc[v][u].y);
+                acc[v][u].z = fmaf(cv, g[u].z, acc[v][u].z);
+                acc[v][u].w = fmaf(cv, g[u].w, acc[v][u].w);
+            }
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t j = j0 + u * 256 + lane * 4;
+            if (j < jend) {
+                const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)v * d + j);
+                float4 y;
+                y.x = alpha * x.x - acc[v][u].x;
+                y.y = alpha * x.y - acc[v][u].y;
+                y.z = alpha * x.z - acc[v][u].z;
+                y.w = alpha * x.w - acc[v][u].w;
+                *reinterpret_cast<float4*>(Y + (int64_t)v * d + j) = y;
+            }
+        }
+}
+
+// x_j = theta_j / [F^-1]_jj where keep_mask_j == 0, else 0
+__global__ void k_obs_x(const float* __restrict__ theta, const uint8_t* __restrict__ keep,
+                        const double* __restrict__ diag, int64_t d, float* __restrict__ x) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j < d) x[j] = keep[j] ? 0.f : (float)((double)theta[j] / diag[j]);
+}
+
+// One wave per query: (delta_ij - sum_k W[k,i] W[k,j]) / lambda within a block.
+__global__ __launch_bounds__(256) void k_static_element(const float* __restrict__ W, int m, int64_t d, int B,
+                                                        int64_t nq, const int64_t* __restrict__ ij, double inv_lam,
+                                                        double* __restrict__ out, int* __restrict__ err) {
+    const int lane = threadIdx.x & 63;
+    const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (q >= nq) return;
+    const int64_t i = ij[2 * q], j = ij[2 * q + 1];
+    if (i < 0 || i >= d || j < 0 || j >= d) {
+        if (lane == 0) {
+            out[q] = __longlong_as_double(0x7ff8000000000000ll);
+            atomicOr(err, 32);
+        }
+        return;
+    }
+    if (i / B != j / B) {
+        if (lane == 0) out[q] = 0.0;
+        return;
+    }
+    double s = 0.0;
+    for (int k = lane; k < m; k += 64) s += (double)W[(int64_t)k * d + i] * (double)W[(int64_t)k * d + j];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (lane == 0) out[q] = ((i == j ? 1.0 : 0.0) - s) * inv_lam;
+}
+
+template <int NV>
+struct SqCfg {
+    static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : 2;  // pass 1
+    static constexpr int U2 = NV <= 2 ? 2 : 1;               // pass 2
+};
+
+template <int NV>
+hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, float alpha, double pscale, float* Y,
+                      double* part, float* coef, hipStream_t st) {
+    constexpr int U = SqCfg<NV>::U, U2 = SqCfg<NV>::U2;
+    const int nblocks = (int)(d / B);
+    const int cpb = (int)ceil_div(B, 256 * U);
+    const size_t lds = (size_t)m * NV * sizeof(float);
+    hipLaunchKernelGGL((k_sq_pass1<NV, U>), dim3((unsigned)(nblocks * cpb)), dim3(256), lds, st, W, m, d, B, cpb, X,
+                       part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sq_reduce, dim3((unsigned)ceil_div(m * NV, 256), nblocks), dim3(256), 0, st, part, cpb,
+                       m * NV, pscale, coef);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int cpb2 = (int)ceil_div(B, 256 * U2);
+    const int64_t nw = (int64_t)nblocks * cpb2;
+    hipLaunchKernelGGL((k_sq_pass2<NV, U2>), dim3((unsigned)ceil_div(nw, 4)), dim3(256), 0, st, W, m, d, B, cpb2, nw,
+                       coef, X, alpha, Y);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t static_query_part_doubles(int64_t d, int B, int m) {
+    // pass-1 partials for up to 4 vectors at the narrowest chunk width (512)
+    return (d / B) * ceil_div(B, 512) * (int64_t)m * 4;
+}
+
+hipError_t launch_static_ihvp(const float* W, int m, int64_t d, int B, int n, const float* X, float alpha,
+                              double pscale, float* Y, double* part, float* coef, hipStream_t st) {
+    switch (n) {
+        case 1: return sq_ihvp_nv<1>(W, m, d, B, X, alpha, pscale, Y, part, coef, st);
+        case 2: return sq_ihvp_nv<2>(W, m, d, B, X, alpha, pscale, Y, part, coef, st);
+        case 3: return sq_ihvp_nv<3>(W, m, d, B, X, alpha, pscale, Y, part, coef, st);
+        case 4: return sq_ihvp_nv<4>(W, m, d, B, X, alpha, pscale, Y, part, coef, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_obs_x(const float* theta, const uint8_t* keep, const double* diag, int64_t d, float* x,
+                        hipStream_t st) {
+    hipLaunchKernelGGL(k_obs_x, dim3((unsigned)ceil_div(d, 256)), dim3(256), 0, st, theta, keep, diag, d, x);
+    return hipGetLastError();
+}
+
+hipError_t launch_static_element(const float* W, int m, int64_t d, int B, int64_t nq, const int64_t* ij, double lam,
+                                 double* out, int* err, hipStream_t st) {
+    if (nq <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_static_element, dim3((unsigned)ceil_div(nq, 4)), dim3(256), 0, st, W, m, d, B, nq, ij,
+                       1.0 / lam, out, err);
+    return hipGetLastError();
+}
+
+}  // namespace mfac

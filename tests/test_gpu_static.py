@@ -104,3 +104,63 @@ def test_mask_edges_and_ties(dev, keep_frac):
     sref = omask.scores(theta.numpy(), dref)
     np.testing.assert_array_equal(mk, omask.keep_mask(sref, keep))
     assert int(mk.sum()) == keep
+
+
+@pytest.mark.parametrize("m,B,nb,lam,scale_full", [
+    (100, 256, 6, 1e-3, False),
+    (1024, 2048, 2, 1e-4, True),     # pruning block width and m, full-size entry scale
+    (37, 100, 3, 1e-2, False),       # B not a multiple of the chunk widths, m padded
+])
+def test_static_ihvp_element_and_obs_update(dev, m, B, nb, lam, scale_full):
+    from paper_2107_03356_amd import StaticBlocks
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=B * nb, m=m, block=B, lam=lam, scale_d=(base.d if scale_full else B))
+    gs = GradientStream(wl, seed=31)
+    G = gs.rows(0, m)
+    theta = gs.theta()
+    X = gs.queries(0, 3)
+    say("static queries", m, B, nb)
+    sb = StaticBlocks(G.to(dev).contiguous(), B, lam)
+    Y = sb.ihvp(X.to(dev).contiguous())
+    Gn, Xn = G.numpy(), X.numpy()
+    Yo = ostatic.ihvp(Gn, lam, B, Xn)
+    for q in range(3):
+        assert rel_l2(Y[q].cpu().numpy(), Yo[q]) < 1e-4
+    # element queries: same block, diagonal, across blocks, ragged positions
+    rng = np.random.default_rng(5)
+    pairs = [(0, 0), (1, 2), (B - 1, 0), (B, B + 3), (wl.d - 1, wl.d - 2), (3, B + 3), (B // 2, B // 2)]
+    pairs += [(int(i), int(i // B * B + rng.integers(0, B))) for i in rng.integers(0, wl.d, 20)]
+    ij = torch.tensor(pairs, dtype=torch.int64)
+    el = sb.element(ij).cpu().numpy()
+    ref = np.array([ostatic.element(Gn, lam, B, i, j) for i, j in pairs])
+    scale = np.abs(ref).max()
+    assert np.max(np.abs(el - ref)) < 1e-5 * scale
+    # OBS correction for the complement of the 50% keep-mask
+    keep = wl.d // 2
+    mask, _ = sb.obs_mask(theta.to(dev), keep)
+    delta = sb.obs_update(theta.to(dev), mask)
+    torch.cuda.synchronize()
+    assert sb.status() == 0
+    dref = ostatic.obs_update(Gn, lam, B, theta.numpy(), mask.cpu().numpy())
+    assert rel_l2(delta.cpu().numpy(), dref) < 1e-4
+
+
+def test_obs_single_weight_and_bad_element_index(dev):
+    from paper_2107_03356_amd import MFAC_ENONFINITE, StaticBlocks
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=4 * 512, m=64, block=512, lam=1e-3, scale_d=512)
+    gs = GradientStream(wl, seed=32)
+    G = gs.rows(0, wl.m)
+    theta = gs.theta()
+    say("obs single weight")
+    sb = StaticBlocks(G.to(dev).contiguous(), wl.block, wl.lam)
+    mask = torch.ones(wl.d, dtype=torch.uint8)
+    mask[700] = 0
+    delta = sb.obs_update(theta.to(dev), mask.to(dev)).cpu().numpy()
+    th = theta.numpy().astype(np.float64)
+    assert abs(th[700] + delta[700]) < 1e-4 * abs(th[700])     # the removed weight goes to zero
+    assert np.all(delta[:512] == 0) and np.all(delta[1024:] == 0)  # only its block moves
+    out = sb.element(torch.tensor([[0, wl.d]], dtype=torch.int64)).cpu().numpy()
+    assert np.isnan(out[0])
+    assert sb.status() == MFAC_ENONFINITE
+    assert sb.status() == 0

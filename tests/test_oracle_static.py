@@ -136,3 +136,72 @@ def test_mask_matches_python_sort_with_ties():
 def test_keep_count():
     assert mask.keep_count(4_194_304, 0.5) == 2_097_152
     assert mask.keep_count(7, 0.5) == 3
+
+
+# ---------------------------------------------------------------------------
+# static queries: IHVP, element, OBS update (Section 3.1 eq. 5, Appendix C eq. 9, Section 4.1)
+# ---------------------------------------------------------------------------
+
+def test_static_ihvp_and_element_match_dense_inverse():
+    rng = np.random.default_rng(8)
+    m, B, nb, lam = 10, 24, 3, 1e-2
+    G = (rng.standard_normal((m, B * nb)) / np.sqrt(B)).astype(np.float32)
+    X = rng.standard_normal((2, B * nb)).astype(np.float32)
+    Y = st.ihvp(G, lam, B, X)
+    for b in range(nb):
+        sl = slice(b * B, (b + 1) * B)
+        Finv = np.linalg.inv(bruteforce.fisher(G[:, sl], lam))
+        np.testing.assert_allclose(Y[:, sl], X[:, sl].astype(np.float64) @ Finv.T, rtol=1e-10, atol=1e-10)
+        for (i, j) in [(0, 0), (3, 17), (23, 5)]:
+            assert abs(st.element(G, lam, B, b * B + i, b * B + j) - Finv[i, j]) < 1e-9 * np.abs(Finv).max()
+    assert st.element(G, lam, B, 1, B + 1) == 0.0          # different blocks
+    np.testing.assert_allclose([st.element(G, lam, B, j, j) for j in range(B * nb)], st.inv_diag(G, lam, B),
+                               rtol=1e-11)
+
+
+def test_static_ihvp_equals_paper_eq9():
+    """Appendix C eq. 9 with the paper's V and q gives the same block IHVP."""
+    rng = np.random.default_rng(9)
+    m, B, lam = 16, 64, 1e-3
+    G = (rng.standard_normal((m, B)) / np.sqrt(B)).astype(np.float32)
+    x = rng.standard_normal(B)
+    V, q = recursions.static_precompute(G, lam)
+    assert _rel(st.block_ihvp(G, lam, x), recursions.static_ihvp(V, q, lam, x)) < 1e-11
+
+
+def test_obs_single_weight_zeroes_it():
+    """Section 4.1: the OBS correction for one weight sets that weight to zero."""
+    rng = np.random.default_rng(10)
+    m, B, nb, lam = 8, 32, 2, 1e-2
+    G = (rng.standard_normal((m, B * nb)) / np.sqrt(B)).astype(np.float32)
+    theta = rng.standard_normal(B * nb) * 0.05
+    for i in (3, B + 7):
+        keep = np.ones(B * nb, np.uint8)
+        keep[i] = 0
+        delta = st.obs_update(G, lam, B, theta, keep)
+        assert abs(theta[i] + delta[i]) < 1e-12
+        # only i's block moves (block-diagonal F)
+        other = slice(0, B) if i >= B else slice(B, 2 * B)
+        assert np.all(delta[other] == 0)
+        # equals -theta_i F^-1 e_i / [F^-1]_ii from the dense inverse
+        b = i // B
+        Finv = np.linalg.inv(bruteforce.fisher(G[:, b * B:(b + 1) * B], lam))
+        li = i - b * B
+        np.testing.assert_allclose(delta[b * B:(b + 1) * B], -theta[i] * Finv[:, li] / Finv[li, li],
+                                   rtol=1e-9, atol=1e-12)
+
+
+def test_obs_set_is_sum_of_single_updates():
+    rng = np.random.default_rng(11)
+    m, B, lam = 6, 20, 1e-2
+    G = (rng.standard_normal((m, B)) / np.sqrt(B)).astype(np.float32)
+    theta = rng.standard_normal(B) * 0.05
+    keep = np.ones(B, np.uint8)
+    keep[[2, 9, 13]] = 0
+    total = st.obs_update(G, lam, B, theta, keep)
+    parts = []
+    for i in (2, 9, 13):
+        k1 = np.ones(B, np.uint8)
+        k1[i] = 0
+        parts.append(st.obs_update(G, lam, B, theta, k1))
+    np.testing.assert_allclose(total, np.sum(parts, axis=0), rtol=1e-10, atol=1e-13)
