@@ -114,37 +114,55 @@ __global__ __launch_bounds__(256) void k_assemble(double* __restrict__ K, int m,
 
 // ------------------------------------------------------------------ potrf
 // One 64-thread wave per batch item: factor diagonal tile t in place (lower)
-// and write its inverse into the diagonal tile of Linv.
+// and write its inverse into the diagonal tile of Linv. Lane i keeps row i of
+// the tile in registers; each column step broadcasts the new column through a
+// double-buffered LDS vector (reads of step j and writes of step j+2 are
+// separated by the barriers of step j+1), so the trailing update is a run of
+// independent FMAs on registers.
 __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, double* __restrict__ Linv,
                                                    int mp, int64_t bstride, int t, int* __restrict__ err) {
+    __shared__ double col[2][64];
     __shared__ double T[64][65];
-    __shared__ double I[64][65];
     double* Ab = A + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
     double* Lb = Linv + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
     const int i = threadIdx.x;
-    for (int c = 0; c < 64; ++c) T[i][c] = Ab[(int64_t)i * mp + c];
-    __syncthreads();
+    double a[64];
+#pragma unroll
+    for (int c = 0; c < 64; ++c) a[c] = Ab[(int64_t)i * mp + c];
     int bad = 0;
+#pragma unroll
     for (int j = 0; j < 64; ++j) {
+        double* cb = col[j & 1];
         if (i == j) {
-            double piv = T[j][j];
+            double piv = a[j];
             if (!(piv > 0.0) || !isfinite(piv)) {
                 bad = 1;
                 piv = 1.0;
             }
-            T[j][j] = sqrt(piv);
+            a[j] = sqrt(piv);
+            cb[j] = a[j];
         }
-        __syncthreads();
-        const double djj = T[j][j];
-        if (i > j) T[i][j] /= djj;
         __syncthreads();
         if (i > j) {
-            const double lij = T[i][j];
-            for (int c = j + 1; c <= i; ++c) T[i][c] -= lij * T[c][j];
+            a[j] = a[j] / cb[j];
+            cb[i] = a[j];
         }
         __syncthreads();
+        if (i > j) {
+            const double lij = a[j];
+#pragma unroll
+            for (int c = j + 1; c < 64; ++c) a[c] -= lij * cb[c];
+        }
     }
     if (bad) atomicOr(err, 2);
+    // the factor (lower part of the registers) into LDS and back to A
+#pragma unroll
+    for (int c = 0; c < 64; ++c) {
+        const double v = (c <= i) ? a[c] : 0.0;
+        T[i][c] = v;
+        Ab[(int64_t)i * mp + c] = v;
+    }
+    __syncthreads();
     // Column i of the inverse of the lower factor by forward substitution,
     // kept in registers: x_r = (delta_ri - sum_{l<r} T[r][l] x_l) / T[r][r].
     // Rows above i come out as exact zeros. Reads of T[r][l] are the same
@@ -166,14 +184,14 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
             for (int l = r & ~3; l < r; ++l) s0 -= T[r][l] * x[l];
             x[r] = ((s0 + s1) + (s2 + s3)) / T[r][r];
         }
+        __syncthreads();
+        // transpose through LDS so each lane writes a row of the inverse
 #pragma unroll
-        for (int r = 0; r < 64; ++r) I[r][i] = x[r];
+        for (int r = 0; r < 64; ++r) T[r][i] = x[r];
     }
     __syncthreads();
-    for (int c = 0; c < 64; ++c) {
-        Ab[(int64_t)i * mp + c] = (c <= i) ? T[i][c] : 0.0;
-        Lb[(int64_t)i * mp + c] = I[i][c];
-    }
+#pragma unroll
+    for (int c = 0; c < 64; ++c) Lb[(int64_t)i * mp + c] = T[i][c];
 }
 
 // Panel: A[r,t] <- A[r,t] * Linv[t,t]^T for r > t. grid (T-1-t, nbatch).

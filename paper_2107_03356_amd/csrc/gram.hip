@@ -11,9 +11,9 @@
 // window is split over work-groups; each work-group flushes its fp32 MFMA
 // accumulators into fp64 registers after every 2048-column slab, and the
 // split partials are summed in fp64, in a fixed order, by k_gram_reduce.
-// Static blocks: fp64 MFMA (v_mfma_f64_16x16x4f64) over the block's columns,
-// written straight into the block's padded fp64 matrix with m*lambda added on
-// the diagonal, because the keep-mask is decided in fp64.
+// Static blocks: fp64 MFMA (v_mfma_f64_16x16x4f64) over the block's columns
+// in 128 x 128 tiles, written straight into the block's padded fp64 matrix
+// with m*lambda added on the diagonal, because the keep-mask is decided in fp64.
 #include "internal.h"
 
 namespace mfac {
@@ -150,48 +150,99 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
     }
 }
 
-// Static blocks: grid (ntiles, nb); block y covers columns [(b0+y)B, (b0+y+1)B).
-__global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d,
-                                                     int B, int b0, double mu, double* __restrict__ A,
-                                                     int mp) {
-    __shared__ float As[64][PITCH];
-    __shared__ float Bs[64][PITCH];
-    int ti, tj;
-    tile_of(blockIdx.x, ti, tj);
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
-    const float* base = G + (int64_t)(b0 + blockIdx.y) * B;
+// Static blocks, fp64 MFMA. One work-group per 128 x 128 lower-triangular tile
+// of one block's Gram matrix (flattened over blocks, XCD-remapped so the tiles
+// of a block share an L2); the block's columns stream through double-buffered
+// LDS in 32-column chunks, the next chunk's loads in flight during the MFMAs.
+constexpr int GT = 128;
 
-    v4d acc[2][2];
+__device__ __forceinline__ int xcd_remap(int p, int n) {
+    if (n % 8) return p;
+    return (p % 8) * (n / 8) + p / 8;
+}
+
+__global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d, int B, int b0,
+                                                     int ntiles, double mu, double* __restrict__ A, int mp) {
+    __shared__ float As[2][GT][PITCH];
+    __shared__ float Bs[2][GT][PITCH];
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int bl = lid / ntiles;
+    int ti, tj;
+    tile_of(lid - bl * ntiles, ti, tj);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int rl = lane & 15, kl = lane >> 4;
+    const bool diag_tile = ti == tj;
+    const float* base = G + (int64_t)(b0 + bl) * B;
+    const int ra0 = ti * GT, rb0 = tj * GT;
+    // staging: 128 rows x 32 columns per operand, 16 floats per thread
+    const int sr = tid >> 1, sc = (tid & 1) * 16;
+    float4 pa[4], pb[4];
+    auto load_chunk = [&](int k0) {
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+        for (int q = 0; q < 4; ++q) {
+            const int col = k0 + sc + 4 * q;
+            const bool okc = col < B;
+            pa[q] = (ra0 + sr < m && okc) ? *reinterpret_cast<const float4*>(base + (int64_t)(ra0 + sr) * d + col)
+                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+            if (!diag_tile)
+                pb[q] = (rb0 + sr < m && okc) ? *reinterpret_cast<const float4*>(base + (int64_t)(rb0 + sr) * d + col)
+                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    };
+    auto store_chunk = [&](int buf) {
 #pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
-    for (int k0 = 0; k0 < B; k0 += KB) {
-        stage(As, base, d, ti * 64, m, k0, B);
-        if (ti != tj) stage(Bs, base, d, tj * 64, m, k0, B);
-        __syncthreads();
-        if (ti != tj)
-            mfma_stage<v4d, true>(As, Bs, wr, wc, lane, acc);
-        else
-            mfma_stage<v4d, true>(As, As, wr, wc, lane, acc);
+        for (int q = 0; q < 4; ++q) {
+            *reinterpret_cast<float4*>(&As[buf][sr][sc + 4 * q]) = pa[q];
+            if (!diag_tile) *reinterpret_cast<float4*>(&Bs[buf][sr][sc + 4 * q]) = pb[q];
+        }
+    };
+
+    v4d acc[4][4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
+    const int nchunk = (B + KB - 1) / KB;
+    load_chunk(0);
+    store_chunk(0);
+    __syncthreads();
+    for (int c = 0; c < nchunk; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < nchunk) load_chunk((c + 1) * KB);
+        float (*Ab)[PITCH] = As[buf];
+        float (*Bb)[PITCH] = diag_tile ? As[buf] : Bs[buf];
+#pragma unroll
+        for (int kk = 0; kk < KB / 4; ++kk) {
+            double av[4], bv[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) av[x] = (double)Ab[wr * 64 + x * 16 + rl][kk * 4 + kl];
+#pragma unroll
+            for (int y = 0; y < 4; ++y) bv[y] = (double)Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+        }
+        if (c + 1 < nchunk) store_chunk(buf ^ 1);
         __syncthreads();
     }
-    double* Ab = A + (int64_t)blockIdx.y * mp * mp;
-    const int rl = lane & 15, kl = lane >> 4;
+    double* Ab = A + (int64_t)bl * mp * mp;
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y)
+        for (int y = 0; y < 4; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 // fp64 MFMA result: lane l register r is row (l/16) + 4r
-                const int row = ti * 64 + wr * 32 + x * 16 + kl + 4 * r;
-                const int col = tj * 64 + wc * 32 + y * 16 + rl;
-                double v = acc[x][y][r];
-                if (row == col) v += (row < m) ? mu : 1.0;
-                Ab[(int64_t)row * mp + col] = v;
+                const int row = ra0 + wr * 64 + x * 16 + kl + 4 * r;
+                const int col = rb0 + wc * 64 + y * 16 + rl;
+                if (row < mp && col < mp) {
+                    double v = acc[x][y][r];
+                    if (row == col) v += (row < m) ? mu : 1.0;
+                    Ab[(int64_t)row * mp + col] = v;
+                }
             }
 }
 
@@ -225,9 +276,10 @@ hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part
 
 hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb, double mu,
                               double* A, int mp, hipStream_t st) {
-    const int T = mp / 64;
+    const int T = (int)ceil_div(mp, GT);
     const int ntiles = T * (T + 1) / 2;
-    hipLaunchKernelGGL(k_gram_blocks, dim3(ntiles, nb), dim3(256), 0, st, G, m, d, B, b0, mu, A, mp);
+    hipLaunchKernelGGL(k_gram_blocks, dim3((unsigned)(ntiles * nb)), dim3(256), 0, st, G, m, d, B, b0, ntiles, mu, A,
+                       mp);
     return hipGetLastError();
 }
 

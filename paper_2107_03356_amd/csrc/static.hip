@@ -6,9 +6,11 @@
 // diag(F_b^-1) = (1 - sum_i W_b[i,:]^2) / lambda (Appendix C, diagonal
 // extraction). k_trmm_diag forms W_b = Linv_b G_b tile by tile on fp64 MFMA,
 // writes it over G in fp32 and accumulates the column sums of squares from the
-// unrounded fp64 tiles. A work-group owns one 64-column slice of one block and
-// walks the row tiles from the bottom up, so every tile of G it still needs
-// is untouched when it overwrites a finished one.
+// unrounded fp64 tiles. A work-group owns one 128-column slice of one block and
+// walks the 64-row tiles from the bottom up, so every tile of G it still needs
+// is untouched when it overwrites a finished one. Each tile's k-loop runs in
+// 32-deep chunks through double-buffered LDS, the next chunk's global loads in
+// flight during the current chunk's MFMAs.
 //
 // Keep-mask (Section 4.1, OBD saliency, global over all blocks): fp64 scores,
 // then an 8-pass radix selection of the keep-th largest key (8-bit digits of
@@ -20,86 +22,124 @@ namespace mfac {
 namespace {
 
 typedef double v4d __attribute__((ext_vector_type(4)));
-constexpr int P = 68;
 
+// Work-groups are dispatched round-robin over the 8 XCDs (each with its own
+// L2). Remap so that consecutive logical indices share an XCD: the column
+// slices of one block then run on one XCD and share its L2 copy of L_b^-1.
+__device__ __forceinline__ int xcd_remap(int p, int n) {
+    if (n % 8) return p;
+    return (p % 8) * (n / 8) + p / 8;
+}
+
+constexpr int TM = 64, TN = 128, TK = 32;  // W tile rows x columns, k-chunk
+constexpr int PA = TK + 2;                 // LDS pitch of the L^-1 chunk (doubles)
+constexpr int PB = TN + 16;                // LDS pitch of the G chunk (floats)
+
+// grid: nslice * nb work-groups (flattened, remapped); slice = TN columns of a block.
 __global__ __launch_bounds__(256) void k_trmm_diag(const double* __restrict__ Linv, int mp, int64_t bstride,
                                                    float* __restrict__ G, int m, int64_t d, int B, int b0,
-                                                   double inv_lam, double* __restrict__ diag) {
-    __shared__ double Sa[64][P];
-    __shared__ double Sb[64][P];
-    __shared__ double red[2][64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+                                                   int nslice, double inv_lam, double* __restrict__ diag) {
+    __shared__ double As[2][TM][PA];
+    __shared__ float Bs[2][TK][PB];
+    __shared__ double red[2][TN];
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int bl = lid / nslice, sl = lid - (lid / nslice) * nslice;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1;
     const int rl = lane & 15, kl = lane >> 4;
-    const int b = b0 + blockIdx.y;
-    const int c0 = blockIdx.x * 64;  // column slice within the block
-    const double* Lb = Linv + (int64_t)blockIdx.y * bstride;
+    const int b = b0 + bl;
+    const int c0 = sl * TN;
+    const int ncol = (B - c0) < TN ? (B - c0) : TN;
+    const double* Lb = Linv + (int64_t)bl * bstride;
     float* Gb = G + (int64_t)b * B + c0;
-    const int T = mp / 64;
-    const int ncol = (B - c0) < 64 ? (B - c0) : 64;
+    const int T = mp / TM;
 
-    double sq[2] = {0.0, 0.0};
+    // global -> register staging of one k-chunk: L^-1 rows [r0, r0+64) x cols
+    // [k0, k0+32) (8 doubles per thread) and G rows [k0, k0+32) x 128 columns
+    // (16 floats per thread)
+    const int ar = tid >> 2, ac = (tid & 3) * 8;
+    const int br = tid >> 3, bc = (tid & 7) * 16;
+    double2 ra[4];
+    float4 rb[4];
+    auto load_chunk = [&](int r0, int k0) {
+        const double* src = Lb + (int64_t)(r0 + ar) * mp + k0 + ac;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ra[q] = *reinterpret_cast<const double2*>(src + 2 * q);
+        const int grow = k0 + br;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int col = bc + 4 * q;
+            rb[q] = (grow < m && col < ncol) ? *reinterpret_cast<const float4*>(Gb + (int64_t)grow * d + col)
+                                             : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    };
+    auto store_chunk = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            As[buf][ar][ac + 2 * q] = ra[q].x;
+            As[buf][ar][ac + 2 * q + 1] = ra[q].y;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&Bs[buf][br][bc + 4 * q]) = rb[q];
+    };
+
+    double sq[4] = {0.0, 0.0, 0.0, 0.0};
     for (int r = T - 1; r >= 0; --r) {
-        v4d acc[2][2];
+        v4d acc[2][4];
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
-            for (int y = 0; y < 2; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
-        for (int k = 0; k <= r; ++k) {
-            // a = Linv[r,k] (rows r, inner k); b[c][kk] = G[k*64 + kk][c0 + c]
-            const double* src = Lb + (int64_t)r * 64 * mp + k * 64;
-            for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-                const int rr = e >> 6, cc = e & 63;
-                Sa[rr][cc] = src[(int64_t)rr * mp + cc];
-                const int grow = k * 64 + rr;
-                Sb[cc][rr] = (grow < m && cc < ncol) ? (double)Gb[(int64_t)grow * d + cc] : 0.0;
-            }
-            __syncthreads();
-#pragma unroll 4
-            for (int kk = 0; kk < 16; ++kk) {
-                double av[2], bv[2];
+            for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
+        const int nchunk = (r + 1) * (TM / TK);
+        load_chunk(r * TM, 0);
+        store_chunk(0);
+        __syncthreads();
+        for (int c = 0; c < nchunk; ++c) {
+            const int buf = c & 1;
+            if (c + 1 < nchunk) load_chunk(r * TM, (c + 1) * TK);
 #pragma unroll
-                for (int s = 0; s < 2; ++s) {
-                    av[s] = Sa[wr * 32 + s * 16 + rl][kk * 4 + kl];
-                    bv[s] = Sb[wc * 32 + s * 16 + rl][kk * 4 + kl];
-                }
+            for (int kk = 0; kk < TK / 4; ++kk) {
+                double av[2], bv[4];
+#pragma unroll
+                for (int x = 0; x < 2; ++x) av[x] = As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
+#pragma unroll
+                for (int y = 0; y < 4; ++y) bv[y] = (double)Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
 #pragma unroll
                 for (int x = 0; x < 2; ++x)
 #pragma unroll
-                    for (int y = 0; y < 2; ++y)
+                    for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
+            if (c + 1 < nchunk) store_chunk(buf ^ 1);
             __syncthreads();
         }
-        // W tile r: write over G (fp32), accumulate squares (fp64)
+        // W tile r: write over G (fp32) and accumulate squares from the fp64 values
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
-            for (int y = 0; y < 2; ++y)
+            for (int y = 0; y < 4; ++y)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int row = r * 64 + wr * 32 + x * 16 + kl + 4 * q;  // fp64 MFMA: row (l/16) + 4q
-                    const int col = wc * 32 + y * 16 + rl;
+                    const int row = r * TM + wr * 32 + x * 16 + kl + 4 * q;  // fp64 MFMA: row (l/16) + 4q
+                    const int col = wc * 64 + y * 16 + rl;
                     const double w = acc[x][y][q];
                     sq[y] += w * w;
                     if (row < m && col < ncol) Gb[(int64_t)row * d + col] = (float)w;
                 }
+        __syncthreads();
     }
-    // reduce the squares of each column: over kl (lanes +16, +32) then over wr
+    // column sums of squares: over kl (lanes +16, +32), then over wr
 #pragma unroll
-    for (int y = 0; y < 2; ++y) {
+    for (int y = 0; y < 4; ++y) {
         sq[y] += __shfl_xor(sq[y], 16, 64);
         sq[y] += __shfl_xor(sq[y], 32, 64);
     }
     if (kl == 0) {
-        red[wr][wc * 32 + rl] = sq[0];
-        red[wr][wc * 32 + 16 + rl] = sq[1];
+#pragma unroll
+        for (int y = 0; y < 4; ++y) red[wr][wc * 64 + y * 16 + rl] = sq[y];
     }
     __syncthreads();
-    if (threadIdx.x < ncol) {
-        const double s = red[0][threadIdx.x] + red[1][threadIdx.x];
-        diag[(int64_t)b * B + c0 + threadIdx.x] = (1.0 - s) * inv_lam;
-    }
+    if (tid < ncol) diag[(int64_t)b * B + c0 + tid] = (1.0 - (red[0][tid] + red[1][tid])) * inv_lam;
 }
 
 __global__ void k_diag_to_f32(const double* __restrict__ dg, int64_t d, float* __restrict__ out) {
@@ -268,8 +308,9 @@ __global__ void k_fill_u8(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
 
 hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* G, int m, int64_t d, int B,
                             int b0, int nb, double lam, double* diag, hipStream_t st) {
-    hipLaunchKernelGGL(k_trmm_diag, dim3((unsigned)ceil_div(B, 64), nb), dim3(256), 0, st, Linv, mp, bstride, G,
-                       m, d, B, b0, 1.0 / lam, diag);
+    const int nslice = (int)ceil_div(B, TN);
+    hipLaunchKernelGGL(k_trmm_diag, dim3((unsigned)(nslice * nb)), dim3(256), 0, st, Linv, mp, bstride, G, m, d, B,
+                       b0, nslice, 1.0 / lam, diag);
     return hipGetLastError();
 }
 
