@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmfac.so")
 ARCH = os.environ.get("MFAC_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["pass.hip", "gram.hip", "chol.hip", "static.hip", "static_query.hip", "capi.hip"]
+SOURCES = ["pass.hip", "gram.hip", "chol.hip", "factor.hip", "static.hip", "static_query.hip", "capi.hip"]
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",

@@ -145,8 +145,7 @@ hipError_t mark_end(mfac_window w, int phase) {
 // A = K + m*lambda*I, A = L L^T, Linv = L^-1, Ainv = Linv^T Linv.
 mfac_status window_factor(mfac_window w, const double* p, int pstride, int k) {
     HIPCHK(launch_assemble(w->K, w->m, p, pstride, k, (double)w->m * w->lambda, w->A, w->mp, w->err, w->st));
-    HIPCHK(launch_potrf(w->A, w->Linv, w->mp, 1, 0, w->err, w->st));
-    HIPCHK(launch_trtri(w->A, w->Linv, w->mp, 1, 0, w->st));
+    HIPCHK(launch_factor_invert(w->A, w->Linv, w->mp, 1, 0, w->err, w->st));
     HIPCHK(launch_lauum(w->Linv, w->Ainv, w->mp, 1, 0, w->st));
     w->since_refactor = 0;
     return MFAC_OK;
@@ -520,8 +519,7 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
     for (int b0 = 0; b0 < s->nblocks; b0 += s->batch) {
         const int nb = (s->nblocks - b0) < s->batch ? (s->nblocks - b0) : s->batch;
         if (launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->st) != hipSuccess) return fail();
-        if (launch_potrf(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st) != hipSuccess) return fail();
-        if (launch_trtri(s->A, s->Linv, s->mp, nb, bstride, s->st) != hipSuccess) return fail();
+        if (launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st) != hipSuccess) return fail();
         if (launch_trmm_diag(s->Linv, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, s->st) !=
             hipSuccess)
             return fail();

@@ -194,75 +194,6 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
     for (int c = 0; c < 64; ++c) Lb[(int64_t)i * mp + c] = T[i][c];
 }
 
-// Panel: A[r,t] <- A[r,t] * Linv[t,t]^T for r > t. grid (T-1-t, nbatch).
-__global__ __launch_bounds__(256) void k_trsm_panel(double* __restrict__ A, const double* __restrict__ Linv,
-                                                    int mp, int64_t bstride, int t) {
-    __shared__ double Sa[64][P];
-    __shared__ double Sb[64][P];
-    const int r = t + 1 + blockIdx.x;
-    double* Ab = A + (int64_t)blockIdx.y * bstride;
-    const double* Lb = Linv + (int64_t)blockIdx.y * bstride;
-    double* Art = Ab + (int64_t)r * 64 * mp + t * 64;
-    stage_tile(Sa, Art, mp);
-    stage_tile(Sb, Lb + (int64_t)t * 64 * mp + t * 64, mp);
-    __syncthreads();
-    v4d acc[2][2];
-    zero_acc(acc);
-    mma_nt(Sa, Sb, acc);
-    for_acc(acc, [&](int row, int col, double v) { Art[(int64_t)row * mp + col] = v; });
-}
-
-// Trailing update: A[r,s] -= A[r,t] A[s,t]^T for t < s <= r. grid (npairs, nbatch).
-__global__ __launch_bounds__(256) void k_syrk_update(double* __restrict__ A, int mp, int64_t bstride, int t) {
-    __shared__ double Sa[64][P];
-    __shared__ double Sb[64][P];
-    // pair index -> (r, s) over the lower triangle of the trailing tiles
-    const int idx = blockIdx.x;
-    int rr = (int)((sqrtf(8.0f * (float)idx + 1.0f) - 1.0f) * 0.5f);
-    while ((rr + 1) * (rr + 2) / 2 <= idx) ++rr;
-    while (rr * (rr + 1) / 2 > idx) --rr;
-    const int ss = idx - rr * (rr + 1) / 2;
-    const int r = t + 1 + rr, s = t + 1 + ss;
-    double* Ab = A + (int64_t)blockIdx.y * bstride;
-    stage_tile(Sa, Ab + (int64_t)r * 64 * mp + t * 64, mp);
-    if (r != s) stage_tile(Sb, Ab + (int64_t)s * 64 * mp + t * 64, mp);
-    __syncthreads();
-    v4d acc[2][2];
-    zero_acc(acc);
-    mma_nt(Sa, r != s ? Sb : Sa, acc);
-    double* C = Ab + (int64_t)r * 64 * mp + s * 64;
-    for_acc(acc, [&](int row, int col, double v) { C[(int64_t)row * mp + col] -= v; });
-}
-
-// ------------------------------------------------------------------ trtri
-// Linv[i,j] = -Linv[i,i] * sum_{k=j}^{i-1} L[i,k] Linv[k,j], i = j + step.
-// grid (T - step, nbatch).
-__global__ __launch_bounds__(256) void k_trtri_step(const double* __restrict__ L, double* __restrict__ Linv,
-                                                    int mp, int64_t bstride, int step) {
-    __shared__ double Sa[64][P];
-    __shared__ double Sb[64][P];
-    const int j = blockIdx.x, i = j + step;
-    const double* Lb = L + (int64_t)blockIdx.y * bstride;
-    double* Ib = Linv + (int64_t)blockIdx.y * bstride;
-    v4d acc[2][2];
-    zero_acc(acc);
-    for (int k = j; k < i; ++k) {
-        stage_tile(Sa, Lb + (int64_t)i * 64 * mp + k * 64, mp);
-        stage_tile_t(Sb, Ib + (int64_t)k * 64 * mp + j * 64, mp);
-        __syncthreads();
-        mma_nt(Sa, Sb, acc);
-        __syncthreads();
-    }
-    // X = acc; stage X^T into Sb, Linv[i,i] into Sa, then -Linv[i,i] X
-    for_acc(acc, [&](int row, int col, double v) { Sb[col][row] = v; });
-    stage_tile(Sa, Ib + (int64_t)i * 64 * mp + i * 64, mp);
-    __syncthreads();
-    zero_acc(acc);
-    mma_nt(Sa, Sb, acc);
-    double* C = Ib + (int64_t)i * 64 * mp + j * 64;
-    for_acc(acc, [&](int row, int col, double v) { C[(int64_t)row * mp + col] = -v; });
-}
-
 __global__ __launch_bounds__(256) void k_zero_upper(double* __restrict__ Linv, int mp, int64_t bstride) {
     // zero the strictly-upper tiles of Linv (tile (i, j) with j > i); grid (T*T, nbatch)
     const int T = mp / 64;
@@ -412,36 +343,16 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
     return hipGetLastError();
 }
 
-hipError_t launch_potrf(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
-                        hipStream_t st) {
-    const int T = mp / 64;
-    for (int t = 0; t < T; ++t) {
-        hipLaunchKernelGGL(k_potrf_diag, dim3(nbatch), dim3(64), 0, st, A, Linv, mp, bstride, t, err);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        const int n = T - 1 - t;
-        if (n == 0) break;
-        hipLaunchKernelGGL(k_trsm_panel, dim3(n, nbatch), dim3(256), 0, st, A, Linv, mp, bstride, t);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(k_syrk_update, dim3(n * (n + 1) / 2, nbatch), dim3(256), 0, st, A, mp, bstride, t);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
+hipError_t launch_potrf_tile(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int t, int* err,
+                             hipStream_t st) {
+    hipLaunchKernelGGL(k_potrf_diag, dim3(nbatch), dim3(64), 0, st, A, Linv, mp, bstride, t, err);
+    return hipGetLastError();
 }
 
-hipError_t launch_trtri(const double* L, double* Linv, int mp, int nbatch, int64_t bstride, hipStream_t st) {
+hipError_t launch_zero_upper(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st) {
     const int T = mp / 64;
-    hipLaunchKernelGGL(k_zero_upper, dim3(T * T, nbatch), dim3(256), 0, st, Linv, mp, bstride);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    for (int s = 1; s < T; ++s) {
-        hipLaunchKernelGGL(k_trtri_step, dim3(T - s, nbatch), dim3(256), 0, st, L, Linv, mp, bstride, s);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
+    hipLaunchKernelGGL(k_zero_upper, dim3(T * T, nbatch), dim3(256), 0, st, M, mp, bstride);
+    return hipGetLastError();
 }
 
 hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, int64_t bstride, hipStream_t st) {

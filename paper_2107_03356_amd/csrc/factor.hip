@@ -1,0 +1,253 @@
+// Recursive blocked Cholesky factor and triangular inverse of a batch of
+// padded SPD matrices A = G G^T + m*lambda*I (the coefficient matrices of
+// both the dynamic and the static path): L L^T = A, and L^-1.
+//
+// A node of size n splits at h (a multiple of 64):
+//   [A11  .  ]   L11 L11^T = A11                      (recursion)
+//   [A21 A22 ]   L21 = A21 L11^-T                      (GEMM, L11^-T upper)
+//                A22 <- A22 - L21 L21^T                (GEMM, lower tiles)
+//                L22 L22^T = A22                      (recursion)
+//                L^-1 21 = -L22^-1 (L21 L11^-1)        (two GEMMs, triangular)
+// Leaves are 64 x 64 tiles factored and inverted by k_potrf_diag. L itself is
+// not kept: L21 lives in the (unused) upper block A12 while the node needs it,
+// and L21 L11^-1 goes into A21, whose input values are consumed by then.
+// Every GEMM is batched over the matrices and skips the K-range its
+// triangular operand makes zero, so the flops are m^3/3 for the factor and
+// m^3/3 for the inverse, nearly all of it in large MFMA tiles.
+#include "internal.h"
+
+namespace mfac {
+
+// defined in chol.hip
+hipError_t launch_potrf_tile(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int t, int* err,
+                             hipStream_t st);
+hipError_t launch_zero_upper(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st);
+
+namespace {
+
+typedef double v4d __attribute__((ext_vector_type(4)));
+
+constexpr int BM = 128, BN = 128, BK = 16;
+constexpr int PA = BK + 2;   // pitch of [row][k] chunks (doubles)
+constexpr int PBN = BN + 4;  // pitch of a [k][n] chunk (doubles)
+
+enum : int {
+    KHI_ROW = 1,   // A lower triangular: k < (I+1)*BM for output row tile I
+    KHI_COL = 2,   // op(B) upper triangular: k < (J+1)*BN for output column tile J
+    KLO_COL = 4,   // op(B) lower triangular: k >= J*BN
+    LOWER_ONLY = 8 // only output tiles with I >= J
+};
+
+__device__ __forceinline__ int xcd_remap(int p, int n) {
+    if (n % 8) return p;
+    return (p % 8) * (n / 8) + p / 8;
+}
+
+struct GemmArgs {
+    const double* A;
+    const double* B;
+    double* C;
+    int ld;
+    int64_t bstride;
+    int a0r, a0c;  // stored A origin (row, col)
+    int b0r, b0c;  // stored B origin
+    int cm0, cn0;  // C origin
+    int M, N, K;
+    double alpha, beta;
+    int flags;
+    int tiles_m, tiles_n;
+};
+
+// C = alpha * op(A) op(B) + beta * C on sub-matrices of every batch item:
+//   op(A)[m][k] = TA ? A[a0r+k][a0c+m] : A[a0r+m][a0c+k]
+//   op(B)[k][n] = TB ? B[b0r+n][b0c+k] : B[b0r+k][b0c+n]
+// One work-group per 128 x 128 output tile, 16-deep k-chunks through
+// double-buffered LDS with the next chunk's loads in flight.
+template <bool TA, bool TB>
+__global__ __launch_bounds__(256) void k_bgemm(GemmArgs g) {
+    // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
+    __shared__ double As[2][TA ? BK : BM][TA ? PBN : PA];
+    __shared__ double Bs[2][TB ? BN : BK][TB ? PA : PBN];
+    const int ntile = g.tiles_m * g.tiles_n;
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int bt = lid / ntile;
+    const int tt = lid - bt * ntile;
+    const int I = tt / g.tiles_n, J = tt - (tt / g.tiles_n) * g.tiles_n;
+    if ((g.flags & LOWER_ONLY) && I < J) return;
+    int klo = 0, khi = g.K;
+    if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BM);
+    if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BN);
+    if (g.flags & KLO_COL) klo = J * BN;
+    const double* A = g.A + (int64_t)bt * g.bstride;
+    const double* B = g.B + (int64_t)bt * g.bstride;
+    double* C = g.C + (int64_t)bt * g.bstride;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = wave >> 1, wc = wave & 1;
+    const int rl = lane & 15, kl = lane >> 4;
+    const int mrow0 = I * BM, ncol0 = J * BN;
+
+    // staging of 2048 doubles per operand and chunk, 8 per thread:
+    // [row][k] layout: row tid/2, k (tid%2)*8;  [k][row] layout: k tid/16, row (tid%16)*8
+    const int sr = tid >> 1, sk = (tid & 1) * 8;
+    const int tk = tid >> 4, tn = (tid & 15) * 8;
+    double2 pa[4], pb[4];
+    auto load_chunk = [&](int k0) {
+        if (TA) {
+            const double* a = A + (int64_t)(g.a0r + k0 + tk) * g.ld + g.a0c + mrow0 + tn;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                pa[q] = (mrow0 + tn + 2 * q < g.M) ? *reinterpret_cast<const double2*>(a + 2 * q) : make_double2(0.0, 0.0);
+        } else {
+            const bool ok = mrow0 + sr < g.M;
+            const double* a = A + (int64_t)(g.a0r + mrow0 + sr) * g.ld + g.a0c + k0 + sk;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) pa[q] = ok ? *reinterpret_cast<const double2*>(a + 2 * q) : make_double2(0.0, 0.0);
+        }
+        if (TB) {
+            const bool ok = ncol0 + sr < g.N;
+            const double* b = B + (int64_t)(g.b0r + ncol0 + sr) * g.ld + g.b0c + k0 + sk;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) pb[q] = ok ? *reinterpret_cast<const double2*>(b + 2 * q) : make_double2(0.0, 0.0);
+        } else {
+            const double* b = B + (int64_t)(g.b0r + k0 + tk) * g.ld + g.b0c + ncol0 + tn;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                pb[q] = (ncol0 + tn + 2 * q < g.N) ? *reinterpret_cast<const double2*>(b + 2 * q) : make_double2(0.0, 0.0);
+        }
+    };
+    auto store_chunk = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (TA) {
+                As[buf][tk][tn + 2 * q] = pa[q].x;
+                As[buf][tk][tn + 2 * q + 1] = pa[q].y;
+            } else {
+                As[buf][sr][sk + 2 * q] = pa[q].x;
+                As[buf][sr][sk + 2 * q + 1] = pa[q].y;
+            }
+            if (TB) {
+                Bs[buf][sr][sk + 2 * q] = pb[q].x;
+                Bs[buf][sr][sk + 2 * q + 1] = pb[q].y;
+            } else {
+                Bs[buf][tk][tn + 2 * q] = pb[q].x;
+                Bs[buf][tk][tn + 2 * q + 1] = pb[q].y;
+            }
+        }
+    };
+
+    v4d acc[4][4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
+    const int nchunk = (khi - klo) / BK;
+    if (nchunk > 0) {
+        load_chunk(klo);
+        store_chunk(0);
+        __syncthreads();
+    }
+    for (int c = 0; c < nchunk; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < nchunk) load_chunk(klo + (c + 1) * BK);
+#pragma unroll
+        for (int kk = 0; kk < BK / 4; ++kk) {
+            double av[4], bv[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                av[x] = TA ? As[buf][kk * 4 + kl][wr * 64 + x * 16 + rl] : As[buf][wr * 64 + x * 16 + rl][kk * 4 + kl];
+#pragma unroll
+            for (int y = 0; y < 4; ++y)
+                bv[y] = TB ? Bs[buf][wc * 64 + y * 16 + rl][kk * 4 + kl] : Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 4; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+        }
+        if (c + 1 < nchunk) store_chunk(buf ^ 1);
+        __syncthreads();
+    }
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                // fp64 MFMA result: lane l register r is row (l/16) + 4r
+                const int row = mrow0 + wr * 64 + x * 16 + kl + 4 * r;
+                const int col = ncol0 + wc * 64 + y * 16 + rl;
+                if (row < g.M && col < g.N) {
+                    double* cp = C + (int64_t)(g.cm0 + row) * g.ld + g.cn0 + col;
+                    const double v = g.alpha * acc[x][y][r];
+                    *cp = (g.beta != 0.0) ? v + g.beta * (*cp) : v;
+                }
+            }
+}
+
+hipError_t gemm(bool ta, bool tb, const double* A, int a0r, int a0c, const double* B, int b0r, int b0c, double* C,
+                int cm0, int cn0, int M, int N, int K, double alpha, double beta, int flags, int mp, int nbatch,
+                int64_t bstride, hipStream_t st) {
+    GemmArgs g;
+    g.A = A;
+    g.B = B;
+    g.C = C;
+    g.ld = mp;
+    g.bstride = bstride;
+    g.a0r = a0r;
+    g.a0c = a0c;
+    g.b0r = b0r;
+    g.b0c = b0c;
+    g.cm0 = cm0;
+    g.cn0 = cn0;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.alpha = alpha;
+    g.beta = beta;
+    g.flags = flags;
+    g.tiles_m = (int)ceil_div(M, BM);
+    g.tiles_n = (int)ceil_div(N, BN);
+    const int64_t grid = (int64_t)g.tiles_m * g.tiles_n * nbatch;
+    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<false, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
+    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<false, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
+    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<true, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
+    if (ta && tb) hipLaunchKernelGGL((k_bgemm<true, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
+    return hipGetLastError();
+}
+
+// Factor and invert the diagonal block [o, o+n) of every batch item (n a
+// multiple of 64). U = L21^T (h x n2) is kept in the upper block A12.
+hipError_t factor_node(double* A, double* Linv, int o, int n, int mp, int nbatch, int64_t bstride, int* err,
+                       hipStream_t st) {
+    if (n == 64) return launch_potrf_tile(A, Linv, mp, nbatch, bstride, o / 64, err, st);
+    const int h = (n / 128) * 64;  // split at a multiple of 64; n2 >= h
+    const int n2 = n - h;
+    const int p = o + h;
+    hipError_t e = factor_node(A, Linv, o, h, mp, nbatch, bstride, err, st);
+    if (e != hipSuccess) return e;
+    // U = Linv11 A21^T (h x n2) -> A12; Linv11 lower: k < (I+1) BM
+    e = gemm(false, true, Linv, o, o, A, p, o, A, o, p, h, n2, h, 1.0, 0.0, KHI_ROW, mp, nbatch, bstride, st);
+    if (e != hipSuccess) return e;
+    // A22 -= U^T U (lower tiles)
+    e = gemm(true, false, A, o, p, A, o, p, A, p, p, n2, n2, h, -1.0, 1.0, LOWER_ONLY, mp, nbatch, bstride, st);
+    if (e != hipSuccess) return e;
+    e = factor_node(A, Linv, p, n2, mp, nbatch, bstride, err, st);
+    if (e != hipSuccess) return e;
+    // T = U^T Linv11 (n2 x h) -> A21; Linv11 lower: op(B)[k][j] = 0 for k < j
+    e = gemm(true, false, A, o, p, Linv, o, o, A, p, o, n2, h, h, 1.0, 0.0, KLO_COL, mp, nbatch, bstride, st);
+    if (e != hipSuccess) return e;
+    // Linv21 = -Linv22 T; Linv22 lower
+    return gemm(false, false, Linv, p, p, A, p, o, Linv, p, o, n2, h, n2, -1.0, 0.0, KHI_ROW, mp, nbatch, bstride,
+                st);
+}
+
+}  // namespace
+
+hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                                hipStream_t st) {
+    hipError_t e = launch_zero_upper(Linv, mp, nbatch, bstride, st);
+    if (e != hipSuccess) return e;
+    return factor_node(A, Linv, 0, mp, mp, nbatch, bstride, err, st);
+}
+
+}  // namespace mfac

@@ -67,13 +67,12 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
 // row/column k of K with p (dynamic replace).
 hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k, double mu,
                            double* A, int mp, int* err, hipStream_t st);
-// In-place lower Cholesky of nbatch matrices (mp x mp, batch stride) and the
-// inverses of its diagonal NB x NB blocks into Linv's diagonal blocks.
-hipError_t launch_potrf(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
-                        hipStream_t st);
-// Off-diagonal blocks of Linv = L^-1 (diagonal blocks from launch_potrf).
-hipError_t launch_trtri(const double* L, double* Linv, int mp, int nbatch, int64_t bstride,
-                        hipStream_t st);
+// Cholesky factor and inverse of nbatch SPD matrices (mp x mp, mp a multiple
+// of 64, batch stride bstride): Linv <- L^-1 (lower, zeros above), A is
+// consumed (its contents afterwards are scratch). err |= 2 on a non-positive
+// pivot. Recursive blocked algorithm on batched fp64 MFMA GEMMs.
+hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                                hipStream_t st);
 // Ainv = Linv^T Linv (the explicit inverse of A = L L^T), full mp x mp.
 hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, int64_t bstride, hipStream_t st);
 // O(m^2) slot replacement: K row/column k <- p and Ainv <- (A with column k
