@@ -29,7 +29,7 @@ typedef double v4d __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 128, BN = 128, BK = 16;
 constexpr int PA = BK + 2;   // pitch of [row][k] chunks (doubles)
-constexpr int PBN = BN + 4;  // pitch of a [k][n] chunk (doubles)
+constexpr int PBN = BN + 16; // pitch of a [k][n] chunk (doubles): rows k, k+1 on disjoint LDS banks
 
 enum : int {
     KHI_ROW = 1,   // A lower triangular: k < (I+1)*BM for output row tile I
@@ -62,9 +62,12 @@ struct GemmArgs {
 //   op(A)[m][k] = TA ? A[a0r+k][a0c+m] : A[a0r+m][a0c+k]
 //   op(B)[k][n] = TB ? B[b0r+n][b0c+k] : B[b0r+k][b0c+n]
 // One work-group per 128 x 128 output tile, 16-deep k-chunks through
-// double-buffered LDS with the next chunk's loads in flight.
+// double-buffered LDS with the next chunk's loads in flight; two work-groups
+// per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
+// of 64) load clamped, in-bounds data and are never stored. The elements C
+// writes are disjoint from the ones A and B read (they may share a buffer).
 template <bool TA, bool TB>
-__global__ __launch_bounds__(256) void k_bgemm(GemmArgs g) {
+__global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
     __shared__ double As[2][TA ? BK : BM][TA ? PBN : PA];
     __shared__ double Bs[2][TB ? BN : BK][TB ? PA : PBN];
@@ -78,71 +81,84 @@ __global__ __launch_bounds__(256) void k_bgemm(GemmArgs g) {
     if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BM);
     if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BN);
     if (g.flags & KLO_COL) klo = J * BN;
-    const double* A = g.A + (int64_t)bt * g.bstride;
-    const double* B = g.B + (int64_t)bt * g.bstride;
-    double* C = g.C + (int64_t)bt * g.bstride;
+    const double* __restrict__ A = g.A + (int64_t)bt * g.bstride;
+    const double* __restrict__ B = g.B + (int64_t)bt * g.bstride;
+    double* __restrict__ C = g.C + (int64_t)bt * g.bstride;
+    const int ld = g.ld;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1;
     const int rl = lane & 15, kl = lane >> 4;
     const int mrow0 = I * BM, ncol0 = J * BN;
 
     // staging of 2048 doubles per operand and chunk, 8 per thread:
-    // [row][k] layout: row tid/2, k (tid%2)*8;  [k][row] layout: k tid/16, row (tid%16)*8
+    //   [row][k] layout: row tid/2, k (tid%2)*8 .. +7 (two 64-byte row pieces)
+    //   [k][row] layout: k tid/64 + 4q, row 2*(tid%64) .. +1 (a wave per 1 KB row)
     const int sr = tid >> 1, sk = (tid & 1) * 8;
-    const int tk = tid >> 4, tn = (tid & 15) * 8;
+    const int tk = tid >> 6, tn = (tid & 63) * 2;
+    // clamped source rows / columns (M, N are even, so a clamped pair stays
+    // inside the operand)
+    const int am = min(mrow0 + (TA ? tn : sr), g.M - (TA ? 2 : 1));
+    const int bn = min(ncol0 + (TB ? sr : tn), g.N - (TB ? 1 : 2));
+    const double* __restrict__ ap =
+        TA ? A + (int64_t)g.a0r * ld + g.a0c + am : A + (int64_t)(g.a0r + am) * ld + g.a0c + sk;
+    const double* __restrict__ bp =
+        TB ? B + (int64_t)(g.b0r + bn) * ld + g.b0c + sk : B + (int64_t)g.b0r * ld + g.b0c + bn;
     double2 pa[4], pb[4];
     auto load_chunk = [&](int k0) {
-        if (TA) {
-            const double* a = A + (int64_t)(g.a0r + k0 + tk) * g.ld + g.a0c + mrow0 + tn;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                pa[q] = (mrow0 + tn + 2 * q < g.M) ? *reinterpret_cast<const double2*>(a + 2 * q) : make_double2(0.0, 0.0);
-        } else {
-            const bool ok = mrow0 + sr < g.M;
-            const double* a = A + (int64_t)(g.a0r + mrow0 + sr) * g.ld + g.a0c + k0 + sk;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) pa[q] = ok ? *reinterpret_cast<const double2*>(a + 2 * q) : make_double2(0.0, 0.0);
+        for (int q = 0; q < 4; ++q) {
+            if constexpr (TA)
+                pa[q] = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk + 4 * q) * ld);
+            else
+                pa[q] = *reinterpret_cast<const double2*>(ap + k0 + 2 * q);
+            if constexpr (TB)
+                pb[q] = *reinterpret_cast<const double2*>(bp + k0 + 2 * q);
+            else
+                pb[q] = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk + 4 * q) * ld);
         }
-        if (TB) {
-            const bool ok = ncol0 + sr < g.N;
-            const double* b = B + (int64_t)(g.b0r + ncol0 + sr) * g.ld + g.b0c + k0 + sk;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) pb[q] = ok ? *reinterpret_cast<const double2*>(b + 2 * q) : make_double2(0.0, 0.0);
-        } else {
-            const double* b = B + (int64_t)(g.b0r + k0 + tk) * g.ld + g.b0c + ncol0 + tn;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                pb[q] = (ncol0 + tn + 2 * q < g.N) ? *reinterpret_cast<const double2*>(b + 2 * q) : make_double2(0.0, 0.0);
-        }
+    };
+    auto put = [](double* dst, double2 v) {
+        dst[0] = v.x;
+        dst[1] = v.y;
     };
     auto store_chunk = [&](int buf) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            if (TA) {
-                As[buf][tk][tn + 2 * q] = pa[q].x;
-                As[buf][tk][tn + 2 * q + 1] = pa[q].y;
-            } else {
-                As[buf][sr][sk + 2 * q] = pa[q].x;
-                As[buf][sr][sk + 2 * q + 1] = pa[q].y;
-            }
-            if (TB) {
-                Bs[buf][sr][sk + 2 * q] = pb[q].x;
-                Bs[buf][sr][sk + 2 * q + 1] = pb[q].y;
-            } else {
-                Bs[buf][tk][tn + 2 * q] = pb[q].x;
-                Bs[buf][tk][tn + 2 * q + 1] = pb[q].y;
-            }
+            if constexpr (TA)
+                put(&As[buf][tk + 4 * q][tn], pa[q]);
+            else
+                put(&As[buf][sr][sk + 2 * q], pa[q]);
+            if constexpr (TB)
+                put(&Bs[buf][sr][sk + 2 * q], pb[q]);
+            else
+                put(&Bs[buf][tk + 4 * q][tn], pb[q]);
         }
     };
 
+    // C tile coordinates of accumulator (x, y, r): fp64 MFMA result register r
+    // of lane l is row (l/16) + 4r, column l%16
+    auto crow = [&](int x, int r) { return mrow0 + wr * 64 + x * 16 + kl + 4 * r; };
+    auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
+    const int nchunk = (khi - klo) / BK;
+    if (nchunk > 0) load_chunk(klo);
+    // beta C enters as the accumulator's start value (scaled by 1/alpha), so
+    // its loads issue together with the first chunk's
     v4d acc[4][4];
+    const double cs = g.beta / g.alpha;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
-    const int nchunk = (khi - klo) / BK;
+        for (int y = 0; y < 4; ++y)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                double v = 0.0;
+                if (g.beta != 0.0) {
+                    const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
+                    v = cs * C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
+                }
+                acc[x][y][r] = v;
+            }
     if (nchunk > 0) {
-        load_chunk(klo);
         store_chunk(0);
         __syncthreads();
     }
@@ -173,14 +189,8 @@ __global__ __launch_bounds__(256) void k_bgemm(GemmArgs g) {
         for (int y = 0; y < 4; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                // fp64 MFMA result: lane l register r is row (l/16) + 4r
-                const int row = mrow0 + wr * 64 + x * 16 + kl + 4 * r;
-                const int col = ncol0 + wc * 64 + y * 16 + rl;
-                if (row < g.M && col < g.N) {
-                    double* cp = C + (int64_t)(g.cm0 + row) * g.ld + g.cn0 + col;
-                    const double v = g.alpha * acc[x][y][r];
-                    *cp = (g.beta != 0.0) ? v + g.beta * (*cp) : v;
-                }
+                const int row = crow(x, r), col = ccol(y);
+                if (row < g.M && col < g.N) C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col] = g.alpha * acc[x][y][r];
             }
 }
 

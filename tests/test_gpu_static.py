@@ -49,6 +49,8 @@ def _run(dev, G, B, lam, theta, keep):
     (64, 512, 3, 1e-4, 2),         # batch boundary inside the block loop
     (1, 64, 4, 1e-2, None),        # m = 1 closed form
     (200, 2048, 2, 1e-4, None),    # the pruning block width
+    (300, 512, 3, 1e-4, None),     # padded to 320: uneven splits in the recursive factor
+    (700, 2048, 2, 1e-4, None),    # padded to 704: 11 tiles, half tiles at several levels
 ])
 def test_static_small(dev, m, B, nb, lam, batch_cap, monkeypatch):
     if batch_cap:
