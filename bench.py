@@ -25,7 +25,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 METRIC = "IHVP steps/sec and achieved HBM GB/s at d=25.6M, m=1024 (1 GPU)"
 COUNTERS = os.path.join(ROOT, "profiles", "pass_kernels_hbm_counters.txt")
-PASS_SRC = os.path.join(ROOT, "paper_2107_03356_amd", "csrc", "pass.hip")
+PASS_SRC = [os.path.join(ROOT, "paper_2107_03356_amd", "csrc", f) for f in ("pass.hip", "device_util.h")]
 
 
 def log(*a):
@@ -42,13 +42,21 @@ def pass_bytes(d, m):
     return 4 * (m + 1) * d, 4 * (m + 1) * d, 4 * 2 * d
 
 
+def pass_src_sha():
+    """First 16 hex digits of the SHA-256 over the streaming kernels' sources."""
+    h = hashlib.sha256()
+    for path in PASS_SRC:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()[:16]
+
+
 def read_counters(kernel):
     """HBM traffic per launch from the committed rocprofv3 --pmc summary, if it
-    was taken on the current pass.hip (else None)."""
+    was taken on the current streaming-kernel sources (else None)."""
     if not os.path.exists(COUNTERS):
         return None
     text = open(COUNTERS).read()
-    sha = hashlib.sha256(open(PASS_SRC, "rb").read()).hexdigest()[:16]
+    sha = pass_src_sha()
     m = re.search(r"pass_src_sha256_16:\s*(\w+)", text)
     if not m or m.group(1) != sha:
         return None
