@@ -169,6 +169,164 @@ def bench_static(args, wl, dev):
     print(json.dumps(out), flush=True)
 
 
+def resnet20(num_classes=10):
+    """CIFAR ResNet-20 (3 stages x 3 basic blocks, 16/32/64 channels, identity
+    shortcuts that subsample and zero-pad channels): 269,722 weights."""
+    import torch
+    import torch.nn as nn
+    import torch.nn.functional as F
+
+    class Block(nn.Module):
+        def __init__(self, cin, cout, stride):
+            super().__init__()
+            self.c1 = nn.Conv2d(cin, cout, 3, stride, 1, bias=False)
+            self.b1 = nn.BatchNorm2d(cout)
+            self.c2 = nn.Conv2d(cout, cout, 3, 1, 1, bias=False)
+            self.b2 = nn.BatchNorm2d(cout)
+            self.stride, self.pad = stride, cout - cin
+
+        def forward(self, x):
+            out = F.relu(self.b1(self.c1(x)))
+            out = self.b2(self.c2(out))
+            sc = x[:, :, ::self.stride, ::self.stride] if self.stride > 1 else x
+            if self.pad:
+                sc = F.pad(sc, (0, 0, 0, 0, self.pad // 2, self.pad - self.pad // 2))
+            return F.relu(out + sc)
+
+    class Net(nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.c = nn.Conv2d(3, 16, 3, 1, 1, bias=False)
+            self.b = nn.BatchNorm2d(16)
+            layers, cin = [], 16
+            for cout, stride in ((16, 1), (32, 2), (64, 2)):
+                for i in range(3):
+                    layers.append(Block(cin, cout, stride if i == 0 else 1))
+                    cin = cout
+            self.layers = nn.Sequential(*layers)
+            self.fc = nn.Linear(64, num_classes)
+
+        def forward(self, x):
+            x = self.layers(F.relu(self.b(self.c(x))))
+            return self.fc(torch.flatten(F.adaptive_avg_pool2d(x, 1), 1))
+
+    return Net()
+
+
+def bench_optimizer(args, wl, dev):
+    """Training steps (forward + backward + optimizer) of a CIFAR-shaped
+    ResNet-20 with M-FAC (window m) and, in the same process, with SGD
+    (momentum 0.9): M-FAC steps/s and its overhead over SGD (Section 4.2,
+    Table 4's metric). Random-init weights, random inputs and labels resident
+    in HBM."""
+    import torch
+
+    import paper_2107_03356_amd as P
+    from paper_2107_03356_amd.optim import MFAC
+
+    P.load()
+    torch.cuda.set_device(dev)
+    torch.backends.cudnn.benchmark = True
+    g = torch.Generator(device="cpu")
+    g.manual_seed(args.seed)
+    nb = 16
+    xs = torch.randn((nb, wl.batch, 3, 32, 32), generator=g).to(dev)
+    ys = torch.randint(0, 10, (nb, wl.batch), generator=g).to(dev)
+    lossf = torch.nn.CrossEntropyLoss()
+
+    def make(opt_name):
+        torch.manual_seed(args.seed)
+        net = resnet20().to(dev)
+        d = sum(p.numel() for p in net.parameters())
+        assert d == wl.d, d
+        if opt_name == "sgd":
+            opt = torch.optim.SGD(net.parameters(), lr=0.1, momentum=0.9, weight_decay=5e-4, foreach=True)
+        else:
+            opt = MFAC(net.parameters(), lr=1e-3, m=wl.m, damp=wl.lam, weight_decay=5e-4)
+        return net, opt
+
+    def run(net, opt, t0, n):
+        for t in range(t0, t0 + n):
+            opt.zero_grad(set_to_none=True)
+            lossf(net(xs[t % nb]), ys[t % nb]).backward()
+            opt.step()
+
+    stream = torch.cuda.current_stream(dev)
+    res = {}
+    for name in ("sgd", "mfac"):
+        net, opt = make(name)
+        run(net, opt, 0, args.warmup)
+        torch.cuda.synchronize()
+        if name == "mfac":
+            opt.window.trace_read()
+            opt.window.trace(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run(net, opt, args.warmup, args.steps)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / args.steps
+        log(f"{name}: {res[name]:.3f} ms/step")
+        if name == "mfac":
+            opt.window.trace(False)
+            ph_ms, ph_cnt = opt.window.trace_read()
+            if opt.status() != 0:
+                log("device error in the M-FAC step")
+                sys.exit(1)
+            mfac_opt = opt
+        del net
+    avg = [ph_ms[i] / max(ph_cnt[i], 1) for i in range(4)]
+    b1, b2, bw = pass_bytes(wl.d, wl.m)
+    gbs1 = b1 / (avg[0] * 1e-3) / 1e9
+    gbs2 = b2 / (avg[2] * 1e-3) / 1e9
+    kname, achieved = ("k_pass1", gbs1) if avg[0] >= avg[2] else ("k_pass2", gbs2)
+    out = {
+        "metric": "M-FAC training steps/s on a CIFAR-shaped ResNet-20, batch 128, m = 512 (overhead over SGD)",
+        "value": 1000.0 / res["mfac"], "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": res["mfac"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "model": "resnet20 (random init)", "d": wl.d, "m": wl.m,
+                   "global_batch": wl.batch, "image": [3, 32, 32], "damp": wl.lam},
+        "sgd_ms_per_step": res["sgd"],
+        "overhead_over_sgd": res["mfac"] / res["sgd"],
+        "mfac_phases_ms_per_step": {"row_write": avg[3], "pass1": avg[0], "coefficients": avg[1], "pass2": avg[2]},
+        "roofline": {"bound": "hbm", "kernel": kname, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "cpu_baseline": None,
+    }
+    del mfac_opt
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_optimizer_baseline(wl, args.seed, args.cpu_steps)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_optimizer_baseline(wl, seed, nsteps):
+    """The oracle's M-FAC step (window insert + F^-1 g, fp64) at the model's d
+    and m, on a full window, without the model's forward/backward."""
+    import numpy as np
+
+    from oracle.optimizer import MFACOracle
+    from synth import GradientStream
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    gs = GradientStream(wl, seed=seed)
+    orc = MFACOracle(wl.d, wl.m, wl.lam)
+    for r in range(wl.m):
+        orc.window.replace(r, gs.row(r).numpy())
+    w = np.zeros(wl.d)
+    t0 = time.perf_counter()
+    for t in range(nsteps):
+        w, _ = orc.step(w, gs.step_row(t).numpy(), 1e-3)
+    sec = (time.perf_counter() - t0) / nsteps
+    return {"value": 1.0 / sec, "unit": "optimizer steps/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{nsteps} oracle M-FAC steps (fp64 window insert + F^-1 g) at d={wl.d}, m={wl.m}, "
+                      "full window, model forward/backward excluded"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -195,6 +353,8 @@ def main():
     dev = torch.device("cuda:0")
     if wl.kind == "static":
         return bench_static(args, wl, dev)
+    if wl.kind == "optim":
+        return bench_optimizer(args, wl, dev)
     torch.cuda.set_device(dev)
     P.load()
     d, m = wl.d, wl.m

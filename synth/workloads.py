@@ -21,7 +21,7 @@ from typing import Optional
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str            # "dynamic" or "static"
+    kind: str            # "dynamic", "static" or "optim"
     d: int
     m: int
     lam: float
@@ -34,6 +34,7 @@ class Workload:
     fill_by_replace: bool = False   # dynamic: start empty, fill with m replaces
     scale_d: int = 0     # d in the 1/sqrt(d) entry scale (0: the workload's own d);
                          # reduced-size parity cases keep the full-size scale
+    batch: int = 0       # optim: mini-batch size of the model's synthetic batches
 
     def scaled(self, **kw) -> "Workload":
         """Same recipe at another size (parity cases the oracle finishes in seconds)."""
@@ -61,6 +62,11 @@ WORKLOADS = {
     "static_d4.19m_b2048_m1024": Workload(
         "static_d4.19m_b2048_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
         dist="lognormal", block=2048, theta_std=0.05),
+    # the optimizer loop on a CIFAR-shaped ResNet-20 (269,722 weights), batch 128,
+    # window m = 512 (Section 4.2, Table 4 settings); random inputs and labels
+    "optim_resnet20_cifar_b128_m512": Workload(
+        "optim_resnet20_cifar_b128_m512", "optim", d=269_722, m=512, lam=1e-4,
+        dist="gauss", steps=100, batch=128),
 }
 
 HEADLINE = "dyn_resnet50_d25.6m_m1024"

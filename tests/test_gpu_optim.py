@@ -1,0 +1,144 @@
+"""GPU parity of the M-FAC optimizer loop (Section 4.2) against the fp64 oracle.
+
+The GPU side trains fp32 torch parameters with paper_2107_03356_amd.optim.MFAC;
+the oracle side runs the same loop on a flat float64 vector with CPU fp64
+gradients. Both start from the same seeded weights and see the same seeded
+loss coefficients / mini-batches; neither sees the other's outputs.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import require_gpu, say
+from oracle.optimizer import MFACOracle
+from synth.optim import linear_problem, mlp_problem
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def _flat(ts):
+    return np.concatenate([t.detach().cpu().double().reshape(-1).numpy() for t in ts])
+
+
+def _disp_err(w_gpu, w_or, w0):
+    """|w_gpu - w_or| relative to the distance travelled |w_or - w0|."""
+    return np.linalg.norm(w_gpu - w_or) / np.linalg.norm(w_or - w0)
+
+
+def test_linear_loss_two_groups_matches_oracle(dev):
+    """Gradients independent of w (loss_t = sum <C_t, w>): both sides see the
+    same sequence. Two groups with their own lr and weight decay, window
+    wraps twice."""
+    from paper_2107_03356_amd.optim import MFAC
+    shapes = [(7, 5), (13,), (3, 4, 2)]
+    steps, m, lam = 11, 4, 0.5
+    w0, C = linear_problem(seed=3, shapes=shapes, steps=steps)
+    w0 = [w.float().double() for w in w0]                 # both start from the fp32 weights
+    C = [[c.float() for c in ct] for ct in C]
+    params = [torch.nn.Parameter(w.float().to(dev)) for w in w0]
+    opt = MFAC([{"params": params[:2], "lr": 0.1, "weight_decay": 0.01},
+                {"params": params[2:], "lr": 0.05, "weight_decay": 0.0}], lr=0.1, m=m, damp=lam)
+    n01 = sum(int(np.prod(s)) for s in shapes[:2])
+    d = sum(int(np.prod(s)) for s in shapes)
+    lr = np.where(np.arange(d) < n01, 0.1, 0.05)
+    wd = np.where(np.arange(d) < n01, 0.01, 0.0)
+    orc = MFACOracle(d, m, lam)
+    w_or = _flat(w0)
+    w_start = w_or.copy()
+    say("optimizer linear loss", d, m)
+    for t in range(steps):
+        opt.zero_grad()
+        loss = sum((c.to(dev) * p).sum() for c, p in zip(C[t], params))
+        loss.backward()
+        opt.step()
+        w_or, _ = orc.step(w_or, _flat(C[t]), lr, wd)
+        err = _disp_err(_flat(params), w_or, w_start)
+        assert err < 1e-5, (t, err)
+    torch.cuda.synchronize()
+    assert opt.status() == 0
+
+
+def _mlp_loss(ws, x, y):
+    h = x
+    for i in range(0, len(ws) - 2, 2):
+        h = torch.tanh(h @ ws[i].T + ws[i + 1])
+    out = h @ ws[-2].T + ws[-1]
+    return 0.5 * ((out - y) ** 2).sum(dim=1).mean()
+
+
+def test_mlp_training_matches_oracle(dev):
+    """A tanh MLP trained for 12 steps (window of 6 wraps): fp32 GPU training
+    against the fp64 oracle loop with fp64 autograd gradients."""
+    from paper_2107_03356_amd.optim import MFAC
+    sizes, batch, steps, m, lam, lr = (20, 32, 8), 16, 12, 6, 1e-2, 0.05
+    ws, data = mlp_problem(seed=4, sizes=sizes, batch=batch, steps=steps)
+    ws = [w.float().double() for w in ws]
+    params = [torch.nn.Parameter(w.float().to(dev)) for w in ws]
+    opt = MFAC(params, lr=lr, m=m, damp=lam)
+    d = sum(w.numel() for w in ws)
+    orc = MFACOracle(d, m, lam)
+    w_or = _flat(ws)
+    w_start = w_or.copy()
+    say("optimizer mlp", d, m)
+    for t in range(steps):
+        x, y = data[t]
+        opt.zero_grad()
+        _mlp_loss(params, x.float().to(dev), y.float().to(dev)).backward()
+        opt.step()
+        # oracle: fp64 autograd at the oracle's own weights
+        wt, off = [], 0
+        for w in ws:
+            n = w.numel()
+            wt.append(torch.tensor(w_or[off:off + n].reshape(tuple(w.shape)), requires_grad=True))
+            off += n
+        _mlp_loss(wt, x, y).backward()
+        w_or, _ = orc.step(w_or, _flat([w.grad for w in wt]), lr)
+        err = _disp_err(_flat(params), w_or, w_start)
+        assert err < 1e-3, (t, err)
+    torch.cuda.synchronize()
+    assert opt.status() == 0
+
+
+def test_checkpoint_resume_continues_the_run(dev):
+    """state_dict after 5 steps, a fresh optimizer loads it and runs 6 more:
+    same weights as the uninterrupted run (the reload refactors the window)."""
+    from paper_2107_03356_amd.optim import MFAC
+    shapes = [(40, 9), (9,)]
+    steps, m, lam = 11, 4, 0.5
+    w0, C = linear_problem(seed=5, shapes=shapes, steps=steps)
+
+    def run(split):
+        params = [torch.nn.Parameter(w.float().to(dev)) for w in w0]
+        opt = MFAC(params, lr=0.1, m=m, damp=lam, weight_decay=0.02)
+        for t in range(steps):
+            if t == split:
+                sd = opt.state_dict()
+                params = [torch.nn.Parameter(p.detach().clone()) for p in params]
+                opt = MFAC(params, lr=0.1, m=m, damp=lam, weight_decay=0.02)
+                opt.load_state_dict(sd)
+            opt.zero_grad()
+            sum((c.float().to(dev) * p).sum() for c, p in zip(C[t], params)).backward()
+            opt.step()
+        torch.cuda.synchronize()
+        assert opt.status() == 0 and opt.steps == steps
+        return _flat(params)
+
+    say("optimizer checkpoint/resume")
+    straight = run(split=-1)
+    resumed = run(split=5)
+    start = _flat(w0)
+    assert _disp_err(resumed, straight, start) < 1e-5
+
+
+def test_rejects_cpu_and_half_parameters(dev):
+    from paper_2107_03356_amd.optim import MFAC
+    with pytest.raises(ValueError):
+        MFAC([torch.nn.Parameter(torch.zeros(4))], lr=0.1, m=2)
+    with pytest.raises(ValueError):
+        MFAC([torch.nn.Parameter(torch.zeros(4, device=dev, dtype=torch.float16))], lr=0.1, m=2)
