@@ -155,8 +155,42 @@ def bench_static(args, wl, dev):
         if rep >= args.warmup:
             times.append(e0.elapsed_time(e1))
         log(f"rep {rep}: {e0.elapsed_time(e1):.1f} ms")
-        sb.close()
+        if rep + 1 < args.warmup + args.steps:
+            sb.close()
     ms = sum(times) / len(times)
+
+    # queries on the finished precompute (W in place of G): block-wise IHVP
+    # with 1 and 4 vectors, and the OBS correction for the keep-mask's complement
+    queries = {}
+    X = torch.empty((4, d), dtype=torch.float32, device=dev)
+    for q in range(4):
+        X[q] = gs.queries(0, 4)[q]
+    reps = 10
+    for n in (1, 4):
+        Y = torch.empty((n, d), dtype=torch.float32, device=dev)
+        sb.ihvp(X[:n], Y)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            sb.ihvp(X[:n], Y)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        qms = e0.elapsed_time(e1) / reps
+        qbytes = 2 * 4 * m * d + 4 * 3 * n * d      # W read twice; X read twice, Y written
+        queries[f"ihvp_n{n}"] = {"ms": qms, "hbm_gbs": qbytes / (qms * 1e-3) / 1e9}
+    delta = sb.obs_update(theta, mask)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        sb.obs_update(theta, mask, delta)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    queries["obs_update"] = {"ms": e0.elapsed_time(e1) / reps}
+    if sb.status() != 0:
+        log("device error in the static queries")
+        sys.exit(1)
+    sb.close()
+    log(f"queries: {queries}")
     out = {
         "metric": "static block-wise precompute + inverse diagonal + top-50% OBD mask, runs/sec (1 GPU)",
         "value": 1000.0 / ms, "unit": "runs/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -165,6 +199,7 @@ def bench_static(args, wl, dev):
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep},
         "roofline": {"bound": "mfma", "achieved": flops / (ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
                      "frac": flops / (ms * 1e-3) / 1e12 / 78.6, "traffic": None},
+        "queries": queries,
     }
     print(json.dumps(out), flush=True)
 

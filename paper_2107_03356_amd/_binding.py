@@ -297,11 +297,13 @@ class StaticBlocks:
         _check("mfac_static_element", load().mfac_static_element(self.handle, ij.shape[0], _ptr(ij), _ptr(out)))
         return out
 
-    def obs_update(self, theta, keep_mask):
+    def obs_update(self, theta, keep_mask, delta=None):
         """OBS correction delta (fp32, d) for removing the coordinates outside keep_mask."""
         t = self.torch
         assert theta.dtype == t.float32 and keep_mask.dtype == t.uint8
-        delta = t.empty(self.d, dtype=t.float32, device=self.device)
+        if delta is None:
+            delta = t.empty(self.d, dtype=t.float32, device=self.device)
+        assert delta.dtype == t.float32 and delta.is_contiguous() and delta.numel() == self.d
         _check("mfac_obs_update", load().mfac_obs_update(self.handle, _ptr(theta), _ptr(keep_mask), _ptr(delta)))
         return delta
 
