@@ -5,6 +5,7 @@ The shared library lands next to this file; nothing is installed elsewhere.
 """
 
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -40,10 +41,23 @@ def build(verbose: bool = False) -> str:
     objs = []
     for src in SOURCES:
         obj = os.path.join(out_dir, src.replace(".hip", ".o"))
-        cmd = [cc, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [cc, *FLAGS, "-Rpass-analysis=kernel-resource-usage", "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True)
+        r = subprocess.run(cmd, stderr=subprocess.PIPE, text=True)
+        if r.returncode != 0:
+            sys.stderr.write(r.stderr)
+            raise subprocess.CalledProcessError(r.returncode, cmd)
+        # kernels that use per-lane scratch (arrays the compiler did not keep
+        # in registers) are a performance bug: report them
+        name = None
+        for line in r.stderr.splitlines():
+            m = re.search(r"Function Name: (\S+)", line)
+            if m:
+                name = m.group(1)
+            m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+            if m and int(m.group(1)) > 0:
+                print(f"[build] warning: {src}: {name} uses {m.group(1)} bytes/lane of scratch", file=sys.stderr)
         objs.append(obj)
     tmp = LIB + ".tmp"
     cmd = [cc, *FLAGS, "-shared", *objs, "-o", tmp]

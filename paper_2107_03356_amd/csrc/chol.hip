@@ -194,12 +194,10 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
     for (int c = 0; c < 64; ++c) Lb[(int64_t)i * mp + c] = T[i][c];
 }
 
-__global__ __launch_bounds__(256) void k_zero_upper(double* __restrict__ Linv, int mp, int64_t bstride) {
-    // zero the strictly-upper tiles of Linv (tile (i, j) with j > i); grid (T*T, nbatch)
-    const int T = mp / 64;
-    const int ti = blockIdx.x / T, tj = blockIdx.x % T;
-    if (tj <= ti) return;
-    double* C = Linv + (int64_t)blockIdx.y * bstride + (int64_t)ti * 64 * mp + tj * 64;
+__global__ __launch_bounds__(256) void k_zero_superdiag(double* __restrict__ Linv, int mp, int64_t bstride) {
+    // zero the first superdiagonal of 64 x 64 tiles, (t, t+1); grid (T-1, nbatch)
+    const int t = blockIdx.x;
+    double* C = Linv + (int64_t)blockIdx.y * bstride + (int64_t)t * 64 * mp + (t + 1) * 64;
     for (int e = threadIdx.x; e < 4096; e += 256) C[(int64_t)(e >> 6) * mp + (e & 63)] = 0.0;
 }
 
@@ -349,9 +347,10 @@ hipError_t launch_potrf_tile(double* A, double* Linv, int mp, int nbatch, int64_
     return hipGetLastError();
 }
 
-hipError_t launch_zero_upper(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st) {
+hipError_t launch_zero_superdiag(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st) {
     const int T = mp / 64;
-    hipLaunchKernelGGL(k_zero_upper, dim3(T * T, nbatch), dim3(256), 0, st, M, mp, bstride);
+    if (T < 2) return hipSuccess;
+    hipLaunchKernelGGL(k_zero_superdiag, dim3(T - 1, nbatch), dim3(256), 0, st, M, mp, bstride);
     return hipGetLastError();
 }
 

@@ -15,17 +15,16 @@
 // triangular operand makes zero, so the flops are m^3/3 for the factor and
 // m^3/3 for the inverse, nearly all of it in large MFMA tiles.
 #include "internal.h"
+#include "tile_util.h"
 
 namespace mfac {
 
 // defined in chol.hip
 hipError_t launch_potrf_tile(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int t, int* err,
                              hipStream_t st);
-hipError_t launch_zero_upper(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st);
+hipError_t launch_zero_superdiag(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st);
 
 namespace {
-
-typedef double v4d __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 128, BN = 128, BK = 16;
 constexpr int PA = BK + 2;   // pitch of [row][k] chunks (doubles)
@@ -37,11 +36,6 @@ enum : int {
     KLO_COL = 4,   // op(B) lower triangular: k >= J*BN
     LOWER_ONLY = 8 // only output tiles with I >= J
 };
-
-__device__ __forceinline__ int xcd_remap(int p, int n) {
-    if (n % 8) return p;
-    return (p % 8) * (n / 8) + p / 8;
-}
 
 struct GemmArgs {
     const double* A;
@@ -56,14 +50,53 @@ struct GemmArgs {
     double alpha, beta;
     int flags;
     int tiles_m, tiles_n;
+    int mode;   // task layout, see task_tiles
+    int ntask;  // tasks per batch item
 };
+
+enum : int {
+    TASK_PLAIN = 0,      // one tile per task
+    TASK_LOWER = 1,      // lower-triangle tiles only (I >= J), compact
+    TASK_PAIR_ROWS = 2,  // tiles (i, J) and (T-1-i, J): equal total K range under KHI_ROW
+    TASK_PAIR_COLS = 3   // tiles (I, j) and (I, T-1-j): equal total K range under KLO_COL / KHI_COL
+};
+
+// Output tiles of one task (I1 < 0: a single tile).
+__device__ __forceinline__ void task_tiles(const GemmArgs& g, int t, int& I0, int& J0, int& I1, int& J1) {
+    I1 = J1 = -1;
+    if (g.mode == TASK_LOWER) {
+        int i = (int)((sqrtf(8.0f * (float)t + 1.0f) - 1.0f) * 0.5f);
+        while ((i + 1) * (i + 2) / 2 <= t) ++i;
+        while (i * (i + 1) / 2 > t) --i;
+        I0 = i;
+        J0 = t - i * (i + 1) / 2;
+    } else if (g.mode == TASK_PAIR_ROWS) {
+        const int i = t / g.tiles_n;
+        J0 = J1 = t - i * g.tiles_n;
+        I0 = i;
+        if (g.tiles_m - 1 - i != i) I1 = g.tiles_m - 1 - i;
+        else J1 = -1;
+    } else if (g.mode == TASK_PAIR_COLS) {
+        const int half = (g.tiles_n + 1) / 2;
+        const int j = t % half;
+        I0 = I1 = t / half;
+        J0 = j;
+        if (g.tiles_n - 1 - j != j) J1 = g.tiles_n - 1 - j;
+        else I1 = -1;
+    } else {
+        I0 = t / g.tiles_n;
+        J0 = t - I0 * g.tiles_n;
+    }
+}
 
 // C = alpha * op(A) op(B) + beta * C on sub-matrices of every batch item:
 //   op(A)[m][k] = TA ? A[a0r+k][a0c+m] : A[a0r+m][a0c+k]
 //   op(B)[k][n] = TB ? B[b0r+n][b0c+k] : B[b0r+k][b0c+n]
-// One work-group per 128 x 128 output tile, 16-deep k-chunks through
-// double-buffered LDS with the next chunk's loads in flight; two work-groups
-// per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
+// One work-group per task of one or two 128 x 128 output tiles (a long and a
+// short tile of a triangular product together, so tasks take equal time;
+// lower-triangle products launch only their lower tiles), 16-deep k-chunks
+// through double-buffered LDS with the next chunk's loads in flight; two
+// work-groups per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
 // of 64) load clamped, in-bounds data and are never stored. The elements C
 // writes are disjoint from the ones A and B read (they may share a buffer).
 template <bool TA, bool TB>
@@ -71,16 +104,10 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
     __shared__ double As[2][TA ? BK : BM][TA ? PBN : PA];
     __shared__ double Bs[2][TB ? BN : BK][TB ? PA : PBN];
-    const int ntile = g.tiles_m * g.tiles_n;
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
-    const int bt = lid / ntile;
-    const int tt = lid - bt * ntile;
-    const int I = tt / g.tiles_n, J = tt - (tt / g.tiles_n) * g.tiles_n;
-    if ((g.flags & LOWER_ONLY) && I < J) return;
-    int klo = 0, khi = g.K;
-    if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BM);
-    if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BN);
-    if (g.flags & KLO_COL) klo = J * BN;
+    const int bt = lid / g.ntask;
+    int I0, J0, I1, J1;
+    task_tiles(g, lid - bt * g.ntask, I0, J0, I1, J1);
     const double* __restrict__ A = g.A + (int64_t)bt * g.bstride;
     const double* __restrict__ B = g.B + (int64_t)bt * g.bstride;
     double* __restrict__ C = g.C + (int64_t)bt * g.bstride;
@@ -88,110 +115,121 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1;
     const int rl = lane & 15, kl = lane >> 4;
-    const int mrow0 = I * BM, ncol0 = J * BN;
+    auto tile = [&](int I, int J) {
+        int klo = 0, khi = g.K;
+        if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BM);
+        if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BN);
+        if (g.flags & KLO_COL) klo = J * BN;
+        const int mrow0 = I * BM, ncol0 = J * BN;
 
-    // staging of 2048 doubles per operand and chunk, 8 per thread:
-    //   [row][k] layout: row tid/2, k (tid%2)*8 .. +7 (two 64-byte row pieces)
-    //   [k][row] layout: k tid/64 + 4q, row 2*(tid%64) .. +1 (a wave per 1 KB row)
-    const int sr = tid >> 1, sk = (tid & 1) * 8;
-    const int tk = tid >> 6, tn = (tid & 63) * 2;
-    // clamped source rows / columns (M, N are even, so a clamped pair stays
-    // inside the operand)
-    const int am = min(mrow0 + (TA ? tn : sr), g.M - (TA ? 2 : 1));
-    const int bn = min(ncol0 + (TB ? sr : tn), g.N - (TB ? 1 : 2));
-    const double* __restrict__ ap =
-        TA ? A + (int64_t)g.a0r * ld + g.a0c + am : A + (int64_t)(g.a0r + am) * ld + g.a0c + sk;
-    const double* __restrict__ bp =
-        TB ? B + (int64_t)(g.b0r + bn) * ld + g.b0c + sk : B + (int64_t)g.b0r * ld + g.b0c + bn;
-    double2 pa[4], pb[4];
-    auto load_chunk = [&](int k0) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if constexpr (TA)
-                pa[q] = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk + 4 * q) * ld);
-            else
-                pa[q] = *reinterpret_cast<const double2*>(ap + k0 + 2 * q);
-            if constexpr (TB)
-                pb[q] = *reinterpret_cast<const double2*>(bp + k0 + 2 * q);
-            else
-                pb[q] = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk + 4 * q) * ld);
-        }
-    };
-    auto put = [](double* dst, double2 v) {
-        dst[0] = v.x;
-        dst[1] = v.y;
-    };
-    auto store_chunk = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if constexpr (TA)
-                put(&As[buf][tk + 4 * q][tn], pa[q]);
-            else
-                put(&As[buf][sr][sk + 2 * q], pa[q]);
-            if constexpr (TB)
-                put(&Bs[buf][sr][sk + 2 * q], pb[q]);
-            else
-                put(&Bs[buf][tk + 4 * q][tn], pb[q]);
-        }
-    };
-
-    // C tile coordinates of accumulator (x, y, r): fp64 MFMA result register r
-    // of lane l is row (l/16) + 4r, column l%16
-    auto crow = [&](int x, int r) { return mrow0 + wr * 64 + x * 16 + kl + 4 * r; };
-    auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
-    const int nchunk = (khi - klo) / BK;
-    if (nchunk > 0) load_chunk(klo);
-    // beta C enters as the accumulator's start value (scaled by 1/alpha), so
-    // its loads issue together with the first chunk's
-    v4d acc[4][4];
-    const double cs = g.beta / g.alpha;
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                double v = 0.0;
-                if (g.beta != 0.0) {
-                    const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
-                    v = cs * C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
-                }
-                acc[x][y][r] = v;
+        // staging of 2048 doubles per operand and chunk, 8 per thread:
+        //   [row][k] layout: row tid/2, k (tid%2)*8 .. +7 (two 64-byte row pieces)
+        //   [k][row] layout: k tid/64 + 4q, row 2*(tid%64) .. +1 (a wave per 1 KB row)
+        const int sr = tid >> 1, sk = (tid & 1) * 8;
+        const int tk = tid >> 6, tn = (tid & 63) * 2;
+        // clamped source rows / columns (M, N are even, so a clamped pair stays
+        // inside the operand)
+        const int am = min(mrow0 + (TA ? tn : sr), g.M - (TA ? 2 : 1));
+        const int bn = min(ncol0 + (TB ? sr : tn), g.N - (TB ? 1 : 2));
+        const double* __restrict__ ap =
+            TA ? A + (int64_t)g.a0r * ld + g.a0c + am : A + (int64_t)(g.a0r + am) * ld + g.a0c + sk;
+        const double* __restrict__ bp =
+            TB ? B + (int64_t)(g.b0r + bn) * ld + g.b0c + sk : B + (int64_t)g.b0r * ld + g.b0c + bn;
+        double2 pa[4], pb[4];
+        auto load_chunk = [&](int k0) {
+    #pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if constexpr (TA)
+                    pa[q] = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk + 4 * q) * ld);
+                else
+                    pa[q] = *reinterpret_cast<const double2*>(ap + k0 + 2 * q);
+                if constexpr (TB)
+                    pb[q] = *reinterpret_cast<const double2*>(bp + k0 + 2 * q);
+                else
+                    pb[q] = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk + 4 * q) * ld);
             }
-    if (nchunk > 0) {
-        store_chunk(0);
-        __syncthreads();
-    }
-    for (int c = 0; c < nchunk; ++c) {
-        const int buf = c & 1;
-        if (c + 1 < nchunk) load_chunk(klo + (c + 1) * BK);
-#pragma unroll
-        for (int kk = 0; kk < BK / 4; ++kk) {
-            double av[4], bv[4];
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-                av[x] = TA ? As[buf][kk * 4 + kl][wr * 64 + x * 16 + rl] : As[buf][wr * 64 + x * 16 + rl][kk * 4 + kl];
-#pragma unroll
+        };
+        auto put = [](double* dst, double2 v) {
+            dst[0] = v.x;
+            dst[1] = v.y;
+        };
+        auto store_chunk = [&](int buf) {
+    #pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if constexpr (TA)
+                    put(&As[buf][tk + 4 * q][tn], pa[q]);
+                else
+                    put(&As[buf][sr][sk + 2 * q], pa[q]);
+                if constexpr (TB)
+                    put(&Bs[buf][sr][sk + 2 * q], pb[q]);
+                else
+                    put(&Bs[buf][tk + 4 * q][tn], pb[q]);
+            }
+        };
+
+        // C tile coordinates of accumulator (x, y, r): fp64 MFMA result register r
+        // of lane l is row (l/16) + 4r, column l%16
+        auto crow = [&](int x, int r) { return mrow0 + wr * 64 + x * 16 + kl + 4 * r; };
+        auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
+        const int nchunk = (khi - klo) / BK;
+        if (nchunk > 0) load_chunk(klo);
+        // beta C enters as the accumulator's start value (scaled by 1/alpha), so
+        // its loads issue together with the first chunk's
+        v4d acc[4][4];
+        const double cs = g.beta / g.alpha;
+    #pragma unroll
+        for (int x = 0; x < 4; ++x)
+    #pragma unroll
             for (int y = 0; y < 4; ++y)
-                bv[y] = TB ? Bs[buf][wc * 64 + y * 16 + rl][kk * 4 + kl] : Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
-#pragma unroll
-                for (int y = 0; y < 4; ++y)
-                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    double v = 0.0;
+                    if (g.beta != 0.0) {
+                        const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
+                        v = cs * C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
+                    }
+                    acc[x][y][r] = v;
+                }
+        if (nchunk > 0) {
+            store_chunk(0);
+            __syncthreads();
         }
-        if (c + 1 < nchunk) store_chunk(buf ^ 1);
-        __syncthreads();
-    }
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = crow(x, r), col = ccol(y);
-                if (row < g.M && col < g.N) C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col] = g.alpha * acc[x][y][r];
+        for (int c = 0; c < nchunk; ++c) {
+            const int buf = c & 1;
+            if (c + 1 < nchunk) load_chunk(klo + (c + 1) * BK);
+    #pragma unroll
+            for (int kk = 0; kk < BK / 4; ++kk) {
+                double av[4], bv[4];
+    #pragma unroll
+                for (int x = 0; x < 4; ++x)
+                    av[x] = TA ? As[buf][kk * 4 + kl][wr * 64 + x * 16 + rl] : As[buf][wr * 64 + x * 16 + rl][kk * 4 + kl];
+    #pragma unroll
+                for (int y = 0; y < 4; ++y)
+                    bv[y] = TB ? Bs[buf][wc * 64 + y * 16 + rl][kk * 4 + kl] : Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
+    #pragma unroll
+                for (int x = 0; x < 4; ++x)
+    #pragma unroll
+                    for (int y = 0; y < 4; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
+            if (c + 1 < nchunk) store_chunk(buf ^ 1);
+            __syncthreads();
+        }
+    #pragma unroll
+        for (int x = 0; x < 4; ++x)
+    #pragma unroll
+            for (int y = 0; y < 4; ++y)
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = crow(x, r), col = ccol(y);
+                    if (row < g.M && col < g.N) C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col] = g.alpha * acc[x][y][r];
+                }
+    };
+    tile(I0, J0);
+    if (I1 >= 0) {
+        __syncthreads();
+        tile(I1, J1);
+    }
 }
 
 hipError_t gemm(bool ta, bool tb, const double* A, int a0r, int a0c, const double* B, int b0r, int b0c, double* C,
@@ -217,7 +255,20 @@ hipError_t gemm(bool ta, bool tb, const double* A, int a0r, int a0c, const doubl
     g.flags = flags;
     g.tiles_m = (int)ceil_div(M, BM);
     g.tiles_n = (int)ceil_div(N, BN);
-    const int64_t grid = (int64_t)g.tiles_m * g.tiles_n * nbatch;
+    if (flags & LOWER_ONLY) {
+        g.mode = TASK_LOWER;  // square: tiles_m == tiles_n
+        g.ntask = g.tiles_m * (g.tiles_m + 1) / 2;
+    } else if (flags & KHI_ROW) {
+        g.mode = TASK_PAIR_ROWS;
+        g.ntask = (g.tiles_m + 1) / 2 * g.tiles_n;
+    } else if (flags & (KLO_COL | KHI_COL)) {
+        g.mode = TASK_PAIR_COLS;
+        g.ntask = g.tiles_m * ((g.tiles_n + 1) / 2);
+    } else {
+        g.mode = TASK_PLAIN;
+        g.ntask = g.tiles_m * g.tiles_n;
+    }
+    const int64_t grid = (int64_t)g.ntask * nbatch;
     if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<false, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
     if (!ta && tb) hipLaunchKernelGGL((k_bgemm<false, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
     if (ta && !tb) hipLaunchKernelGGL((k_bgemm<true, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
@@ -255,7 +306,11 @@ hipError_t factor_node(double* A, double* Linv, int o, int n, int mp, int nbatch
 
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
                                 hipStream_t st) {
-    hipError_t e = launch_zero_upper(Linv, mp, nbatch, bstride, st);
+    // The trimmed K ranges read Linv only in the lower triangle and in the
+    // first superdiagonal of 64 x 64 tiles (upper halves of 128-wide diagonal
+    // blocks at 64-aligned origins); the leaves write zeros above their own
+    // diagonals, so only that superdiagonal needs clearing.
+    hipError_t e = launch_zero_superdiag(Linv, mp, nbatch, bstride, st);
     if (e != hipSuccess) return e;
     return factor_node(A, Linv, 0, mp, mp, nbatch, bstride, err, st);
 }

@@ -15,13 +15,12 @@
 // in 128 x 128 tiles, written straight into the block's padded fp64 matrix
 // with m*lambda added on the diagonal, because the keep-mask is decided in fp64.
 #include "internal.h"
+#include "tile_util.h"
 
 namespace mfac {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
-typedef double v4d __attribute__((ext_vector_type(4)));
-
 constexpr int KB = 32;     // columns per LDS stage
 constexpr int PITCH = 36;  // LDS row pitch (floats)
 
@@ -155,11 +154,6 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
 // of a block share an L2); the block's columns stream through double-buffered
 // LDS in 32-column chunks, the next chunk's loads in flight during the MFMAs.
 constexpr int GT = 128;
-
-__device__ __forceinline__ int xcd_remap(int p, int n) {
-    if (n % 8) return p;
-    return (p % 8) * (n / 8) + p / 8;
-}
 
 __global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d, int B, int b0,
                                                      int ntiles, double mu, double* __restrict__ A, int mp) {

@@ -68,7 +68,9 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
 hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k, double mu,
                            double* A, int mp, int* err, hipStream_t st);
 // Cholesky factor and inverse of nbatch SPD matrices (mp x mp, mp a multiple
-// of 64, batch stride bstride): Linv <- L^-1 (lower, zeros above), A is
+// of 64, batch stride bstride): the lower triangle of Linv <- L^-1 (the
+// diagonal 64 x 64 tiles carry zeros above their diagonals; the strictly
+// upper tiles are left unspecified: readers use the lower triangle only). A is
 // consumed (its contents afterwards are scratch). err |= 2 on a non-positive
 // pivot. Recursive blocked algorithm on batched fp64 MFMA GEMMs.
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,

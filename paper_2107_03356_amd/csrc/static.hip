@@ -17,19 +17,10 @@
 // the IEEE bit pattern, which orders non-negative doubles), then a mask pass
 // that ranks exact ties by index with a deterministic chunked scan.
 #include "internal.h"
+#include "tile_util.h"
 
 namespace mfac {
 namespace {
-
-typedef double v4d __attribute__((ext_vector_type(4)));
-
-// Work-groups are dispatched round-robin over the 8 XCDs (each with its own
-// L2). Remap so that consecutive logical indices share an XCD: the column
-// slices of one block then run on one XCD and share its L2 copy of L_b^-1.
-__device__ __forceinline__ int xcd_remap(int p, int n) {
-    if (n % 8) return p;
-    return (p % 8) * (n / 8) + p / 8;
-}
 
 constexpr int TM = 64, TN = 128, TK = 32;  // W tile rows x columns, k-chunk
 constexpr int PA = TK + 2;                 // LDS pitch of the L^-1 chunk (doubles)

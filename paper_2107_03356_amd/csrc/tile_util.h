@@ -1,0 +1,26 @@
+// Device helpers shared by the fp64 MFMA tile kernels (gram.hip, factor.hip,
+// static.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace mfac {
+namespace {
+
+typedef double v4d __attribute__((ext_vector_type(4)));
+
+// Work-groups are dispatched round-robin over the 8 XCDs (each with its own
+// L2). Remap so that consecutive logical indices share an XCD: the tiles of
+// one matrix then run on one XCD and share its L2 copy of the operands.
+__device__ __forceinline__ int xcd_remap(int p, int n) {
+    if (n % 8) return p;
+    return (p % 8) * (n / 8) + p / 8;
+}
+
+// v where ok, else zeros; element-wise so the value stays in registers.
+__device__ __forceinline__ float4 keep4(bool ok, float4 v) {
+    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+}
+
+}  // namespace
+}  // namespace mfac
