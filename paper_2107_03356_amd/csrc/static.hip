@@ -7,10 +7,10 @@
 // extraction). k_trmm_diag forms W_b = Linv_b G_b tile by tile on fp64 MFMA,
 // writes it over G in fp32 and accumulates the column sums of squares from the
 // unrounded fp64 tiles. A work-group owns one 128-column slice of one block and
-// walks the 64-row tiles from the bottom up, so every tile of G it still needs
-// is untouched when it overwrites a finished one. Each tile's k-loop runs in
-// 32-deep chunks through double-buffered LDS, the next chunk's global loads in
-// flight during the current chunk's MFMAs.
+// walks the 128-row tiles from the bottom up, so every tile of G it still
+// needs is untouched when it overwrites a finished one. Each tile's k-loop runs
+// in 16-deep chunks through double-buffered LDS, the next chunk's global loads
+// in flight during the current chunk's MFMAs.
 //
 // Keep-mask (Section 4.1, OBD saliency, global over all blocks): fp64 scores,
 // then an 8-pass radix selection of the keep-th largest key (8-bit digits of
@@ -22,16 +22,25 @@
 namespace mfac {
 namespace {
 
-constexpr int TM = 64, TN = 128, TK = 32;  // W tile rows x columns, k-chunk
-constexpr int PA = TK + 2;                 // LDS pitch of the L^-1 chunk (doubles)
-constexpr int PB = TN + 16;                // LDS pitch of the G chunk (floats)
+constexpr int TM = 128, TN = 128, TK = 16;  // W tile rows x columns, k-chunk
+constexpr int PA = TK + 2;                  // LDS pitch of the L^-1 chunk, [row][k] (doubles)
+constexpr int PB = TN + 16;                 // LDS pitch of the G chunk, [k][col] (doubles)
 
-// grid: nslice * nb work-groups (flattened, remapped); slice = TN columns of a block.
-__global__ __launch_bounds__(256) void k_trmm_diag(const double* __restrict__ Linv, int mp, int64_t bstride,
-                                                   float* __restrict__ G, int m, int64_t d, int B, int b0,
-                                                   int nslice, double inv_lam, double* __restrict__ diag) {
+// grid: nslice * nb work-groups (flattened, remapped); slice = TN columns of a
+// block. Each work-group walks the 128-row tiles of its slice from the bottom
+// up; tile r needs L^-1 columns [0, (r+1)*128) and the same rows of G, so G
+// rows that tile r overwrites are never read again. Two work-groups per CU.
+//
+// Operand values that are never used load clamped, in-bounds addresses:
+// L^-1 rows past mp, G rows past m (their L^-1 coefficients are the exact
+// zeros above the diagonal; the K range stays inside the diagonal 128-block,
+// whose upper part is zero) and columns past the slice. W rows past m (zero
+// padding or clamped rows) are neither stored nor summed.
+__global__ __launch_bounds__(256, 2) void k_trmm_diag(const double* __restrict__ Linv, int mp, int64_t bstride,
+                                                      float* __restrict__ G, int m, int64_t d, int B, int b0,
+                                                      int nslice, double inv_lam, double* __restrict__ diag) {
     __shared__ double As[2][TM][PA];
-    __shared__ float Bs[2][TK][PB];
+    __shared__ double Bs[2][TK][PB];
     __shared__ double red[2][TN];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     const int bl = lid / nslice, sl = lid - (lid / nslice) * nslice;
@@ -41,28 +50,25 @@ __global__ __launch_bounds__(256) void k_trmm_diag(const double* __restrict__ Li
     const int b = b0 + bl;
     const int c0 = sl * TN;
     const int ncol = (B - c0) < TN ? (B - c0) : TN;
-    const double* Lb = Linv + (int64_t)bl * bstride;
-    float* Gb = G + (int64_t)b * B + c0;
-    const int T = mp / TM;
+    const double* __restrict__ Lb = Linv + (int64_t)bl * bstride;
+    float* __restrict__ Gb = G + (int64_t)b * B + c0;
+    const int T = (mp + TM - 1) / TM;
 
-    // global -> register staging of one k-chunk: L^-1 rows [r0, r0+64) x cols
-    // [k0, k0+32) (8 doubles per thread) and G rows [k0, k0+32) x 128 columns
-    // (16 floats per thread)
-    const int ar = tid >> 2, ac = (tid & 3) * 8;
-    const int br = tid >> 3, bc = (tid & 7) * 16;
+    // staging of one k-chunk: L^-1 rows [r0, r0+128) x cols [k0, k0+16), 8
+    // doubles per thread (row tid/2, cols (tid%2)*8..+7); G rows [k0, k0+16) x
+    // 128 columns, 8 floats per thread (row tid/16, cols (tid%16)*8..+7)
+    const int ar = tid >> 1, ac = (tid & 1) * 8;
+    const int br = tid >> 4, bc = (tid & 15) * 8;
+    const int bc0 = min(bc, ncol - 4), bc1 = min(bc + 4, ncol - 4);
     double2 ra[4];
-    float4 rb[4];
+    float4 rb[2];
     auto load_chunk = [&](int r0, int k0) {
-        const double* src = Lb + (int64_t)(r0 + ar) * mp + k0 + ac;
+        const double* src = Lb + (int64_t)min(r0 + ar, mp - 1) * mp + k0 + ac;
 #pragma unroll
         for (int q = 0; q < 4; ++q) ra[q] = *reinterpret_cast<const double2*>(src + 2 * q);
-        const int grow = k0 + br;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int col = bc + 4 * q;
-            rb[q] = (grow < m && col < ncol) ? *reinterpret_cast<const float4*>(Gb + (int64_t)grow * d + col)
-                                             : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        const float* gsrc = Gb + (int64_t)min(k0 + br, m - 1) * d;
+        rb[0] = *reinterpret_cast<const float4*>(gsrc + bc0);
+        rb[1] = *reinterpret_cast<const float4*>(gsrc + bc1);
     };
     auto store_chunk = [&](int buf) {
 #pragma unroll
@@ -70,18 +76,26 @@ __global__ __launch_bounds__(256) void k_trmm_diag(const double* __restrict__ Li
             As[buf][ar][ac + 2 * q] = ra[q].x;
             As[buf][ar][ac + 2 * q + 1] = ra[q].y;
         }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&Bs[buf][br][bc + 4 * q]) = rb[q];
+        double* bd = &Bs[buf][br][bc];
+        bd[0] = rb[0].x;
+        bd[1] = rb[0].y;
+        bd[2] = rb[0].z;
+        bd[3] = rb[0].w;
+        bd[4] = rb[1].x;
+        bd[5] = rb[1].y;
+        bd[6] = rb[1].z;
+        bd[7] = rb[1].w;
     };
 
     double sq[4] = {0.0, 0.0, 0.0, 0.0};
     for (int r = T - 1; r >= 0; --r) {
-        v4d acc[2][4];
+        v4d acc[4][4];
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
+        for (int x = 0; x < 4; ++x)
 #pragma unroll
             for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
-        const int nchunk = (r + 1) * (TM / TK);
+        const int khi = min((r + 1) * TM, mp);
+        const int nchunk = khi / TK;
         load_chunk(r * TM, 0);
         store_chunk(0);
         __syncthreads();
@@ -90,13 +104,13 @@ __global__ __launch_bounds__(256) void k_trmm_diag(const double* __restrict__ Li
             if (c + 1 < nchunk) load_chunk(r * TM, (c + 1) * TK);
 #pragma unroll
             for (int kk = 0; kk < TK / 4; ++kk) {
-                double av[2], bv[4];
+                double av[4], bv[4];
 #pragma unroll
-                for (int x = 0; x < 2; ++x) av[x] = As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
+                for (int x = 0; x < 4; ++x) av[x] = As[buf][wr * 64 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                for (int y = 0; y < 4; ++y) bv[y] = (double)Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
+                for (int y = 0; y < 4; ++y) bv[y] = Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
 #pragma unroll
-                for (int x = 0; x < 2; ++x)
+                for (int x = 0; x < 4; ++x)
 #pragma unroll
                     for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
@@ -106,18 +120,19 @@ __global__ __launch_bounds__(256) void k_trmm_diag(const double* __restrict__ Li
         }
         // W tile r: write over G (fp32) and accumulate squares from the fp64 values
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
+        for (int x = 0; x < 4; ++x)
 #pragma unroll
             for (int y = 0; y < 4; ++y)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int row = r * TM + wr * 32 + x * 16 + kl + 4 * q;  // fp64 MFMA: row (l/16) + 4q
+                    const int row = r * TM + wr * 64 + x * 16 + kl + 4 * q;  // fp64 MFMA: row (l/16) + 4q
                     const int col = wc * 64 + y * 16 + rl;
                     const double w = acc[x][y][q];
-                    sq[y] += w * w;
-                    if (row < m && col < ncol) Gb[(int64_t)row * d + col] = (float)w;
+                    if (row < m) {
+                        sq[y] += w * w;
+                        if (col < ncol) Gb[(int64_t)row * d + col] = (float)w;
+                    }
                 }
-        __syncthreads();
     }
     // column sums of squares: over kl (lanes +16, +32), then over wr
 #pragma unroll
