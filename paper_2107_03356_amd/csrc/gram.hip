@@ -2,10 +2,10 @@
 // "evaluating G G^T in a straightforward fashion", O(d m^2); Section 3.1
 // block-wise precompute, one m x m Gram per block).
 //
-// Tiling: one work-group (4 waves) per 64 x 64 lower-triangular output tile;
-// each wave owns a 32 x 32 quadrant as 2 x 2 MFMA 16x16x4 tiles. Operands are
-// staged through LDS in 64 x 32 fp32 panels (row pitch 36 floats: the 16-row x
-// 4-k read pattern of one MFMA operand then hits every bank at most twice).
+// Tiling: one work-group (8 waves) per 128 x 128 lower-triangular output tile;
+// each wave owns a 32 x 64 piece as 2 x 4 MFMA 16x16x4 tiles. Operands are
+// staged through double-buffered LDS in 128 x 32 fp32 panels (row pitch 36
+// floats: the 16-row x 4-k read pattern of one MFMA operand is conflict-free).
 //
 // Window Gram: fp32 MFMA (v_mfma_f32_16x16x4f32). The column range of the
 // window is split over work-groups; each work-group flushes its fp32 MFMA
@@ -32,118 +32,134 @@ __device__ __forceinline__ void tile_of(int idx, int& ti, int& tj) {
     tj = idx - t * (t + 1) / 2;
 }
 
-// Stage rows [r0, r0+64) x columns [k0, k0+KB) of a segment into LDS.
-__device__ __forceinline__ void stage(float (*S)[PITCH], const float* __restrict__ base, int64_t ld,
-                                      int r0, int m, int k0, int w) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int q = threadIdx.x + 256 * h;
-        const int row = q >> 3;
-        const int c4 = (q & 7) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (r0 + row < m && k0 + c4 < w)
-            v = *reinterpret_cast<const float4*>(base + (int64_t)(r0 + row) * ld + k0 + c4);
-        *reinterpret_cast<float4*>(&S[row][c4]) = v;
-    }
-}
+// Window Gram partials. Grid (ntiles, nsplit): work-group (t, s) computes the
+// 128 x 128 lower tile t of K over slabs [s*sps, min(nslab, (s+1)*sps)). Eight
+// waves, each owning a 32 x 64 piece as 2 x 4 fp32 MFMA tiles (two waves per
+// SIMD hide each other's LDS and memory waits); the fp32 accumulators are
+// added into fp64 registers after every slab (2048 columns). The slab's rows
+// stream through double-buffered LDS in 32-column chunks (128 x 32 fp32 per
+// operand), the next chunk's global loads in flight during the MFMAs. Rows
+// past m load clamped, in-bounds data; only rows and columns below m of the
+// partial are ever summed into K.
+constexpr int WT = 128;  // window Gram tile
 
-// One KB-column stage of MFMA work for this wave's 2x2 sub-tiles.
-template <typename Acc, bool F64>
-__device__ __forceinline__ void mfma_stage(float (*As)[PITCH], float (*Bs)[PITCH], int wr, int wc,
-                                           int lane, Acc (&acc)[2][2]) {
-    const int rl = lane & 15;
-    const int kl = lane >> 4;
-#pragma unroll
-    for (int kk = 0; kk < KB / 4; ++kk) {
-        float a[2], b[2];
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            a[s] = As[wr * 32 + s * 16 + rl][kk * 4 + kl];
-            b[s] = Bs[wc * 32 + s * 16 + rl][kk * 4 + kl];
-        }
-#pragma unroll
-        for (int x = 0; x < 2; ++x)
-#pragma unroll
-            for (int y = 0; y < 2; ++y) {
-                if constexpr (F64)
-                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a[x], (double)b[y], acc[x][y], 0, 0, 0);
-                else
-                    acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[x], b[y], acc[x][y], 0, 0, 0);
-            }
-    }
-}
-
-// Window Gram partials: grid (ntiles, nsplit); split s sums slabs [s*sps, min(nslab, (s+1)*sps)).
-__global__ __launch_bounds__(256) void k_gram_window(const float* __restrict__ G, int m, int64_t nslab,
+__global__ __launch_bounds__(512) void k_gram_window(const float* __restrict__ G, int m, int64_t nslab,
                                                      int64_t sps, double* __restrict__ part, int ntiles) {
-    __shared__ float As[64][PITCH];
-    __shared__ float Bs[64][PITCH];
+    __shared__ float As[2][WT][PITCH];
+    __shared__ float Bs[2][WT][PITCH];
     int ti, tj;
     tile_of(blockIdx.x, ti, tj);
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
+    const int rl = lane & 15, kl = lane >> 4;
     const int64_t s0 = (int64_t)blockIdx.y * sps;
-    int64_t s1 = s0 + sps;
-    if (s1 > nslab) s1 = nslab;
+    const int64_t s1 = min(s0 + sps, nslab);
 
-    v4d accd[2][2];
+    // staging: 128 rows x 32 columns per operand, 8 floats per thread and operand
+    const int sr = tid >> 2, sc = (tid & 3) * 8;
+    const int64_t offa = (int64_t)min(ti * WT + sr, m - 1) * SLAB + sc;
+    const int64_t offb = (int64_t)min(tj * WT + sr, m - 1) * SLAB + sc;
+    // staged chunk: two float4 per operand, kept in named registers
+    float4 pa0, pa1, pb0, pb1;
+#define MFAC_GW_LOAD(S_, K0_)                                            \
+    {                                                                    \
+        const float* base_ = G + (S_) * (int64_t)m * SLAB + (K0_);       \
+        const float4* a_ = reinterpret_cast<const float4*>(base_ + offa); \
+        const float4* b_ = reinterpret_cast<const float4*>(base_ + offb); \
+        pa0 = a_[0];                                                     \
+        pa1 = a_[1];                                                     \
+        pb0 = b_[0];                                                     \
+        pb1 = b_[1];                                                     \
+    }
+#define MFAC_GW_STORE(BUF_)                                              \
+    {                                                                    \
+        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);       \
+        float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);       \
+        a_[0] = pa0;                                                     \
+        a_[1] = pa1;                                                     \
+        b_[0] = pb0;                                                     \
+        b_[1] = pb1;                                                     \
+    }
+
+    v4d accd[2][4];
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) accd[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
-
+        for (int y = 0; y < 4; ++y) accd[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
+    constexpr int NCH = SLAB / KB;  // chunks per slab
+    if (s0 < s1) {
+        MFAC_GW_LOAD(s0, 0)
+        MFAC_GW_STORE(0)
+        __syncthreads();
+    }
+    int buf = 0;
     for (int64_t s = s0; s < s1; ++s) {
-        const float* base = G + s * (int64_t)m * SLAB;
-        v4f acc[2][2];
+        v4f acc[2][4];
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
-            for (int y = 0; y < 2; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
-        for (int k0 = 0; k0 < SLAB; k0 += KB) {
-            stage(As, base, SLAB, ti * 64, m, k0, SLAB);
-            if (ti != tj) stage(Bs, base, SLAB, tj * 64, m, k0, SLAB);
+            for (int y = 0; y < 4; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < NCH; ++c) {
+            // next chunk: the following columns of this slab, or the next slab's first
+            const bool more = c + 1 < NCH || s + 1 < s1;
+            const int64_t sn = c + 1 < NCH ? s : s + 1;
+            const int kn = c + 1 < NCH ? (c + 1) * KB : 0;
+            if (more) MFAC_GW_LOAD(sn, kn)
+            float (*Ab)[PITCH] = As[buf];
+            float (*Bb)[PITCH] = Bs[buf];
+#pragma unroll
+            for (int kk = 0; kk < KB / 4; ++kk) {
+                float av[2], bv[4];
+#pragma unroll
+                for (int x = 0; x < 2; ++x) av[x] = Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
+#pragma unroll
+                for (int y = 0; y < 4; ++y) bv[y] = Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < 4; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+            }
+            if (more) MFAC_GW_STORE(buf ^ 1)
             __syncthreads();
-            if (ti != tj)
-                mfma_stage<v4f, false>(As, Bs, wr, wc, lane, acc);
-            else
-                mfma_stage<v4f, false>(As, As, wr, wc, lane, acc);
-            __syncthreads();
+            buf ^= 1;
         }
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
-            for (int y = 0; y < 2; ++y)
+            for (int y = 0; y < 4; ++y)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) accd[x][y][r] += (double)acc[x][y][r];
     }
 
-    double* out = part + ((int64_t)blockIdx.y * ntiles + blockIdx.x) * (64 * 64);
-    const int rl = lane & 15, kl = lane >> 4;
+    double* out = part + ((int64_t)blockIdx.y * ntiles + blockIdx.x) * (WT * WT);
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y)
+        for (int y = 0; y < 4; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 // fp32 MFMA result: lane l register r is row 4(l/16) + r
                 const int row = wr * 32 + x * 16 + kl * 4 + r;
-                const int col = wc * 32 + y * 16 + rl;
-                out[row * 64 + col] = accd[x][y][r];
+                const int col = wc * 64 + y * 16 + rl;
+                out[row * WT + col] = accd[x][y][r];
             }
 }
 
-// K[row][col] (both triangles) = sum over splits of the tile partials.
+#undef MFAC_GW_LOAD
+#undef MFAC_GW_STORE
+
+// K[row][col] (both triangles) = sum over splits of the tile partials, in split order.
 __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ part, int nsplit,
                                                      int ntiles, int m, double* __restrict__ K) {
     int ti, tj;
     tile_of(blockIdx.x, ti, tj);
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-        const int rr = e >> 6, cc = e & 63;
-        const int row = ti * 64 + rr, col = tj * 64 + cc;
+    for (int e = threadIdx.x; e < WT * WT; e += 256) {
+        const int rr = e / WT, cc = e % WT;
+        const int row = ti * WT + rr, col = tj * WT + cc;
         if (row >= m || col >= m) continue;
         double s = 0.0;
-        for (int k = 0; k < nsplit; ++k) s += part[((int64_t)k * ntiles + blockIdx.x) * 4096 + e];
+        for (int k = 0; k < nsplit; ++k) s += part[((int64_t)k * ntiles + blockIdx.x) * (WT * WT) + e];
         K[(int64_t)row * m + col] = s;
         K[(int64_t)col * m + row] = s;
     }
@@ -242,25 +258,31 @@ __global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G
 
 }  // namespace
 
-int64_t gram_window_part_doubles(int m, int64_t nslab) {
-    const int T = (int)ceil_div(m, 64);
-    const int ntiles = T * (T + 1) / 2;
-    int64_t nsplit = ceil_div(2048, ntiles);
-    if (nsplit > nslab) nsplit = nslab;
-    if (nsplit < 1) nsplit = 1;
-    return nsplit * ntiles * 4096;
-}
-
-hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part, double* K,
-                              hipStream_t st) {
-    const int T = (int)ceil_div(m, 64);
-    const int ntiles = T * (T + 1) / 2;
+namespace {
+// splits of the slab range: enough work-groups for ~8 per CU
+int64_t gram_window_splits(int m, int64_t nslab, int& ntiles) {
+    const int T = (int)ceil_div(m, WT);
+    ntiles = T * (T + 1) / 2;
     int64_t nsplit = ceil_div(2048, ntiles);
     if (nsplit > nslab) nsplit = nslab;
     if (nsplit < 1) nsplit = 1;
     const int64_t sps = ceil_div(nslab, nsplit);
-    nsplit = ceil_div(nslab, sps);
-    hipLaunchKernelGGL(k_gram_window, dim3(ntiles, (unsigned)nsplit), dim3(256), 0, st, G, m, nslab,
+    return ceil_div(nslab, sps);
+}
+}  // namespace
+
+int64_t gram_window_part_doubles(int m, int64_t nslab) {
+    int ntiles;
+    const int64_t nsplit = gram_window_splits(m, nslab, ntiles);
+    return nsplit * ntiles * (int64_t)(WT * WT);
+}
+
+hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part, double* K,
+                              hipStream_t st) {
+    int ntiles;
+    const int64_t nsplit = gram_window_splits(m, nslab, ntiles);
+    const int64_t sps = ceil_div(nslab, nsplit);
+    hipLaunchKernelGGL(k_gram_window, dim3(ntiles, (unsigned)nsplit), dim3(512), 0, st, G, m, nslab,
                        sps, part, ntiles);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
