@@ -4,17 +4,19 @@
 // K/lambda + m I minus m I (Appendix B); equivalently D and B come from the
 // Cholesky factor R of A = K + m*lambda*I: A = lambda * Ru Ru^T with
 // D = diag(Ru) Ru^T - m I and B = lambda^-1 (Ru diag(Ru)^-1)^-1. The
-// coefficients of Theorem 1 are then c = lambda^-1 A^-1 G x. This file keeps
-// that factor explicitly: a blocked right-looking Cholesky of A in NB = 64
-// tiles (the paper's remark that a modified Cholesky kernel would beat its
-// LU), the inverses of the diagonal tiles, optionally the full L^-1, and
-// blocked triangular solves. A is padded to a multiple of 64 with an
+// coefficients of Theorem 1 are then c = lambda^-1 A^-1 G x. The library
+// keeps the explicit inverse A^-1 (the paper's remark that a modified
+// Cholesky kernel would beat its LU): factor.hip computes L and L^-1 with a
+// recursive blocked algorithm whose 64 x 64 leaves this file factors and
+// inverts in registers (k_potrf_diag); k_lauum forms A^-1 = L^-T L^-1; the
+// O(m^2) slot replacement updates A^-1 in place between refactors; and the
+// coefficient kernel applies it. A is padded to a multiple of 64 with an
 // identity block so no kernel needs edge handling.
 //
-// Dense 64 x 64 x 64 tile products run on fp64 MFMA (v_mfma_f64_16x16x4f64):
-// 4 waves, each a 32 x 32 quadrant of 2 x 2 16x16 tiles, operands from LDS.
-// All products are written as C[r][c] = sum_k a[r][k] * b[c][k]; a tile that
-// enters as b[k][c] is transposed while it is staged.
+// Dense 64 x 64 x 64 tile products (k_lauum) run on fp64 MFMA
+// (v_mfma_f64_16x16x4f64): 4 waves, each a 32 x 32 quadrant of 2 x 2 16x16
+// tiles, operands from LDS. They are written as C[r][c] = sum_k a[r][k] *
+// b[c][k]; a tile that enters as b[k][c] is transposed while it is staged.
 #include "internal.h"
 
 namespace mfac {
@@ -22,17 +24,6 @@ namespace {
 
 typedef double v4d __attribute__((ext_vector_type(4)));
 constexpr int P = 68;  // LDS pitch of a 64 x 64 fp64 tile
-
-__device__ __forceinline__ void stage_tile(double (*S)[P], const double* __restrict__ src, int64_t ld) {
-    for (int e = threadIdx.x; e < 64 * 16; e += blockDim.x) {
-        const int r = e >> 4, c = (e & 15) * 4;
-        const double* s = src + (int64_t)r * ld + c;
-        S[r][c] = s[0];
-        S[r][c + 1] = s[1];
-        S[r][c + 2] = s[2];
-        S[r][c + 3] = s[3];
-    }
-}
 
 __device__ __forceinline__ void stage_tile_t(double (*S)[P], const double* __restrict__ src, int64_t ld) {
     for (int e = threadIdx.x; e < 64 * 64; e += blockDim.x) {
