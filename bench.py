@@ -197,7 +197,8 @@ def bench_static(args, wl, dev):
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep},
-        "roofline": {"bound": "mfma", "achieved": flops / (ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
+        "roofline": {"bound": "mfma", "kernel": "whole run (Gram, factor, W and diagonal, mask)",
+                     "achieved": flops / (ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
                      "frac": flops / (ms * 1e-3) / 1e12 / 78.6, "traffic": None},
         "queries": queries,
     }
