@@ -373,6 +373,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-div", type=int, default=64)
     ap.add_argument("--cpu-steps", type=int, default=3)
+    ap.add_argument("--refactor-period", type=int, default=None,
+                    help="coefficient policy: full refactor every N replaces (0 = every replace); default: the library's")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -407,6 +409,8 @@ def main():
         win.set_rows(r0, gs.rows(r0, n))
         log(f"window rows {r0 + n}/{m}")
     win.rebuild()
+    if args.refactor_period is not None:
+        win.set_refactor_period(args.refactor_period)
     log("Gram + factor done")
     nsteps = args.warmup + args.steps
     steps_g = torch.empty((nsteps, d), dtype=torch.float32, device=dev)
@@ -490,6 +494,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": wl.name, "d": d, "m": m, "lambda": wl.lam, "queries": nq,
+            "refactor_period": args.refactor_period,
             "corr_frac": wl.corr_frac,
             "step": "replace oldest row + Gram row + O(m^2) update of the fp64 inverse of G G^T + m lambda I (full refactor every R replaces) + IHVP of the new gradient",
             "parallelism": "single GPU",
