@@ -11,9 +11,10 @@
 // that write with pass 1's reads cost ~8% of pass 1's bandwidth on gfx950.
 //
 // Pass 1: every work-group owns a set of column chunks and keeps per-row
-// running sums in LDS. For each row a wave loads U float4 per lane (128-bit
-// coalesced loads), multiplies with the register-resident vector chunks and
-// reduces across the wave with lane shuffles. Work-group partials go to a
+// running sums in LDS. A wave takes R rows at a time, loads U float4 per lane
+// and row (128-bit coalesced loads), multiplies with the register-resident
+// vector chunks and reduces the R x NV sums across the wave with lane
+// shuffles. Work-group partials go to a
 // [grid][m*nv] fp64 buffer, summed in a fixed order by the reduce kernel
 // (deterministic, no float atomics).
 //
@@ -58,7 +59,7 @@ __global__ __launch_bounds__(256) void k_get_rows(const float* __restrict__ G, i
     st4(rows + (int64_t)r * ld, j, d, aligned, v);
 }
 
-template <int NV, int U>
+template <int NV, int U, int R>
 __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int m, int64_t d,
                                                int64_t nchunk, VecIn vin, int aligned,
                                                double* __restrict__ part) {
@@ -66,6 +67,7 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
     constexpr int CW = 256 * U;     // chunk width (floats): 64 lanes x float4 x U
     constexpr int CPS = SLAB / CW;  // chunks per slab
     static_assert(SLAB % CW == 0, "chunk must tile the slab");
+    static_assert(R * NV <= 64, "one wave reduces at most 64 sums at a time");
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int mnv = m * NV;
@@ -84,40 +86,37 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
 #pragma unroll
             for (int u = 0; u < U; ++u) vr[v][u] = ld4(vin.v[v], j0 + u * 256 + lane * 4, d, aligned);
 
-        // two rows per iteration: rows i and i + 4 of this wave; a missing
-        // second row re-reads row i and its sum is dropped (no branch around loads)
-        for (int i = wave; i < m; i += 8) {
-            const bool has2 = i + 4 < m;
-            const int i2 = has2 ? i + 4 : i;
-            float4 ga[U], gb[U];
+        // R rows per iteration: rows i, i + 4, ..., i + 4(R-1) of this wave; a
+        // missing row re-reads row i and its sums are dropped (no branch around loads)
+        for (int i = wave; i < m; i += 4 * R) {
+            int row[R];
 #pragma unroll
-            for (int u = 0; u < U; ++u) ga[u] = ld_stream(Gs + (int64_t)i * SLAB + u * 256);
+            for (int r = 0; r < R; ++r) row[r] = i + 4 * r < m ? i + 4 * r : i;
+            float4 g[R][U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) gb[u] = ld_stream(Gs + (int64_t)i2 * SLAB + u * 256);
-            // keep all 2U loads in flight before the first use (the scheduler
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < U; ++u) g[r][u] = ld_stream(Gs + (int64_t)row[r] * SLAB + u * 256);
+            // keep all R*U loads in flight before the first use (the scheduler
             // otherwise recycles a few load registers and waits on each load)
             __builtin_amdgcn_sched_barrier(0);
-            // per-lane partial dots: rows i (values 0..NV-1) and i2 (NV..2NV-1)
-            float sv[2 * NV];
+            // per-lane partial dots: value r*NV + v is row r's dot with vector v
+            float sv[R * NV];
 #pragma unroll
-            for (int v = 0; v < NV; ++v) {
-                float a = 0.f, b = 0.f;
+            for (int v = 0; v < NV; ++v)
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    a = dot4(ga[u], vr[v][u], a);
-                    b = dot4(gb[u], vr[v][u], b);
+                for (int r = 0; r < R; ++r) {
+                    float a = 0.f;
+#pragma unroll
+                    for (int u = 0; u < U; ++u) a = dot4(g[r][u], vr[v][u], a);
+                    sv[r * NV + v] = a;
                 }
-                sv[v] = a;
-                sv[NV + v] = b;
-            }
             int idx;
             bool writer;
-            const float tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
+            const float tot = wave_reduce_many<R * NV>(sv, lane, idx, writer);
             if (writer) {
-                if (idx < NV)
-                    acc[i * NV + idx] += tot;
-                else if (has2)
-                    acc[i2 * NV + (idx - NV)] += tot;
+                const int r = idx / NV, v = idx - (idx / NV) * NV;
+                if (i + 4 * r < m) acc[(i + 4 * r) * NV + v] += tot;
             }
         }
     }
@@ -243,17 +242,20 @@ struct PassCfg {
     // (<= ~72 VGPRs); pass 2 uses narrow 512-column wave chunks with 8 rows in
     // flight, which measured fastest on the 105 GB window.
     static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 9 ? 2 : 1;
+    // rows per pass-1 iteration: 4 where the register-resident vectors leave
+    // room, so 2U-wide rows keep 4R loads in flight per lane
+    static constexpr int R = (NV >= 3 && NV <= 16) ? 4 : 2;
     static constexpr int U2 = NV <= 2 ? 2 : 1;
 };
 
 template <int NV>
 hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn& vin, bool aligned,
                     double* part, int* grid_out, hipStream_t st) {
-    constexpr int U = PassCfg<NV>::U;
+    constexpr int U = PassCfg<NV>::U, R = PassCfg<NV>::R;
     const int64_t nchunk = nslab * (SLAB / (256 * U));
     const int grid = (int)(nchunk < PASS1_MAX_GRID ? nchunk : PASS1_MAX_GRID);
     const size_t lds = (size_t)m * NV * sizeof(float);
-    hipLaunchKernelGGL((k_pass1<NV, U>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
+    hipLaunchKernelGGL((k_pass1<NV, U, R>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
                        aligned ? 1 : 0, part);
     *grid_out = grid;
     return hipGetLastError();
