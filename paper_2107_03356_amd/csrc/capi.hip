@@ -1,7 +1,7 @@
 // C ABI of libmfac (include/mfac.h): host-side validation, workspace layout
 // and the launch sequences of the dynamic and static paths. Nothing here
 // computes on the host; every step of the method runs in the kernels of
-// pass.hip, gram.hip, chol.hip and static.hip.
+// pass.hip, gram.hip, chol.hip, factor.hip, static.hip and static_query.hip.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
