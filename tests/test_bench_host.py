@@ -1,0 +1,49 @@
+"""Host-side checks of bench.py: the one-GPU contract and the workload shapes
+its modes rely on (no GPU needed)."""
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_resnet20_has_the_workload_size():
+    sys.path.insert(0, ROOT)
+    import bench
+    from synth import get_workload
+    net = bench.resnet20()
+    assert sum(p.numel() for p in net.parameters()) == get_workload("optim_resnet20_cifar_b128_m512").d
+
+
+def test_pass_bytes_match_the_survey_budget():
+    """2 m d 4 + 3 d 4 bytes per step at the ResNet50-sized window (210.0 GB)."""
+    sys.path.insert(0, ROOT)
+    import bench
+    b1, b2, bw = bench.pass_bytes(25_600_000, 1024)
+    assert b1 + b2 + bw == 2 * 1024 * 25_600_000 * 4 + 4 * 25_600_000 * 4
+    assert abs((b1 + b2 + bw) / 1e9 - 210.0) < 0.5
+
+
+@pytest.mark.parametrize("kernel", ["k_pass1", "k_pass2"])
+def test_committed_counters_match_the_current_pass_sources(kernel):
+    """The committed HBM counter summary was taken on the current streaming
+    kernels (else bench.py reports traffic as null)."""
+    sys.path.insert(0, ROOT)
+    import bench
+    t = bench.read_counters(kernel)
+    if t is None:
+        pytest.skip("the committed HBM counters were taken on other pass sources: retake them")
+    b1, b2, _ = bench.pass_bytes(25_600_000, 1024)
+    alg = b1 if kernel == "k_pass1" else b2
+    assert abs(t / alg - 1.0) < 0.02
