@@ -52,6 +52,9 @@ __global__ __launch_bounds__(512) void k_gram_window(const float* __restrict__ G
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
     const int rl = lane & 15, kl = lane >> 4;
+    // in a diagonal tile, waves whose piece lies wholly above the diagonal only
+    // stage operands (the reduction reads the lower triangle of such tiles)
+    const bool upper_wave = ti == tj && wr * 32 + 31 < wc * 64;
     const int64_t s0 = (int64_t)blockIdx.y * sps;
     const int64_t s1 = min(s0 + sps, nslab);
 
@@ -107,18 +110,20 @@ __global__ __launch_bounds__(512) void k_gram_window(const float* __restrict__ G
             if (more) MFAC_GW_LOAD(sn, kn)
             float (*Ab)[PITCH] = As[buf];
             float (*Bb)[PITCH] = Bs[buf];
+            if (!upper_wave) {
 #pragma unroll
-            for (int kk = 0; kk < KB / 4; ++kk) {
-                float av[2], bv[4];
+                for (int kk = 0; kk < KB / 4; ++kk) {
+                    float av[2], bv[4];
 #pragma unroll
-                for (int x = 0; x < 2; ++x) av[x] = Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
+                    for (int x = 0; x < 2; ++x) av[x] = Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                for (int y = 0; y < 4; ++y) bv[y] = Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
+                    for (int y = 0; y < 4; ++y) bv[y] = Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                for (int x = 0; x < 2; ++x)
+                    for (int x = 0; x < 2; ++x)
 #pragma unroll
-                    for (int y = 0; y < 4; ++y)
-                        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+                        for (int y = 0; y < 4; ++y)
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+                }
             }
             if (more) MFAC_GW_STORE(buf ^ 1)
             __syncthreads();
@@ -132,6 +137,7 @@ __global__ __launch_bounds__(512) void k_gram_window(const float* __restrict__ G
                 for (int r = 0; r < 4; ++r) accd[x][y][r] += (double)acc[x][y][r];
     }
 
+    if (upper_wave) return;
     double* out = part + ((int64_t)blockIdx.y * ntiles + blockIdx.x) * (WT * WT);
 #pragma unroll
     for (int x = 0; x < 2; ++x)
@@ -149,7 +155,8 @@ __global__ __launch_bounds__(512) void k_gram_window(const float* __restrict__ G
 #undef MFAC_GW_LOAD
 #undef MFAC_GW_STORE
 
-// K[row][col] (both triangles) = sum over splits of the tile partials, in split order.
+// K[row][col] (both triangles) = sum over splits of the tile partials, in split
+// order; a diagonal tile contributes its lower triangle (mirrored).
 __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ part, int nsplit,
                                                      int ntiles, int m, double* __restrict__ K) {
     int ti, tj;
@@ -157,7 +164,7 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
     for (int e = threadIdx.x; e < WT * WT; e += 256) {
         const int rr = e / WT, cc = e % WT;
         const int row = ti * WT + rr, col = tj * WT + cc;
-        if (row >= m || col >= m) continue;
+        if (row >= m || col >= m || (ti == tj && rr < cc)) continue;  // diagonal tiles: lower triangle
         double s = 0.0;
         for (int k = 0; k < nsplit; ++k) s += part[((int64_t)k * ntiles + blockIdx.x) * (WT * WT) + e];
         K[(int64_t)row * m + col] = s;
@@ -183,6 +190,9 @@ __global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G
     const int wr = wave >> 1, wc = wave & 1;
     const int rl = lane & 15, kl = lane >> 4;
     const bool diag_tile = ti == tj;
+    // in a diagonal tile the quadrant above the diagonal is never read (the
+    // factorization uses the lower triangle): its wave only stages operands
+    const bool upper_wave = diag_tile && wr < wc;
     const float* base = G + (int64_t)(b0 + bl) * B;
     const int ra0 = ti * GT, rb0 = tj * GT;
     // staging: 128 rows x 32 columns per operand, 16 floats per thread
@@ -222,22 +232,25 @@ __global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G
         if (c + 1 < nchunk) load_chunk((c + 1) * KB);
         float (*Ab)[PITCH] = As[buf];
         float (*Bb)[PITCH] = diag_tile ? As[buf] : Bs[buf];
+        if (!upper_wave) {
 #pragma unroll
-        for (int kk = 0; kk < KB / 4; ++kk) {
-            double av[4], bv[4];
+            for (int kk = 0; kk < KB / 4; ++kk) {
+                double av[4], bv[4];
 #pragma unroll
-            for (int x = 0; x < 4; ++x) av[x] = (double)Ab[wr * 64 + x * 16 + rl][kk * 4 + kl];
+                for (int x = 0; x < 4; ++x) av[x] = (double)Ab[wr * 64 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
-            for (int y = 0; y < 4; ++y) bv[y] = (double)Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
+                for (int y = 0; y < 4; ++y) bv[y] = (double)Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
 #pragma unroll
-            for (int x = 0; x < 4; ++x)
+                for (int x = 0; x < 4; ++x)
 #pragma unroll
-                for (int y = 0; y < 4; ++y)
-                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+                    for (int y = 0; y < 4; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+            }
         }
         if (c + 1 < nchunk) store_chunk(buf ^ 1);
         __syncthreads();
     }
+    if (upper_wave) return;
     double* Ab = A + (int64_t)bl * mp * mp;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
