@@ -82,6 +82,7 @@ def test_tiny_init_equals_fill(dev):
     (3 * 2048 + 777, 40, 1e-3, 3, "gauss"),        # ragged d (d % 4 != 0), m not a multiple of 64
     (20000, 200, 1e-4, 2, "lognormal"),            # several 64-wide leaves in the recursive factor
     (30000, 300, 1e-4, 2, "lognormal"),            # padded to 320: uneven splits and half tiles in the factor
+    (24000, 1500, 1e-4, 3, "lognormal"),           # m > 1024: padded to 1536, 12 Gram tiles, deeper recursion
     (40968, 1024, 1e-5, 8, "lognormal"),           # m = 1024 with 8 fused queries (ResNet18 recipe)
     (2048, 1, 1e-2, 1, "gauss"),                   # m = 1 (Sherman-Morrison)
     (5, 3, 1e-1, 1, "gauss"),                      # d smaller than one float4 group row

@@ -51,6 +51,7 @@ def _run(dev, G, B, lam, theta, keep):
     (200, 2048, 2, 1e-4, None),    # the pruning block width
     (300, 512, 3, 1e-4, None),     # padded to 320: uneven splits in the recursive factor
     (700, 2048, 2, 1e-4, None),    # padded to 704: 11 tiles, half tiles at several levels
+    (1500, 512, 3, 1e-4, None),    # m > B and m > 1024: rank-deficient Gram, padded to 1536
 ])
 def test_static_small(dev, m, B, nb, lam, batch_cap, monkeypatch):
     if batch_cap:
