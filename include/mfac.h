@@ -18,8 +18,11 @@
  *
  * Conventions for every call:
  *   - Pointers are HIP device pointers unless marked (host).
- *   - Vectors of length d are fp32, contiguous, 16-byte aligned; a batch of n
- *     vectors is n rows of length d with row stride d (row-major).
+ *   - Vectors of length d are fp32 and contiguous; a batch of n vectors is n
+ *     rows of length d with row stride d (row-major). The window calls accept
+ *     4-byte aligned vectors and take 128-bit accesses when every vector is
+ *     16-byte aligned (and d % 4 == 0 for batches); the static calls state
+ *     their own alignment below.
  *   - The library never allocates or frees device memory. Window storage,
  *     workspaces and outputs are owned by the caller and must outlive the
  *     handle (storage/workspace) or the call's stream work (inputs/outputs).
@@ -31,6 +34,9 @@
  *     non-positive pivot met on the device latches an error word in the
  *     workspace, reported as MFAC_ENONFINITE by the next *_status call.
  *   - A handle is used by one host thread and one stream at a time.
+ *   - Calls are not meant for stream capture into HIP graphs: the ring head,
+ *     the step count and the refactor counter advance on the host when a call
+ *     is made, so a replayed graph would repeat the captured slot and policy.
  */
 #ifndef MFAC_H
 #define MFAC_H
@@ -188,8 +194,9 @@ size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m);
  * also writes over G: V_i = sqrt(q_i / lambda) W_i). The inverse diagonal
  * diag(F_b^-1) = (1 - sum_i W_b[i,:]^2) / lambda is formed in fp64 from the
  * unrounded W and kept in the workspace.
- * Requirements: 1 <= m, 1 <= block, block % 4 == 0, d % block == 0,
- * lambda > 0 finite. */
+ * Requirements: 1 <= m <= 8192, 4 <= block, block % 4 == 0,
+ * d % block == 0, lambda > 0 finite, G 16-byte aligned, workspace 256-byte
+ * aligned. */
 mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m,
                                    double lambda, float* G, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
@@ -204,14 +211,16 @@ mfac_status mfac_inv_diag64(mfac_static s, double* diag_out);
 /* OBD saliency rho_j = theta_j^2 / (2 [F^-1]_jj) in fp64 (Section 4.1) and a
  * global keep-mask over all blocks: keep_mask[j] = 1 for the `keep` largest
  * rho, ties broken by the lower index; 0 <= keep <= d. scores_out may be
- * NULL. Uses workspace scratch; output is exact given the fp64 diagonal. */
+ * NULL. theta 4-byte aligned. Uses workspace scratch; output is exact given
+ * the fp64 diagonal. */
 mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t keep,
                           double* scores_out, uint8_t* keep_mask_out);
 
 /* Y = F^-1 X for the block-wise Fisher, n x d row-major fp32 X and Y,
  * 1 <= n <= 4 (Appendix C eq. 9; with W in place of V and q:
  * F_b^-1 x_b = (x_b - W_b^T (W_b x_b)) / lambda). Two passes over W (the
- * precompute's output in G's storage). X and Y must not alias G. */
+ * precompute's output in G's storage). X and Y 16-byte aligned and must not
+ * alias G. */
 mfac_status mfac_static_ihvp(mfac_static s, int32_t n, const float* X, float* Y);
 
 /* Element queries [F^-1]_ij, O(m) each (Section 3.1, eq. 5):
@@ -226,7 +235,8 @@ mfac_status mfac_static_element(mfac_static s, int64_t nq, const int64_t* ij, do
  * removed coordinates and 0 elsewhere, i.e. the sum of the single-weight OBS
  * updates -theta_j F^-1 e_j / [F^-1]_jj (the paper's approximate
  * multi-weight OBS). theta + delta zeroes a removed weight that is the only
- * removed one in its block. theta, delta_out: d fp32; keep_mask: d uint8. */
+ * removed one in its block. theta, delta_out: d fp32 (theta 4-byte,
+ * delta_out 16-byte aligned); keep_mask: d uint8. */
 mfac_status mfac_obs_update(mfac_static s, const float* theta, const uint8_t* keep_mask, float* delta_out);
 
 mfac_status mfac_static_set_stream(mfac_static s, hipStream_t stream);
