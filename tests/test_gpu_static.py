@@ -167,3 +167,24 @@ def test_obs_single_weight_and_bad_element_index(dev):
     assert np.isnan(out[0])
     assert sb.status() == MFAC_ENONFINITE
     assert sb.status() == 0
+
+
+def test_nonfinite_gradient_latches_and_other_blocks_stay_exact(dev):
+    """A NaN in one block of G latches MFAC_ENONFINITE (its pivots are not
+    positive); blocks are independent, so the other blocks' diagonals still
+    match the oracle."""
+    from paper_2107_03356_amd import MFAC_ENONFINITE, StaticBlocks
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=3 * 256, m=40, block=256, lam=1e-3, scale_d=256)
+    gs = GradientStream(wl, seed=41)
+    G = gs.rows(0, wl.m)
+    Gbad = G.clone()
+    Gbad[7, 256 + 13] = float("nan")
+    say("static nonfinite")
+    sb = StaticBlocks(Gbad.to(dev).contiguous(), wl.block, wl.lam)
+    d64 = sb.inv_diag(fp64=True).cpu().numpy()
+    assert sb.status() == MFAC_ENONFINITE
+    assert sb.status() == 0                      # the latch clears once reported
+    dref = ostatic.inv_diag(G.numpy(), wl.lam, wl.block, blocks=[0, 2])
+    got = np.concatenate([d64[:256], d64[512:]])
+    assert rel_l2(got, dref) < 1e-11
