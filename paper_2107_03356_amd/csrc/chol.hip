@@ -114,6 +114,7 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
                                                    int mp, int64_t bstride, int t, int* __restrict__ err) {
     __shared__ double col[2][64];
     __shared__ double T[64][65];
+    __shared__ double rdiag[64];  // 1 / L[j][j]
     double* Ab = A + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
     double* Lb = Linv + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
     const int i = threadIdx.x;
@@ -124,18 +125,22 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
         double* cb = col[j & 1];
+        // the pivot lane publishes 1 / L[j][j] = rsqrt(pivot); the column below
+        // it scales by that reciprocal (no division on the per-column chain)
         if (i == j) {
             double piv = a[j];
             if (!(piv > 0.0) || !isfinite(piv)) {
                 bad = 1;
                 piv = 1.0;
             }
-            a[j] = sqrt(piv);
-            cb[j] = a[j];
+            const double r = rsqrt(piv);
+            a[j] = piv * r;
+            cb[j] = r;
+            rdiag[j] = r;
         }
         __syncthreads();
         if (i > j) {
-            a[j] = a[j] / cb[j];
+            a[j] = a[j] * cb[j];
             cb[i] = a[j];
         }
         __syncthreads();
@@ -155,7 +160,8 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
     }
     __syncthreads();
     // Column i of the inverse of the lower factor by forward substitution,
-    // kept in registers: x_r = (delta_ri - sum_{l<r} T[r][l] x_l) / T[r][r].
+    // kept in registers: x_r = (delta_ri - sum_{l<r} T[r][l] x_l) / T[r][r]
+    // (as a product with the stored reciprocal).
     // Rows above i come out as exact zeros. Reads of T[r][l] are the same
     // address across the wave (LDS broadcast); the dot products use four
     // partial sums so consecutive FMAs do not wait on each other.
@@ -173,7 +179,7 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
             }
 #pragma unroll
             for (int l = r & ~3; l < r; ++l) s0 -= T[r][l] * x[l];
-            x[r] = ((s0 + s1) + (s2 + s3)) / T[r][r];
+            x[r] = ((s0 + s1) + (s2 + s3)) * rdiag[r];
         }
         __syncthreads();
         // transpose through LDS so each lane writes a row of the inverse
