@@ -259,3 +259,30 @@ def test_long_run_inverse_updates_do_not_drift(dev):
             errs.append(rel_l2(y.cpu().numpy(), yo))
     assert win.status() == 0
     assert max(errs) < 1e-5, errs
+
+
+def test_default_policy_over_a_refactor_boundary_m1024(dev):
+    """m = 1024 with the default coefficient policy (O(m^2) inverse updates,
+    full refactor every 1024 replaces): 1100 steps, checked right before,
+    at and after the refactor and at the end."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_resnet50_d25.6m_m1024")
+    wl = base.scaled(d=8192, scale_d=base.d)
+    gs = GradientStream(wl, seed=21, device="cpu")
+    G0 = gs.window()
+    win = Window(wl.d, wl.m, wl.lam, G0=G0.to(dev), device=dev)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    checked = {0, 1, 511, 1021, 1022, 1023, 1024, 1025, 1099}
+    say("default policy over a refactor boundary, m = 1024")
+    errs = []
+    for t in range(1100):
+        g = gs.row(wl.m + t)
+        y = win.replace(g.to(dev))
+        if t in checked:
+            yo = orc.slide(g.numpy())
+            errs.append(rel_l2(y.cpu().numpy(), yo))
+            assert errs[-1] < REL_TOL, (t, errs[-1])
+        else:
+            orc.replace(orc.steps % wl.m, g.numpy())
+    assert win.status() == 0
+    assert win.info() == (1100 % wl.m, 1100)
