@@ -48,8 +48,9 @@ def build(verbose: bool = False) -> str:
         if r.returncode != 0:
             sys.stderr.write(r.stderr)
             raise subprocess.CalledProcessError(r.returncode, cmd)
-        # kernels that use per-lane scratch (arrays the compiler did not keep
-        # in registers) are a performance bug: report them
+        # report kernels that use per-lane scratch: a staging array the
+        # compiler did not keep in registers is a performance bug; the window
+        # Gram's spills under its two-work-group launch bound are expected
         name = None
         for line in r.stderr.splitlines():
             m = re.search(r"Function Name: (\S+)", line)
