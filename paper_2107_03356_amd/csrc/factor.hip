@@ -95,12 +95,13 @@ __device__ __forceinline__ void task_tiles(const GemmArgs& g, int t, int& I0, in
 // One work-group per task of one or two 128 x 128 output tiles (a long and a
 // short tile of a triangular product together, so tasks take equal time;
 // lower-triangle products launch only their lower tiles), 16-deep k-chunks
-// through double-buffered LDS with the next chunk's loads in flight; two
-// work-groups per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
+// through double-buffered LDS with the next chunk's loads in flight. Eight
+// waves per work-group, each owning 32 x 64 of a tile as 2 x 4 MFMA tiles, and
+// two work-groups per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
 // of 64) load clamped, in-bounds data and are never stored. The elements C
 // writes are disjoint from the ones A and B read (they may share a buffer).
 template <bool TA, bool TB>
-__global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
+__global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
     __shared__ double As[2][TA ? BK : BM][TA ? PBN : PA];
     __shared__ double Bs[2][TB ? BN : BK][TB ? PA : PBN];
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
     double* __restrict__ C = g.C + (int64_t)bt * g.bstride;
     const int ld = g.ld;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
     const int rl = lane & 15, kl = lane >> 4;
     auto tile = [&](int I, int J) {
         int klo = 0, khi = g.K;
@@ -122,10 +123,11 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
         if (g.flags & KLO_COL) klo = J * BN;
         const int mrow0 = I * BM, ncol0 = J * BN;
 
-        // staging of 2048 doubles per operand and chunk, 8 per thread:
-        //   [row][k] layout: row tid/2, k (tid%2)*8 .. +7 (two 64-byte row pieces)
-        //   [k][row] layout: k tid/64 + 4q, row 2*(tid%64) .. +1 (a wave per 1 KB row)
-        const int sr = tid >> 1, sk = (tid & 1) * 8;
+        // staging of 2048 doubles per operand and chunk, 4 per thread (two
+        // double2, kept in named registers):
+        //   [row][k] layout: row tid/4, k (tid%4)*4 .. +3 (32-byte row pieces)
+        //   [k][row] layout: k tid/64 and tid/64 + 8, row 2*(tid%64) .. +1 (a wave per 1 KB row)
+        const int sr = tid >> 2, sk = (tid & 3) * 4;
         const int tk = tid >> 6, tn = (tid & 63) * 2;
         // clamped source rows / columns (M, N are even, so a clamped pair stays
         // inside the operand)
@@ -135,18 +137,21 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
             TA ? A + (int64_t)g.a0r * ld + g.a0c + am : A + (int64_t)(g.a0r + am) * ld + g.a0c + sk;
         const double* __restrict__ bp =
             TB ? B + (int64_t)(g.b0r + bn) * ld + g.b0c + sk : B + (int64_t)g.b0r * ld + g.b0c + bn;
-        double2 pa[4], pb[4];
+        double2 pa0, pa1, pb0, pb1;
         auto load_chunk = [&](int k0) {
-    #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                if constexpr (TA)
-                    pa[q] = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk + 4 * q) * ld);
-                else
-                    pa[q] = *reinterpret_cast<const double2*>(ap + k0 + 2 * q);
-                if constexpr (TB)
-                    pb[q] = *reinterpret_cast<const double2*>(bp + k0 + 2 * q);
-                else
-                    pb[q] = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk + 4 * q) * ld);
+            if constexpr (TA) {
+                pa0 = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk) * ld);
+                pa1 = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk + 8) * ld);
+            } else {
+                pa0 = *reinterpret_cast<const double2*>(ap + k0);
+                pa1 = *reinterpret_cast<const double2*>(ap + k0 + 2);
+            }
+            if constexpr (TB) {
+                pb0 = *reinterpret_cast<const double2*>(bp + k0);
+                pb1 = *reinterpret_cast<const double2*>(bp + k0 + 2);
+            } else {
+                pb0 = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk) * ld);
+                pb1 = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk + 8) * ld);
             }
         };
         auto put = [](double* dst, double2 v) {
@@ -154,31 +159,34 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
             dst[1] = v.y;
         };
         auto store_chunk = [&](int buf) {
-    #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                if constexpr (TA)
-                    put(&As[buf][tk + 4 * q][tn], pa[q]);
-                else
-                    put(&As[buf][sr][sk + 2 * q], pa[q]);
-                if constexpr (TB)
-                    put(&Bs[buf][sr][sk + 2 * q], pb[q]);
-                else
-                    put(&Bs[buf][tk + 4 * q][tn], pb[q]);
+            if constexpr (TA) {
+                put(&As[buf][tk][tn], pa0);
+                put(&As[buf][tk + 8][tn], pa1);
+            } else {
+                put(&As[buf][sr][sk], pa0);
+                put(&As[buf][sr][sk + 2], pa1);
+            }
+            if constexpr (TB) {
+                put(&Bs[buf][sr][sk], pb0);
+                put(&Bs[buf][sr][sk + 2], pb1);
+            } else {
+                put(&Bs[buf][tk][tn], pb0);
+                put(&Bs[buf][tk + 8][tn], pb1);
             }
         };
 
         // C tile coordinates of accumulator (x, y, r): fp64 MFMA result register r
         // of lane l is row (l/16) + 4r, column l%16
-        auto crow = [&](int x, int r) { return mrow0 + wr * 64 + x * 16 + kl + 4 * r; };
+        auto crow = [&](int x, int r) { return mrow0 + wr * 32 + x * 16 + kl + 4 * r; };
         auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
         const int nchunk = (khi - klo) / BK;
         if (nchunk > 0) load_chunk(klo);
         // beta C enters as the accumulator's start value (scaled by 1/alpha), so
         // its loads issue together with the first chunk's
-        v4d acc[4][4];
+        v4d acc[2][4];
         const double cs = g.beta / g.alpha;
     #pragma unroll
-        for (int x = 0; x < 4; ++x)
+        for (int x = 0; x < 2; ++x)
     #pragma unroll
             for (int y = 0; y < 4; ++y)
     #pragma unroll
@@ -199,15 +207,15 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
             if (c + 1 < nchunk) load_chunk(klo + (c + 1) * BK);
     #pragma unroll
             for (int kk = 0; kk < BK / 4; ++kk) {
-                double av[4], bv[4];
+                double av[2], bv[4];
     #pragma unroll
-                for (int x = 0; x < 4; ++x)
-                    av[x] = TA ? As[buf][kk * 4 + kl][wr * 64 + x * 16 + rl] : As[buf][wr * 64 + x * 16 + rl][kk * 4 + kl];
+                for (int x = 0; x < 2; ++x)
+                    av[x] = TA ? As[buf][kk * 4 + kl][wr * 32 + x * 16 + rl] : As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
     #pragma unroll
                 for (int y = 0; y < 4; ++y)
                     bv[y] = TB ? Bs[buf][wc * 64 + y * 16 + rl][kk * 4 + kl] : Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
     #pragma unroll
-                for (int x = 0; x < 4; ++x)
+                for (int x = 0; x < 2; ++x)
     #pragma unroll
                     for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
@@ -216,7 +224,7 @@ __global__ __launch_bounds__(256, 2) void k_bgemm(GemmArgs g) {
             __syncthreads();
         }
     #pragma unroll
-        for (int x = 0; x < 4; ++x)
+        for (int x = 0; x < 2; ++x)
     #pragma unroll
             for (int y = 0; y < 4; ++y)
     #pragma unroll
@@ -269,10 +277,10 @@ hipError_t gemm(bool ta, bool tb, const double* A, int a0r, int a0c, const doubl
         g.ntask = g.tiles_m * g.tiles_n;
     }
     const int64_t grid = (int64_t)g.ntask * nbatch;
-    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<false, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
-    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<false, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
-    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<true, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
-    if (ta && tb) hipLaunchKernelGGL((k_bgemm<true, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
+    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<false, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<false, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<true, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (ta && tb) hipLaunchKernelGGL((k_bgemm<true, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
     return hipGetLastError();
 }
 

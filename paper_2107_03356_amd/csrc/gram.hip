@@ -180,8 +180,12 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
 // LDS in 32-column chunks, the next chunk's loads in flight during the MFMAs.
 constexpr int GT = 128;
 
-__global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d, int B, int b0,
-                                                     int ntiles, double mu, double* __restrict__ A, int mp) {
+// Eight waves per 128 x 128 tile, each owning 32 x 64 as 2 x 4 MFMA tiles, and
+// two work-groups per CU (4 waves per SIMD hide each other's LDS and memory
+// waits). Staged chunk values live in named registers.
+__global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d, int B,
+                                                        int b0, int ntiles, double mu, double* __restrict__ A,
+                                                        int mp) {
     __shared__ float As[2][GT][PITCH];
     __shared__ float Bs[2][GT][PITCH];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
@@ -189,79 +193,87 @@ __global__ __launch_bounds__(256) void k_gram_blocks(const float* __restrict__ G
     int ti, tj;
     tile_of(lid - bl * ntiles, ti, tj);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
     const int rl = lane & 15, kl = lane >> 4;
     const bool diag_tile = ti == tj;
-    // in a diagonal tile the quadrant above the diagonal is never read (the
-    // factorization uses the lower triangle): its wave only stages operands
-    const bool upper_wave = diag_tile && wr < wc;
+    // in a diagonal tile the part above the diagonal is never read (the
+    // factorization uses the lower triangle): waves wholly above it only stage
+    const bool upper_wave = diag_tile && wr * 32 + 31 < wc * 64;
     const float* base = G + (int64_t)(b0 + bl) * B;
     const int ra0 = ti * GT, rb0 = tj * GT;
-    // staging: 128 rows x 32 columns per operand, 16 floats per thread
-    const int sr = tid >> 1, sc = (tid & 1) * 16;
-    float4 pa[4], pb[4];
-    auto load_chunk = [&](int k0) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int col = k0 + sc + 4 * q;
-            const bool okc = col < B;
-            pa[q] = (ra0 + sr < m && okc) ? *reinterpret_cast<const float4*>(base + (int64_t)(ra0 + sr) * d + col)
-                                          : make_float4(0.f, 0.f, 0.f, 0.f);
-            if (!diag_tile)
-                pb[q] = (rb0 + sr < m && okc) ? *reinterpret_cast<const float4*>(base + (int64_t)(rb0 + sr) * d + col)
-                                              : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-    };
-    auto store_chunk = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            *reinterpret_cast<float4*>(&As[buf][sr][sc + 4 * q]) = pa[q];
-            if (!diag_tile) *reinterpret_cast<float4*>(&Bs[buf][sr][sc + 4 * q]) = pb[q];
-        }
-    };
+    // staging: 128 rows x 32 columns per operand, 8 floats per thread and operand
+    const int sr = tid >> 2, sc = (tid & 3) * 8;
+    const bool oka = ra0 + sr < m, okb = rb0 + sr < m;
+    const float* rowa = base + (int64_t)(ra0 + sr) * d;
+    const float* rowb = base + (int64_t)(rb0 + sr) * d;
+    float4 pa0, pa1, pb0, pb1;
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#define MFAC_GB_LOAD(K0_)                                                                              \
+    {                                                                                                  \
+        const int c_ = (K0_) + sc;                                                                     \
+        pa0 = (oka && c_ < B) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;                    \
+        pa1 = (oka && c_ + 4 < B) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;            \
+        if (!diag_tile) {                                                                              \
+            pb0 = (okb && c_ < B) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;                \
+            pb1 = (okb && c_ + 4 < B) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero;        \
+        }                                                                                              \
+    }
+#define MFAC_GB_STORE(BUF_)                                                                            \
+    {                                                                                                  \
+        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                                     \
+        a_[0] = pa0;                                                                                   \
+        a_[1] = pa1;                                                                                   \
+        if (!diag_tile) {                                                                              \
+            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                                 \
+            b_[0] = pb0;                                                                               \
+            b_[1] = pb1;                                                                               \
+        }                                                                                              \
+    }
 
-    v4d acc[4][4];
+    v4d acc[2][4];
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
     const int nchunk = (B + KB - 1) / KB;
-    load_chunk(0);
-    store_chunk(0);
+    MFAC_GB_LOAD(0)
+    MFAC_GB_STORE(0)
     __syncthreads();
     for (int c = 0; c < nchunk; ++c) {
         const int buf = c & 1;
-        if (c + 1 < nchunk) load_chunk((c + 1) * KB);
+        if (c + 1 < nchunk) MFAC_GB_LOAD((c + 1) * KB)
         float (*Ab)[PITCH] = As[buf];
         float (*Bb)[PITCH] = diag_tile ? As[buf] : Bs[buf];
         if (!upper_wave) {
 #pragma unroll
             for (int kk = 0; kk < KB / 4; ++kk) {
-                double av[4], bv[4];
+                double av[2], bv[4];
 #pragma unroll
-                for (int x = 0; x < 4; ++x) av[x] = (double)Ab[wr * 64 + x * 16 + rl][kk * 4 + kl];
+                for (int x = 0; x < 2; ++x) av[x] = (double)Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
                 for (int y = 0; y < 4; ++y) bv[y] = (double)Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                for (int x = 0; x < 4; ++x)
+                for (int x = 0; x < 2; ++x)
 #pragma unroll
                     for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
         }
-        if (c + 1 < nchunk) store_chunk(buf ^ 1);
+        if (c + 1 < nchunk) MFAC_GB_STORE(buf ^ 1)
         __syncthreads();
     }
+#undef MFAC_GB_LOAD
+#undef MFAC_GB_STORE
     if (upper_wave) return;
     double* Ab = A + (int64_t)bl * mp * mp;
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 4; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 // fp64 MFMA result: lane l register r is row (l/16) + 4r
-                const int row = ra0 + wr * 64 + x * 16 + kl + 4 * r;
+                const int row = ra0 + wr * 32 + x * 16 + kl + 4 * r;
                 const int col = rb0 + wc * 64 + y * 16 + rl;
                 if (row < mp && col < mp) {
                     double v = acc[x][y][r];
@@ -309,7 +321,7 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
                               double* A, int mp, hipStream_t st) {
     const int T = (int)ceil_div(mp, GT);
     const int ntiles = T * (T + 1) / 2;
-    hipLaunchKernelGGL(k_gram_blocks, dim3((unsigned)(ntiles * nb)), dim3(256), 0, st, G, m, d, B, b0, ntiles, mu, A,
+    hipLaunchKernelGGL(k_gram_blocks, dim3((unsigned)(ntiles * nb)), dim3(512), 0, st, G, m, d, B, b0, ntiles, mu, A,
                        mp);
     return hipGetLastError();
 }

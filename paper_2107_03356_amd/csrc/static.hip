@@ -29,23 +29,24 @@ constexpr int PB = TN + 16;                 // LDS pitch of the G chunk, [k][col
 // grid: nslice * nb work-groups (flattened, remapped); slice = TN columns of a
 // block. Each work-group walks the 128-row tiles of its slice from the bottom
 // up; tile r needs L^-1 columns [0, (r+1)*128) and the same rows of G, so G
-// rows that tile r overwrites are never read again. Two work-groups per CU.
+// rows that tile r overwrites are never read again. Eight waves, each owning
+// 32 x 64 of the tile as 2 x 4 MFMA tiles, and two work-groups per CU.
 //
 // Operand values that are never used load clamped, in-bounds addresses:
 // L^-1 rows past mp, G rows past m (their L^-1 coefficients are the exact
 // zeros above the diagonal; the K range stays inside the diagonal 128-block,
 // whose upper part is zero) and columns past the slice. W rows past m (zero
 // padding or clamped rows) are neither stored nor summed.
-__global__ __launch_bounds__(256, 2) void k_trmm_diag(const double* __restrict__ Linv, int mp, int64_t bstride,
+__global__ __launch_bounds__(512, 4) void k_trmm_diag(const double* __restrict__ Linv, int mp, int64_t bstride,
                                                       float* __restrict__ G, int m, int64_t d, int B, int b0,
                                                       int nslice, double inv_lam, double* __restrict__ diag) {
     __shared__ double As[2][TM][PA];
     __shared__ double Bs[2][TK][PB];
-    __shared__ double red[2][TN];
+    __shared__ double red[4][TN];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     const int bl = lid / nslice, sl = lid - (lid / nslice) * nslice;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
     const int rl = lane & 15, kl = lane >> 4;
     const int b = b0 + bl;
     const int c0 = sl * TN;
@@ -54,78 +55,74 @@ __global__ __launch_bounds__(256, 2) void k_trmm_diag(const double* __restrict__
     float* __restrict__ Gb = G + (int64_t)b * B + c0;
     const int T = (mp + TM - 1) / TM;
 
-    // staging of one k-chunk: L^-1 rows [r0, r0+128) x cols [k0, k0+16), 8
-    // doubles per thread (row tid/2, cols (tid%2)*8..+7); G rows [k0, k0+16) x
-    // 128 columns, 8 floats per thread (row tid/16, cols (tid%16)*8..+7)
-    const int ar = tid >> 1, ac = (tid & 1) * 8;
-    const int br = tid >> 4, bc = (tid & 15) * 8;
-    const int bc0 = min(bc, ncol - 4), bc1 = min(bc + 4, ncol - 4);
-    double2 ra[4];
-    float4 rb[2];
-    auto load_chunk = [&](int r0, int k0) {
-        const double* src = Lb + (int64_t)min(r0 + ar, mp - 1) * mp + k0 + ac;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) ra[q] = *reinterpret_cast<const double2*>(src + 2 * q);
-        const float* gsrc = Gb + (int64_t)min(k0 + br, m - 1) * d;
-        rb[0] = *reinterpret_cast<const float4*>(gsrc + bc0);
-        rb[1] = *reinterpret_cast<const float4*>(gsrc + bc1);
-    };
-    auto store_chunk = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            As[buf][ar][ac + 2 * q] = ra[q].x;
-            As[buf][ar][ac + 2 * q + 1] = ra[q].y;
-        }
-        double* bd = &Bs[buf][br][bc];
-        bd[0] = rb[0].x;
-        bd[1] = rb[0].y;
-        bd[2] = rb[0].z;
-        bd[3] = rb[0].w;
-        bd[4] = rb[1].x;
-        bd[5] = rb[1].y;
-        bd[6] = rb[1].z;
-        bd[7] = rb[1].w;
-    };
+    // staging of one k-chunk: L^-1 rows [r0, r0+128) x cols [k0, k0+16), 4
+    // doubles per thread (row tid/4, cols (tid%4)*4..+3); G rows [k0, k0+16) x
+    // 128 columns, 4 floats per thread (row tid/32, cols (tid%32)*4..+3)
+    const int ar = tid >> 2, ac = (tid & 3) * 4;
+    const int br = tid >> 5, bc = (tid & 31) * 4;
+    const int bcc = min(bc, ncol - 4);
+    double2 ra0, ra1;
+    float4 rb;
+#define MFAC_TR_LOAD(R0_, K0_)                                                                  \
+    {                                                                                          \
+        const double* src_ = Lb + (int64_t)min((R0_) + ar, mp - 1) * mp + (K0_) + ac;          \
+        ra0 = *reinterpret_cast<const double2*>(src_);                                         \
+        ra1 = *reinterpret_cast<const double2*>(src_ + 2);                                     \
+        rb = *reinterpret_cast<const float4*>(Gb + (int64_t)min((K0_) + br, m - 1) * d + bcc); \
+    }
+#define MFAC_TR_STORE(BUF_)                                                                     \
+    {                                                                                          \
+        double* ad_ = &As[BUF_][ar][ac];                                                       \
+        ad_[0] = ra0.x;                                                                        \
+        ad_[1] = ra0.y;                                                                        \
+        ad_[2] = ra1.x;                                                                        \
+        ad_[3] = ra1.y;                                                                        \
+        double* bd_ = &Bs[BUF_][br][bc];                                                       \
+        bd_[0] = rb.x;                                                                         \
+        bd_[1] = rb.y;                                                                         \
+        bd_[2] = rb.z;                                                                         \
+        bd_[3] = rb.w;                                                                         \
+    }
 
     double sq[4] = {0.0, 0.0, 0.0, 0.0};
     for (int r = T - 1; r >= 0; --r) {
-        v4d acc[4][4];
+        v4d acc[2][4];
 #pragma unroll
-        for (int x = 0; x < 4; ++x)
+        for (int x = 0; x < 2; ++x)
 #pragma unroll
             for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
         const int khi = min((r + 1) * TM, mp);
         const int nchunk = khi / TK;
-        load_chunk(r * TM, 0);
-        store_chunk(0);
+        MFAC_TR_LOAD(r * TM, 0)
+        MFAC_TR_STORE(0)
         __syncthreads();
         for (int c = 0; c < nchunk; ++c) {
             const int buf = c & 1;
-            if (c + 1 < nchunk) load_chunk(r * TM, (c + 1) * TK);
+            if (c + 1 < nchunk) MFAC_TR_LOAD(r * TM, (c + 1) * TK)
 #pragma unroll
             for (int kk = 0; kk < TK / 4; ++kk) {
-                double av[4], bv[4];
+                double av[2], bv[4];
 #pragma unroll
-                for (int x = 0; x < 4; ++x) av[x] = As[buf][wr * 64 + x * 16 + rl][kk * 4 + kl];
+                for (int x = 0; x < 2; ++x) av[x] = As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
                 for (int y = 0; y < 4; ++y) bv[y] = Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
 #pragma unroll
-                for (int x = 0; x < 4; ++x)
+                for (int x = 0; x < 2; ++x)
 #pragma unroll
                     for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
-            if (c + 1 < nchunk) store_chunk(buf ^ 1);
+            if (c + 1 < nchunk) MFAC_TR_STORE(buf ^ 1)
             __syncthreads();
         }
         // W tile r: write over G (fp32) and accumulate squares from the fp64 values
 #pragma unroll
-        for (int x = 0; x < 4; ++x)
+        for (int x = 0; x < 2; ++x)
 #pragma unroll
             for (int y = 0; y < 4; ++y)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int row = r * TM + wr * 64 + x * 16 + kl + 4 * q;  // fp64 MFMA: row (l/16) + 4q
+                    const int row = r * TM + wr * 32 + x * 16 + kl + 4 * q;  // fp64 MFMA: row (l/16) + 4q
                     const int col = wc * 64 + y * 16 + rl;
                     const double w = acc[x][y][q];
                     if (row < m) {
@@ -134,7 +131,9 @@ __global__ __launch_bounds__(256, 2) void k_trmm_diag(const double* __restrict__
                     }
                 }
     }
-    // column sums of squares: over kl (lanes +16, +32), then over wr
+#undef MFAC_TR_LOAD
+#undef MFAC_TR_STORE
+    // column sums of squares: over kl (lanes +16, +32), then over the four wr
 #pragma unroll
     for (int y = 0; y < 4; ++y) {
         sq[y] += __shfl_xor(sq[y], 16, 64);
@@ -145,7 +144,8 @@ __global__ __launch_bounds__(256, 2) void k_trmm_diag(const double* __restrict__
         for (int y = 0; y < 4; ++y) red[wr][wc * 64 + y * 16 + rl] = sq[y];
     }
     __syncthreads();
-    if (tid < ncol) diag[(int64_t)b * B + c0 + tid] = (1.0 - (red[0][tid] + red[1][tid])) * inv_lam;
+    if (tid < ncol)
+        diag[(int64_t)b * B + c0 + tid] = (1.0 - ((red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]))) * inv_lam;
 }
 
 __global__ void k_diag_to_f32(const double* __restrict__ dg, int64_t d, float* __restrict__ out) {
@@ -315,7 +315,7 @@ __global__ void k_fill_u8(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
 hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* G, int m, int64_t d, int B,
                             int b0, int nb, double lam, double* diag, hipStream_t st) {
     const int nslice = (int)ceil_div(B, TN);
-    hipLaunchKernelGGL(k_trmm_diag, dim3((unsigned)(nslice * nb)), dim3(256), 0, st, Linv, mp, bstride, G, m, d, B,
+    hipLaunchKernelGGL(k_trmm_diag, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv, mp, bstride, G, m, d, B,
                        b0, nslice, 1.0 / lam, diag);
     return hipGetLastError();
 }
