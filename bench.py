@@ -64,6 +64,27 @@ def read_counters(kernel):
     return float(m.group(1)) if m else None
 
 
+STATIC_COUNTERS = os.path.join(ROOT, "profiles", "static_d4.19m_b2048_m1024_counters.md")
+STATIC_SRC = [os.path.join(ROOT, "paper_2107_03356_amd", "csrc", f)
+              for f in ("gram.hip", "static.hip", "factor.hip", "chol.hip", "tile_util.h")]
+
+
+def read_static_counters(kernel):
+    """HBM bytes per launch of a static-path kernel from the committed
+    rocprofv3 --pmc summary, if it was taken on the current sources (else None)."""
+    if not os.path.exists(STATIC_COUNTERS):
+        return None
+    text = open(STATIC_COUNTERS).read()
+    h = hashlib.sha256()
+    for path in STATIC_SRC:
+        h.update(open(path, "rb").read())
+    m = re.search(r"static_src_sha256_16:\s*(\w+)", text)
+    if not m or m.group(1) != h.hexdigest()[:16]:
+        return None
+    m = re.search(rf"{kernel}_traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    return float(m.group(1)) if m else None
+
+
 def cpu_baseline(wl, seed, sample_div, nsteps):
     """The fp64 oracle as it stands, on a column sample of the same workload.
 
@@ -138,13 +159,14 @@ def bench_static(args, wl, dev):
     keep = d // 2
     log(f"setup {time.perf_counter() - t0:.1f} s")
     times = []
+    stage_ms, stage_cnt = [0.0] * 4, [0] * 4
     stream = torch.cuda.current_stream(dev)
     for rep in range(args.warmup + args.steps):
         G.copy_(G0)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        sb = P.StaticBlocks(G, B, wl.lam)
+        sb = P.StaticBlocks(G, B, wl.lam, trace=True)
         diag = sb.inv_diag()
         mask, _ = sb.obs_mask(theta, keep, scores=False)
         e1.record(stream)
@@ -152,12 +174,21 @@ def bench_static(args, wl, dev):
         if sb.status() != 0:
             log("device error in the static path")
             sys.exit(1)
+        sms, scnt = sb.trace_read()
         if rep >= args.warmup:
             times.append(e0.elapsed_time(e1))
+            for i in range(4):
+                stage_ms[i] += sms[i]
+                stage_cnt[i] += scnt[i]
         log(f"rep {rep}: {e0.elapsed_time(e1):.1f} ms")
         if rep + 1 < args.warmup + args.steps:
             sb.close()
     ms = sum(times) / len(times)
+    runs = len(times)
+    # dominant kernel: the batched Gram (lower half of G_b G_b^T: m^2 B flops per block)
+    gram_ms = stage_ms[0] / max(stage_cnt[0], 1)
+    gram_flops = float(m) * m * d * runs / max(stage_cnt[0], 1)
+    gram_tf = gram_flops / (gram_ms * 1e-3) / 1e12
 
     # queries on the finished precompute (W in place of G): block-wise IHVP
     # with 1 and 4 vectors, and the OBS correction for the keep-mask's complement
@@ -197,9 +228,15 @@ def bench_static(args, wl, dev):
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep},
-        "roofline": {"bound": "mfma", "kernel": "whole run (Gram, factor, W and diagonal, mask)",
-                     "achieved": flops / (ms * 1e-3) / 1e12, "peak": 78.6, "unit": "TFLOP/s",
-                     "frac": flops / (ms * 1e-3) / 1e12 / 78.6, "traffic": None},
+        "roofline": {"bound": "mfma", "kernel": "k_gram_blocks", "achieved": gram_tf, "peak": 78.6,
+                     "unit": "TFLOP/s", "frac": gram_tf / 78.6, "traffic": read_static_counters("k_gram_blocks")},
+        "whole_run": {"achieved_tflops": flops / (ms * 1e-3) / 1e12,
+                      "frac": flops / (ms * 1e-3) / 1e12 / 78.6,
+                      "flops": flops},
+        "stages_ms_per_run": {"gram": stage_ms[0] / runs, "factor_inverse": stage_ms[1] / runs,
+                              "w_and_diag": stage_ms[2] / runs, "scores_mask": stage_ms[3] / runs},
+        "stage_launches_per_run": {"gram": stage_cnt[0] // runs, "factor_inverse": stage_cnt[1] // runs,
+                                   "w_and_diag": stage_cnt[2] // runs, "scores_mask": stage_cnt[3] // runs},
         "queries": queries,
     }
     print(json.dumps(out), flush=True)

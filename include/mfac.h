@@ -196,10 +196,23 @@ size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m);
  * unrounded W and kept in the workspace.
  * Requirements: 1 <= m <= 8192, 4 <= block, block % 4 == 0,
  * d % block == 0, lambda > 0 finite, G 16-byte aligned, workspace 256-byte
- * aligned. */
+ * aligned, flags a combination of MFAC_STATIC_* bits. */
 mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m,
                                    double lambda, float* G, void* workspace,
-                                   size_t workspace_bytes, hipStream_t stream);
+                                   size_t workspace_bytes, uint32_t flags, hipStream_t stream);
+
+/* flags of mfac_static_precompute */
+#define MFAC_STATIC_TRACE 1u /* record HIP events around the precompute's stages and
+                                mfac_obs_mask; read with mfac_static_trace_read */
+
+/* Per-stage device time of a static handle created with MFAC_STATIC_TRACE,
+ * since creation or the last read (synchronises the stream). ms_out and
+ * count_out (host arrays of MFAC_STATIC_NPHASES) receive milliseconds and
+ * launch counts for: 0 batched Gram (one launch per batch of blocks), 1
+ * factor and inverse, 2 W and inverse diagonal, 3 scores and keep-mask.
+ * Without the flag every entry is 0. */
+#define MFAC_STATIC_NPHASES 4
+mfac_status mfac_static_trace_read(mfac_static s, double* ms_out /* host */, int64_t* count_out /* host */);
 
 /* diag(F^-1) for all d coordinates (Appendix C, row-selected extraction with
  * the identity selection), rounded to fp32. */

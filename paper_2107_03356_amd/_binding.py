@@ -22,6 +22,7 @@ MFAC_EWORKSPACE = -2
 MFAC_EHIP = -3
 MFAC_ENONFINITE = -4
 MFAC_ESTATE = -5
+MFAC_STATIC_TRACE = 1
 
 _c = ctypes
 _VP, _I32, _I64, _SZ, _F32, _F64 = _c.c_void_p, _c.c_int32, _c.c_int64, _c.c_size_t, _c.c_float, _c.c_double
@@ -48,7 +49,8 @@ SIGNATURES = {
     "mfac_window_status": (_c.c_int, [_VP]),
     "mfac_window_destroy": (_c.c_int, [_VP]),
     "mfac_static_workspace_bytes": (_SZ, [_I64, _I32, _I32]),
-    "mfac_static_precompute": (_c.c_int, [_PVP, _I64, _I32, _I32, _F64, _VP, _VP, _SZ, _VP]),
+    "mfac_static_precompute": (_c.c_int, [_PVP, _I64, _I32, _I32, _F64, _VP, _VP, _SZ, _c.c_uint32, _VP]),
+    "mfac_static_trace_read": (_c.c_int, [_VP, _c.POINTER(_F64), _c.POINTER(_I64)]),
     "mfac_inv_diag": (_c.c_int, [_VP, _VP]),
     "mfac_inv_diag64": (_c.c_int, [_VP, _VP]),
     "mfac_obs_mask": (_c.c_int, [_VP, _VP, _I64, _VP, _VP]),
@@ -242,7 +244,7 @@ class StaticBlocks:
     G is overwritten in place by W (W_b = R_b^-1 G_b per block).
     """
 
-    def __init__(self, G, block, lam, stream=None):
+    def __init__(self, G, block, lam, stream=None, trace=False):
         import torch
         self.torch = torch
         assert G.dtype == torch.float32 and G.is_contiguous() and G.dim() == 2
@@ -257,10 +259,20 @@ class StaticBlocks:
         self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
         self.stream = _stream_handle(torch, self.device, stream)
         h = ctypes.c_void_p()
+        flags = MFAC_STATIC_TRACE if trace else 0
         st = lib.mfac_static_precompute(ctypes.byref(h), self.d, self.block, self.m, self.lam, _ptr(G),
-                                        _ptr(self.workspace), wb, self.stream)
+                                        _ptr(self.workspace), wb, flags, self.stream)
         _check("mfac_static_precompute", st)
         self.handle = h
+
+    def trace_read(self):
+        """(ms per stage, launches per stage) since creation or the last read;
+        stages: Gram, factor and inverse, W and diagonal, scores and mask.
+        Zeros unless created with trace=True."""
+        ms = (ctypes.c_double * 4)()
+        cnt = (ctypes.c_int64 * 4)()
+        _check("mfac_static_trace_read", load().mfac_static_trace_read(self.handle, ms, cnt))
+        return list(ms), list(cnt)
 
     def inv_diag(self, out=None, fp64=False):
         t = self.torch

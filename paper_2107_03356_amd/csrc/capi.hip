@@ -78,6 +78,10 @@ struct mfac_static_s {
     double *A, *Linv, *diag, *scores, *qpart;
     float *qcoef, *xobs;
     SelectScratch sel;
+    // stage tracing (MFAC_STATIC_TRACE): events recorded around the stages
+    bool trace;
+    std::vector<mfac_window_s::Mark>* marks;
+    hipEvent_t open_ev;
 };
 
 namespace {
@@ -124,21 +128,56 @@ bool window_sizes_ok(int64_t d, int32_t m, int32_t max_q) {
     } while (0)
 
 // Tracing: mark_begin before a phase's first launch, mark_end after its last.
-hipError_t mark_begin(mfac_window w) {
-    if (!w->trace) return hipSuccess;
-    hipError_t e = hipEventCreate(&w->open_ev);
+template <typename H>
+hipError_t mark_begin(H* h) {
+    if (!h->trace) return hipSuccess;
+    hipError_t e = hipEventCreate(&h->open_ev);
     if (e != hipSuccess) return e;
-    return hipEventRecord(w->open_ev, w->st);
+    return hipEventRecord(h->open_ev, h->st);
 }
 
-hipError_t mark_end(mfac_window w, int phase) {
-    if (!w->trace) return hipSuccess;
+template <typename H>
+hipError_t mark_end(H* h, int phase) {
+    if (!h->trace) return hipSuccess;
     hipEvent_t b;
     hipError_t e = hipEventCreate(&b);
     if (e != hipSuccess) return e;
-    e = hipEventRecord(b, w->st);
-    w->marks->push_back({phase, w->open_ev, b});
+    e = hipEventRecord(b, h->st);
+    h->marks->push_back({phase, h->open_ev, b});
     return e;
+}
+
+// Sum and release the recorded marks of a handle into ms/count (nph phases).
+template <typename H>
+mfac_status marks_read(H* h, int nph, double* ms_out, int64_t* count_out) {
+    for (int i = 0; i < nph; ++i) {
+        ms_out[i] = 0.0;
+        count_out[i] = 0;
+    }
+    if (!h->marks) return MFAC_OK;
+    if (hipStreamSynchronize(h->st) != hipSuccess) return MFAC_EHIP;
+    mfac_status rc = MFAC_OK;
+    for (auto& mk : *h->marks) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, mk.a, mk.b) != hipSuccess) rc = MFAC_EHIP;
+        ms_out[mk.phase] += ms;
+        count_out[mk.phase] += 1;
+        (void)hipEventDestroy(mk.a);
+        (void)hipEventDestroy(mk.b);
+    }
+    h->marks->clear();
+    return rc;
+}
+
+template <typename H>
+void marks_free(H* h) {
+    if (!h->marks) return;
+    for (auto& mk : *h->marks) {
+        (void)hipEventDestroy(mk.a);
+        (void)hipEventDestroy(mk.b);
+    }
+    delete h->marks;
+    h->marks = nullptr;
 }
 
 // Full refactor from K (optionally after replacing row/column k with p):
@@ -380,23 +419,7 @@ MFAC_API mfac_status mfac_window_trace(mfac_window w, int32_t enable) {
 
 MFAC_API mfac_status mfac_window_trace_read(mfac_window w, double* ms_out, int64_t* count_out) {
     if (!w || !ms_out || !count_out) return MFAC_EINVAL;
-    for (int i = 0; i < MFAC_NPHASES; ++i) {
-        ms_out[i] = 0.0;
-        count_out[i] = 0;
-    }
-    if (!w->marks) return MFAC_OK;
-    HIPCHK(hipStreamSynchronize(w->st));
-    mfac_status rc = MFAC_OK;
-    for (auto& mk : *w->marks) {
-        float ms = 0.f;
-        if (hipEventElapsedTime(&ms, mk.a, mk.b) != hipSuccess) rc = MFAC_EHIP;
-        ms_out[mk.phase] += ms;
-        count_out[mk.phase] += 1;
-        (void)hipEventDestroy(mk.a);
-        (void)hipEventDestroy(mk.b);
-    }
-    w->marks->clear();
-    return rc;
+    return marks_read(w, MFAC_NPHASES, ms_out, count_out);
 }
 
 MFAC_API mfac_status mfac_window_status(mfac_window w) {
@@ -414,13 +437,7 @@ MFAC_API mfac_status mfac_window_status(mfac_window w) {
 
 MFAC_API mfac_status mfac_window_destroy(mfac_window w) {
     if (!w) return MFAC_OK;
-    if (w->marks) {
-        for (auto& mk : *w->marks) {
-            (void)hipEventDestroy(mk.a);
-            (void)hipEventDestroy(mk.b);
-        }
-        delete w->marks;
-    }
+    marks_free(w);
     free(w);
     return MFAC_OK;
 }
@@ -489,10 +506,12 @@ MFAC_API size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m)
 }
 
 MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m, double lambda,
-                                            float* G, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                                            float* G, void* workspace, size_t workspace_bytes, uint32_t flags,
+                                            hipStream_t stream) {
     if (!out) return MFAC_EINVAL;
     *out = nullptr;
     if (!static_sizes_ok(d, block, m)) return MFAC_EINVAL;
+    if (flags & ~MFAC_STATIC_TRACE) return MFAC_EINVAL;
     if (!(lambda > 0.0) || !isfinite(lambda)) return MFAC_EINVAL;
     if (!G || !workspace || !aligned16(G) || ((uintptr_t)workspace & 255u)) return MFAC_EINVAL;
     if (workspace_bytes < mfac_static_workspace_bytes(d, block, m)) return MFAC_EWORKSPACE;
@@ -507,25 +526,38 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
     s->lambda = lambda;
     s->G = G;
     s->st = stream;
+    s->trace = (flags & MFAC_STATIC_TRACE) != 0;
+    if (s->trace) s->marks = new std::vector<mfac_window_s::Mark>();
     static_layout<mfac_static_s>(d, block, m, (char*)workspace, s);
 
     const int64_t bstride = (int64_t)s->mp * s->mp;
     const double mu = (double)m * lambda;
     auto fail = [&]() {
+        (void)hipStreamSynchronize(s->st);
+        marks_free(s);
         free(s);
         return MFAC_EHIP;
     };
     if (launch_fill_zero((float*)s->err, 1, s->st) != hipSuccess) return fail();
     for (int b0 = 0; b0 < s->nblocks; b0 += s->batch) {
         const int nb = (s->nblocks - b0) < s->batch ? (s->nblocks - b0) : s->batch;
+        if (mark_begin(s) != hipSuccess) return fail();
         if (launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->st) != hipSuccess) return fail();
+        if (mark_end(s, 0) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
         if (launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st) != hipSuccess) return fail();
+        if (mark_end(s, 1) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
         if (launch_trmm_diag(s->Linv, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, s->st) !=
             hipSuccess)
             return fail();
+        if (mark_end(s, 2) != hipSuccess) return fail();
     }
     *out = s;
     return MFAC_OK;
+}
+
+MFAC_API mfac_status mfac_static_trace_read(mfac_static s, double* ms_out, int64_t* count_out) {
+    if (!s || !ms_out || !count_out) return MFAC_EINVAL;
+    return marks_read(s, MFAC_STATIC_NPHASES, ms_out, count_out);
 }
 
 MFAC_API mfac_status mfac_inv_diag(mfac_static s, float* diag_out) {
@@ -545,8 +577,10 @@ MFAC_API mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t ke
     if (!s || !theta || !keep_mask_out || keep < 0 || keep > s->d || !aligned4(theta)) return MFAC_EINVAL;
     if (scores_out && ((uintptr_t)scores_out & 7u)) return MFAC_EINVAL;
     double* sc = scores_out ? scores_out : s->scores;
+    HIPCHK(mark_begin(s));
     HIPCHK(launch_scores(theta, s->diag, s->d, sc, s->err, s->st));
     HIPCHK(launch_topk_mask(sc, s->d, keep, s->sel, keep_mask_out, s->st));
+    HIPCHK(mark_end(s, 3));
     return MFAC_OK;
 }
 
@@ -594,6 +628,8 @@ MFAC_API mfac_status mfac_static_status(mfac_static s) {
 }
 
 MFAC_API mfac_status mfac_static_destroy(mfac_static s) {
+    if (!s) return MFAC_OK;
+    marks_free(s);
     free(s);
     return MFAC_OK;
 }

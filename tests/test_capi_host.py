@@ -97,7 +97,18 @@ def test_static_precompute_rejects_on_host(args, expect):
     lib = B.load()
     h = ctypes.c_void_p()
     d, blk, m, lam = args
-    assert lib.mfac_static_precompute(ctypes.byref(h), d, blk, m, lam, 256, 512, 1 << 40, None) == expect
+    assert lib.mfac_static_precompute(ctypes.byref(h), d, blk, m, lam, 256, 512, 1 << 40, 0, None) == expect
     assert h.value is None
     # workspace too small
-    assert lib.mfac_static_precompute(ctypes.byref(h), 4096, 256, 64, 1e-4, 256, 512, 16, None) == B.MFAC_EWORKSPACE
+    assert lib.mfac_static_precompute(ctypes.byref(h), 4096, 256, 64, 1e-4, 256, 512, 16, 0, None) == B.MFAC_EWORKSPACE
+    # unknown flag bits
+    assert lib.mfac_static_precompute(ctypes.byref(h), 4096, 256, 64, 1e-4, 256, 512, 1 << 40, 6,
+                                      None) == B.MFAC_EINVAL
+
+
+def test_trace_read_rejects_null_arguments():
+    lib = B.load()
+    ms = (ctypes.c_double * 4)()
+    cnt = (ctypes.c_int64 * 4)()
+    assert lib.mfac_static_trace_read(None, ms, cnt) == B.MFAC_EINVAL
+    assert lib.mfac_window_trace_read(None, ms, cnt) == B.MFAC_EINVAL
