@@ -286,3 +286,33 @@ def test_default_policy_over_a_refactor_boundary_m1024(dev):
             orc.replace(orc.steps % wl.m, g.numpy())
     assert win.status() == 0
     assert win.info() == (1100 % wl.m, 1100)
+
+
+def test_two_windows_on_two_streams_interleaved(dev):
+    """Handles are independent: two windows, each bound to its own stream,
+    replaced alternately without host synchronisation, both match their oracles."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wls = [base.scaled(d=20000, m=48, scale_d=base.d), base.scaled(d=13001, m=70, scale_d=base.d)]
+    streams = [torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)]
+    say("two windows on two streams")
+    wins, orcs, gss, outs = [], [], [], [[], []]
+    for i, wl in enumerate(wls):
+        gs = GradientStream(wl, seed=50 + i)
+        G0 = gs.window()
+        with torch.cuda.stream(streams[i]):
+            wins.append(Window(wl.d, wl.m, wl.lam, G0=G0.to(dev), device=dev))
+        orcs.append(WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy()))
+        gss.append(gs)
+    torch.cuda.synchronize()
+    for t in range(6):
+        for i in range(2):
+            g = gss[i].row(wls[i].m + t)
+            with torch.cuda.stream(streams[i]):
+                outs[i].append((wins[i].replace(g.to(dev, non_blocking=False)), g))
+    torch.cuda.synchronize()
+    for i in range(2):
+        for y, g in outs[i]:
+            yo = orcs[i].slide(g.numpy())
+            assert rel_l2(y.cpu().numpy(), yo) < REL_TOL
+        assert wins[i].status() == 0
