@@ -64,17 +64,18 @@ def read_counters(kernel):
     return float(m.group(1)) if m else None
 
 
-STATIC_COUNTERS = os.path.join(ROOT, "profiles", "static_d4.19m_b2048_m1024_counters.md")
 STATIC_SRC = [os.path.join(ROOT, "paper_2107_03356_amd", "csrc", f)
               for f in ("gram.hip", "static.hip", "factor.hip", "chol.hip", "tile_util.h")]
 
 
-def read_static_counters(kernel):
+def read_static_counters(workload, kernel):
     """HBM bytes per launch of a static-path kernel from the committed
-    rocprofv3 --pmc summary, if it was taken on the current sources (else None)."""
-    if not os.path.exists(STATIC_COUNTERS):
+    rocprofv3 --pmc summary of this workload, if it was taken on the current
+    sources (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_counters.md")
+    if not os.path.exists(path):
         return None
-    text = open(STATIC_COUNTERS).read()
+    text = open(path).read()
     h = hashlib.sha256()
     for path in STATIC_SRC:
         h.update(open(path, "rb").read())
@@ -222,6 +223,13 @@ def bench_static(args, wl, dev):
         sys.exit(1)
     sb.close()
     log(f"queries: {queries}")
+    cpu = None
+    if not args.no_cpu_baseline:
+        del G, X, Y, delta
+        torch.cuda.empty_cache()
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_static_baseline(wl, G0, theta, wl.lam, args.cpu_blocks)
+        log(f"cpu baseline {cpu}")
     out = {
         "metric": "static block-wise precompute + inverse diagonal + top-50% OBD mask, runs/sec (1 GPU)",
         "value": 1000.0 / ms, "unit": "runs/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -229,7 +237,7 @@ def bench_static(args, wl, dev):
         "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep},
         "roofline": {"bound": "mfma", "kernel": "k_gram_blocks", "achieved": gram_tf, "peak": 78.6,
-                     "unit": "TFLOP/s", "frac": gram_tf / 78.6, "traffic": read_static_counters("k_gram_blocks")},
+                     "unit": "TFLOP/s", "frac": gram_tf / 78.6, "traffic": read_static_counters(wl.name, "k_gram_blocks")},
         "whole_run": {"achieved_tflops": flops / (ms * 1e-3) / 1e12,
                       "frac": flops / (ms * 1e-3) / 1e12 / 78.6,
                       "flops": flops},
@@ -238,6 +246,7 @@ def bench_static(args, wl, dev):
         "stage_launches_per_run": {"gram": stage_cnt[0] // runs, "factor_inverse": stage_cnt[1] // runs,
                                    "w_and_diag": stage_cnt[2] // runs, "scores_mask": stage_cnt[3] // runs},
         "queries": queries,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 
@@ -373,6 +382,39 @@ def bench_optimizer(args, wl, dev):
     print(json.dumps(out), flush=True)
 
 
+def cpu_static_baseline(wl, G0, theta, lam, nsample):
+    """The oracle's block-wise inverse diagonal, scores and keep-mask (fp64) on a
+    column sample of the same G: the first `nsample` whole blocks, or for B = d
+    the first d/32 columns as one block. The time is scaled by d / sampled
+    columns (the O(m^2 d) Gram and solve dominate; for B = d the sampled
+    block's m^3 Cholesky is scaled with them, a slight overestimate)."""
+    from oracle import mask as omask
+    from oracle import static as ostatic
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    d, B = wl.d, wl.block
+    if d // B > 1:
+        ds, bs = min(nsample, d // B) * B, B
+        what = f"{ds // B} blocks of {B}"
+    else:
+        ds = d // 32
+        bs = ds
+        what = f"one block of the first {ds} columns (d/32)"
+    Gs = G0[:, :ds].cpu().numpy()
+    ts = theta[:ds].cpu().numpy()
+    t0 = time.perf_counter()
+    dg = ostatic.inv_diag(Gs, lam, bs)
+    omask.keep_mask(omask.scores(ts, dg), ds // 2)
+    sec = (time.perf_counter() - t0) * (d / ds)
+    return {"value": 1.0 / sec, "unit": "runs/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"oracle inverse diagonal + scores + keep-mask (numpy fp64, Cholesky and triangular "
+                       f"solve per block) on {what} of the same G, time x{d / ds:.0f}")}
+
+
 def cpu_optimizer_baseline(wl, seed, nsteps):
     """The oracle's M-FAC step (window insert + F^-1 g, fp64) at the model's d
     and m, on a full window, without the model's forward/backward."""
@@ -410,6 +452,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-div", type=int, default=64)
     ap.add_argument("--cpu-steps", type=int, default=3)
+    ap.add_argument("--cpu-blocks", type=int, default=128,
+                    help="static workloads: blocks the oracle baseline is timed on")
     ap.add_argument("--refactor-period", type=int, default=None,
                     help="coefficient policy: full refactor every N replaces (0 = every replace); default: the library's")
     args = ap.parse_args()

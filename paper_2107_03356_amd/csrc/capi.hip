@@ -75,7 +75,7 @@ struct mfac_static_s {
     float* G;
     hipStream_t st;
     int* err;
-    double *A, *Linv, *diag, *scores, *qpart;
+    double *A, *Linv, *gpart, *diag, *scores, *qpart;
     float *qcoef, *xobs;
     SelectScratch sel;
     // stage tracing (MFAC_STATIC_TRACE): events recorded around the stages
@@ -466,7 +466,17 @@ int static_batch(int64_t d, int B, int m) {
     if (b < 1) b = 1;
     if (b > 65535) b = 65535;
     if (b > nblocks) b = nblocks;
-    return (int)b;
+    // equal batches (the last one at most one block smaller than the others)
+    const int64_t nbatch = ceil_div(nblocks, b);
+    return (int)ceil_div(nblocks, nbatch);
+}
+
+// partial-tile storage of the split block Gram, for the largest need among the
+// batch sizes used (full batches and the last one)
+int64_t static_gram_part(int64_t nblocks, int batch, int mp, int B) {
+    const int last = (int)(nblocks - (ceil_div(nblocks, batch) - 1) * batch);
+    const int64_t a = gram_blocks_part_doubles(batch, mp, B), b = gram_blocks_part_doubles(last, mp, B);
+    return a > b ? a : b;
 }
 
 template <typename S>
@@ -480,6 +490,7 @@ size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
     char* sel = c.take<char>((size_t)select_scratch_bytes(d));
     double* A = c.take<double>((size_t)batch * mp * mp);
     double* Linv = c.take<double>((size_t)batch * mp * mp);
+    double* gpart = c.take<double>((size_t)static_gram_part(d / B, batch, mp, B));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
     float* qcoef = c.take<float>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
@@ -493,6 +504,7 @@ size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
         s->sel = select_scratch_carve(sel, d);
         s->A = A;
         s->Linv = Linv;
+        s->gpart = gpart;
         s->batch = batch;
     }
     return c.off;
@@ -542,7 +554,7 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
     for (int b0 = 0; b0 < s->nblocks; b0 += s->batch) {
         const int nb = (s->nblocks - b0) < s->batch ? (s->nblocks - b0) : s->batch;
         if (mark_begin(s) != hipSuccess) return fail();
-        if (launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->st) != hipSuccess) return fail();
+        if (launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->gpart, s->st) != hipSuccess) return fail();
         if (mark_end(s, 0) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
         if (launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st) != hipSuccess) return fail();
         if (mark_end(s, 1) != hipSuccess || mark_begin(s) != hipSuccess) return fail();

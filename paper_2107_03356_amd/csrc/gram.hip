@@ -14,6 +14,10 @@
 // Static blocks: fp64 MFMA (v_mfma_f64_16x16x4f64) over the block's columns
 // in 128 x 128 tiles, written straight into the block's padded fp64 matrix
 // with m*lambda added on the diagonal, because the keep-mask is decided in fp64.
+// When a batch has too few tiles to fill the chip (few, wide blocks; B = d is
+// the full-d precompute of Section 3.1) the block's columns are also split
+// over work-groups and the fp64 partial tiles are summed in split order by
+// k_gram_blocks_reduce.
 #include "internal.h"
 #include "tile_util.h"
 
@@ -175,23 +179,31 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const double* __restrict__ 
 }
 
 // Static blocks, fp64 MFMA. One work-group per 128 x 128 lower-triangular tile
-// of one block's Gram matrix (flattened over blocks, XCD-remapped so the tiles
-// of a block share an L2); the block's columns stream through double-buffered
-// LDS in 32-column chunks, the next chunk's loads in flight during the MFMAs.
+// of one block's Gram matrix and column split (flattened over blocks, splits
+// and tiles, XCD-remapped so the tiles of one block and split share an L2);
+// the split's columns stream through double-buffered LDS in 32-column chunks,
+// the next chunk's loads in flight during the MFMAs.
 constexpr int GT = 128;
 
 // Eight waves per 128 x 128 tile, each owning 32 x 64 as 2 x 4 MFMA tiles, and
 // two work-groups per CU (4 waves per SIMD hide each other's LDS and memory
-// waits). Staged chunk values live in named registers.
+// waits). Staged chunk values live in named registers. nsplit == 1: the tile
+// goes straight into A (plus mu on the diagonal); otherwise split s of the
+// block's columns [s*kcols, min(B, (s+1)*kcols)) writes its fp64 partial tile
+// to part[(block*nsplit + s)*ntiles + tile].
 __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d, int B,
-                                                        int b0, int ntiles, double mu, double* __restrict__ A,
-                                                        int mp) {
+                                                        int b0, int ntiles, int nsplit, int kcols, double mu,
+                                                        double* __restrict__ A, int mp, double* __restrict__ part) {
     __shared__ float As[2][GT][PITCH];
     __shared__ float Bs[2][GT][PITCH];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
-    const int bl = lid / ntiles;
+    const int per_block = ntiles * nsplit;
+    const int bl = lid / per_block;
+    const int rem = lid - bl * per_block;
+    const int sp = rem / ntiles;
+    const int tile = rem - sp * ntiles;
     int ti, tj;
-    tile_of(lid - bl * ntiles, ti, tj);
+    tile_of(tile, ti, tj);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
     const int rl = lane & 15, kl = lane >> 4;
@@ -199,7 +211,9 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
     // in a diagonal tile the part above the diagonal is never read (the
     // factorization uses the lower triangle): waves wholly above it only stage
     const bool upper_wave = diag_tile && wr * 32 + 31 < wc * 64;
-    const float* base = G + (int64_t)(b0 + bl) * B;
+    const int cbeg = sp * kcols;
+    const int ncols = (B - cbeg) < kcols ? (B - cbeg) : kcols;
+    const float* base = G + (int64_t)(b0 + bl) * B + cbeg;
     const int ra0 = ti * GT, rb0 = tj * GT;
     // staging: 128 rows x 32 columns per operand, 8 floats per thread and operand
     const int sr = tid >> 2, sc = (tid & 3) * 8;
@@ -211,11 +225,11 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
 #define MFAC_GB_LOAD(K0_)                                                                              \
     {                                                                                                  \
         const int c_ = (K0_) + sc;                                                                     \
-        pa0 = (oka && c_ < B) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;                    \
-        pa1 = (oka && c_ + 4 < B) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;            \
+        pa0 = (oka && c_ < ncols) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;                \
+        pa1 = (oka && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;        \
         if (!diag_tile) {                                                                              \
-            pb0 = (okb && c_ < B) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;                \
-            pb1 = (okb && c_ + 4 < B) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero;        \
+            pb0 = (okb && c_ < ncols) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;            \
+            pb1 = (okb && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero;    \
         }                                                                                              \
     }
 #define MFAC_GB_STORE(BUF_)                                                                            \
@@ -235,7 +249,7 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
     for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
-    const int nchunk = (B + KB - 1) / KB;
+    const int nchunk = (ncols + KB - 1) / KB;
     MFAC_GB_LOAD(0)
     MFAC_GB_STORE(0)
     __syncthreads();
@@ -265,6 +279,17 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
 #undef MFAC_GB_LOAD
 #undef MFAC_GB_STORE
     if (upper_wave) return;
+    if (nsplit > 1) {
+        double* out = part + ((int64_t)bl * nsplit + sp) * ntiles * (GT * GT) + (int64_t)tile * (GT * GT);
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    out[(wr * 32 + x * 16 + kl + 4 * r) * GT + wc * 64 + y * 16 + rl] = acc[x][y][r];
+        return;
+    }
     double* Ab = A + (int64_t)bl * mp * mp;
 #pragma unroll
     for (int x = 0; x < 2; ++x)
@@ -281,6 +306,28 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
                     Ab[(int64_t)row * mp + col] = v;
                 }
             }
+}
+
+// A_b (lower triangle of every tile the factorization reads) = sum over the
+// column splits of the partial tiles, in split order, plus mu on the diagonal
+// (identity on the padding rows). Grid (ntiles, nb).
+__global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __restrict__ part, int nsplit, int ntiles,
+                                                            int m, double mu, double* __restrict__ A, int mp) {
+    const int tile = blockIdx.x, bl = blockIdx.y;
+    int ti, tj;
+    tile_of(tile, ti, tj);
+    const double* src = part + (int64_t)bl * nsplit * ntiles * (GT * GT) + (int64_t)tile * (GT * GT);
+    const int64_t sstride = (int64_t)ntiles * (GT * GT);
+    double* Ab = A + (int64_t)bl * mp * mp;
+    for (int e = threadIdx.x; e < GT * GT; e += 256) {
+        const int rr = e / GT, cc = e % GT;
+        const int row = ti * GT + rr, col = tj * GT + cc;
+        if (row >= mp || col >= mp || (ti == tj && rr < cc)) continue;
+        double v = 0.0;
+        for (int s = 0; s < nsplit; ++s) v += src[s * sstride + e];
+        if (row == col) v += (row < m) ? mu : 1.0;
+        Ab[(int64_t)row * mp + col] = v;
+    }
 }
 
 }  // namespace
@@ -317,12 +364,45 @@ hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part
     return hipGetLastError();
 }
 
-hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb, double mu,
-                              double* A, int mp, hipStream_t st) {
+namespace {
+// Column splits of a batch of nb blocks: none when the batch has >= 1024
+// tiles; otherwise up to 2048 work-groups (four rounds of the 512 that are
+// resident at once, two per CU, without a nearly empty fifth), each split
+// >= 2048 columns (its fp64 partial tile stays small next to the operand
+// reads). kcols is a multiple of the 32-column stage, so every split starts
+// 16-byte aligned.
+int gram_blocks_splits(int nb, int mp, int B, int& ntiles, int& kcols) {
     const int T = (int)ceil_div(mp, GT);
-    const int ntiles = T * (T + 1) / 2;
-    hipLaunchKernelGGL(k_gram_blocks, dim3((unsigned)(ntiles * nb)), dim3(512), 0, st, G, m, d, B, b0, ntiles, mu, A,
-                       mp);
+    ntiles = T * (T + 1) / 2;
+    const int64_t wgs = (int64_t)nb * ntiles;
+    int64_t ns = 1;
+    if (wgs < 1024) {
+        ns = 2048 / wgs;
+        const int64_t maxs = B / 2048;
+        if (ns > maxs) ns = maxs;
+        if (ns < 1) ns = 1;
+    }
+    kcols = (int)round_up(ceil_div(B, ns), KB);
+    return (int)ceil_div(B, kcols);
+}
+}  // namespace
+
+int64_t gram_blocks_part_doubles(int nb, int mp, int B) {
+    int ntiles, kcols;
+    const int ns = gram_blocks_splits(nb, mp, B, ntiles, kcols);
+    return ns > 1 ? (int64_t)nb * ns * ntiles * (GT * GT) : 0;
+}
+
+hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb, double mu,
+                              double* A, int mp, double* part, hipStream_t st) {
+    int ntiles, kcols;
+    const int ns = gram_blocks_splits(nb, mp, B, ntiles, kcols);
+    hipLaunchKernelGGL(k_gram_blocks, dim3((unsigned)(ntiles * ns * nb)), dim3(512), 0, st, G, m, d, B, b0, ntiles,
+                       ns, kcols, mu, A, mp, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || ns == 1) return e;
+    hipLaunchKernelGGL(k_gram_blocks_reduce, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part, ns,
+                       ntiles, m, mu, A, mp);
     return hipGetLastError();
 }
 

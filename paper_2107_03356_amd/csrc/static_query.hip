@@ -13,6 +13,9 @@
 namespace mfac {
 namespace {
 
+// pass-1 partials for up to 4 vectors at the narrowest chunk width (512)
+int64_t static_query_main_doubles(int64_t d, int B, int m) { return (d / B) * ceil_div(B, 512) * (int64_t)m * 4; }
+
 // Pass 1: one work-group per column chunk of width 256*U inside one block.
 // part[c][i*NV + v] = sum_{j in chunk c} W[i, j] x_v[j].
 template <int NV, int U>
@@ -82,6 +85,22 @@ __global__ __launch_bounds__(256) void k_sq_reduce(const double* __restrict__ pa
     double s = 0.0;
     for (int cb = 0; cb < cpb; ++cb) s += part[((int64_t)b * cpb + cb) * mnv + t];
     coef[(int64_t)b * mnv + t] = (float)(scale * s);
+}
+
+// Wide blocks (many chunks per block): first sum segments of SEG chunks in
+// parallel, part2[(b*nseg + s)*mnv + t] = sum over chunks [s*SEG, (s+1)*SEG)
+// (fixed order); k_sq_reduce then sums the nseg segments of each block.
+constexpr int SEG = 64;
+__global__ __launch_bounds__(256) void k_sq_reduce_seg(const double* __restrict__ part, int cpb, int nseg, int mnv,
+                                                       double* __restrict__ part2) {
+    const int bs = blockIdx.y;  // block * nseg + segment
+    const int b = bs / nseg, sg = bs - (bs / nseg) * nseg;
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t >= mnv) return;
+    const int c0 = sg * SEG, c1 = (c0 + SEG) < cpb ? (c0 + SEG) : cpb;
+    double s = 0.0;
+    for (int cb = c0; cb < c1; ++cb) s += part[((int64_t)b * cpb + cb) * mnv + t];
+    part2[(int64_t)bs * mnv + t] = s;
 }
 
 // Pass 2: one wave per 256*U-column chunk of one block:
@@ -191,8 +210,20 @@ hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, f
                        part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_sq_reduce, dim3((unsigned)ceil_div(m * NV, 256), nblocks), dim3(256), 0, st, part, cpb,
-                       m * NV, pscale, coef);
+    if (cpb > SEG) {
+        // part2 follows the pass-1 partials (static_query_part_doubles holds both)
+        double* part2 = part + static_query_main_doubles(d, B, m);
+        const int nseg = (int)ceil_div(cpb, SEG);
+        hipLaunchKernelGGL(k_sq_reduce_seg, dim3((unsigned)ceil_div(m * NV, 256), (unsigned)(nblocks * nseg)),
+                           dim3(256), 0, st, part, cpb, nseg, m * NV, part2);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_sq_reduce, dim3((unsigned)ceil_div(m * NV, 256), nblocks), dim3(256), 0, st, part2,
+                           nseg, m * NV, pscale, coef);
+    } else {
+        hipLaunchKernelGGL(k_sq_reduce, dim3((unsigned)ceil_div(m * NV, 256), nblocks), dim3(256), 0, st, part,
+                           cpb, m * NV, pscale, coef);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int cpb2 = (int)ceil_div(B, 256 * U2);
@@ -205,8 +236,8 @@ hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, f
 }  // namespace
 
 int64_t static_query_part_doubles(int64_t d, int B, int m) {
-    // pass-1 partials for up to 4 vectors at the narrowest chunk width (512)
-    return (d / B) * ceil_div(B, 512) * (int64_t)m * 4;
+    // pass-1 partials, then the per-segment sums of wide blocks
+    return static_query_main_doubles(d, B, m) + (d / B) * ceil_div(ceil_div(B, 512), SEG) * (int64_t)m * 4;
 }
 
 hipError_t launch_static_ihvp(const float* W, int m, int64_t d, int B, int n, const float* X, float alpha,

@@ -62,6 +62,11 @@ WORKLOADS = {
     "static_d4.19m_b2048_m1024": Workload(
         "static_d4.19m_b2048_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
         dist="lognormal", block=2048, theta_std=0.05),
+    # the full-d static precompute (Section 3.1, a single block B = d) at the
+    # same size
+    "static_full_d4.19m_m1024": Workload(
+        "static_full_d4.19m_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
+        dist="lognormal", block=4_194_304, theta_std=0.05),
     # the optimizer loop on a CIFAR-shaped ResNet-20 (269,722 weights), batch 128,
     # window m = 512 (Section 4.2, Table 4 settings); random inputs and labels
     "optim_resnet20_cifar_b128_m512": Workload(

@@ -52,6 +52,10 @@ def _run(dev, G, B, lam, theta, keep):
     (300, 512, 3, 1e-4, None),     # padded to 320: uneven splits in the recursive factor
     (700, 2048, 2, 1e-4, None),    # padded to 704: 11 tiles, half tiles at several levels
     (1500, 512, 3, 1e-4, None),    # m > B and m > 1024: rank-deficient Gram, padded to 1536
+    (256, 65536, 1, 1e-4, None),   # B = d (full-d precompute): Gram columns split over 32 work-groups
+    (100, 20000, 1, 1e-3, None),   # B = d not a multiple of 32: 9 column splits, ragged last split
+    (1024, 16384, 2, 1e-4, None),  # two wide blocks at m = 1024: 8 splits of 36 tiles each
+    (64, 8192, 3, 1e-4, 2),        # split Gram in a batch of 2 blocks and a last batch of 1
 ])
 def test_static_small(dev, m, B, nb, lam, batch_cap, monkeypatch):
     if batch_cap:
@@ -113,6 +117,8 @@ def test_mask_edges_and_ties(dev, keep_frac):
     (100, 256, 6, 1e-3, False),
     (1024, 2048, 2, 1e-4, True),     # pruning block width and m, full-size entry scale
     (37, 100, 3, 1e-2, False),       # B not a multiple of the chunk widths, m padded
+    (64, 65536, 1, 1e-3, False),     # B = d: 128 pass-1 chunks per block, summed in 2 segments
+    (128, 262144, 1, 1e-4, False),   # B = d: segmented chunk sums for 1 and for 3 vectors
 ])
 def test_static_ihvp_element_and_obs_update(dev, m, B, nb, lam, scale_full):
     from paper_2107_03356_amd import StaticBlocks
@@ -133,6 +139,7 @@ def test_static_ihvp_element_and_obs_update(dev, m, B, nb, lam, scale_full):
     rng = np.random.default_rng(5)
     pairs = [(0, 0), (1, 2), (B - 1, 0), (B, B + 3), (wl.d - 1, wl.d - 2), (3, B + 3), (B // 2, B // 2)]
     pairs += [(int(i), int(i // B * B + rng.integers(0, B))) for i in rng.integers(0, wl.d, 20)]
+    pairs = [(i, j) for i, j in pairs if i < wl.d and j < wl.d]    # one block: no second block to pair with
     ij = torch.tensor(pairs, dtype=torch.int64)
     el = sb.element(ij).cpu().numpy()
     ref = np.array([ostatic.element(Gn, lam, B, i, j) for i, j in pairs])
