@@ -86,6 +86,7 @@ def test_tiny_init_equals_fill(dev):
     (40968, 1024, 1e-5, 8, "lognormal"),           # m = 1024 with 8 fused queries (ResNet18 recipe)
     (2048, 1, 1e-2, 1, "gauss"),                   # m = 1 (Sherman-Morrison)
     (5, 3, 1e-1, 1, "gauss"),                      # d smaller than one float4 group row
+    (8192, 4096, 1e-3, 1, "gauss"),                # m = 4096: 528 Gram tiles, six recursion levels
 ])
 def test_ragged_and_multitile_with_queries(dev, d, m, lam, q, dist):
     base = get_workload("dyn_resnet18_d11.2m_m1024_q8")

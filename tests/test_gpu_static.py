@@ -56,6 +56,7 @@ def _run(dev, G, B, lam, theta, keep):
     (100, 20000, 1, 1e-3, None),   # B = d not a multiple of 32: 9 column splits, ragged last split
     (1024, 16384, 2, 1e-4, None),  # two wide blocks at m = 1024: 8 splits of 36 tiles each
     (64, 8192, 3, 1e-4, 2),        # split Gram in a batch of 2 blocks and a last batch of 1
+    (8192, 1024, 2, 1e-3, None),   # the largest m (8192 > B): 2080 Gram tiles, seven recursion levels
 ])
 def test_static_small(dev, m, B, nb, lam, batch_cap, monkeypatch):
     if batch_cap:
