@@ -263,7 +263,15 @@ MFAC_API mfac_status mfac_window_init(mfac_window* out, int64_t d, int32_t m, do
                           : launch_fill_zero(w->G, w->nslab * (int64_t)m * SLAB, w->st);
         if (e != hipSuccess) rc = MFAC_EHIP;
     }
-    if (rc == MFAC_OK) rc = mfac_window_rebuild(w);
+    if (rc == MFAC_OK) {
+        if (G0) {
+            rc = mfac_window_rebuild(w);
+        } else {
+            // empty window: K = 0 without a Gram pass over the zero rows
+            if (launch_fill_zero((float*)w->K, 2 * (int64_t)m * m, w->st) != hipSuccess) rc = MFAC_EHIP;
+            if (rc == MFAC_OK) rc = window_factor(w, nullptr, 0, -1);
+        }
+    }
     if (rc != MFAC_OK) {
         free(w);
         return rc;
@@ -466,7 +474,7 @@ int static_batch(int64_t d, int B, int m) {
     if (b < 1) b = 1;
     if (b > 65535) b = 65535;
     if (b > nblocks) b = nblocks;
-    // equal batches (the last one at most one block smaller than the others)
+    // batches of equal size up to rounding (the last one may be smaller)
     const int64_t nbatch = ceil_div(nblocks, b);
     return (int)ceil_div(nblocks, nbatch);
 }

@@ -196,3 +196,33 @@ def test_nonfinite_gradient_latches_and_other_blocks_stay_exact(dev):
     dref = ostatic.inv_diag(G.numpy(), wl.lam, wl.block, blocks=[0, 2])
     got = np.concatenate([d64[:256], d64[512:]])
     assert rel_l2(got, dref) < 1e-11
+
+
+def test_stage_trace_counts_and_unchanged_results(dev, monkeypatch):
+    """MFAC_STATIC_TRACE: one interval per batch for the Gram, factor and W
+    stages and one per mask call; tracing leaves every output bit-identical."""
+    from paper_2107_03356_amd import StaticBlocks
+    monkeypatch.setenv("MFAC_STATIC_BATCH_BLOCKS", "2")
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=5 * 512, m=96, block=512, lam=1e-3, scale_d=512)
+    gs = GradientStream(wl, seed=13)
+    G = gs.rows(0, wl.m)
+    theta = gs.theta().to(dev)
+    say("static trace", wl.d, wl.m)
+    outs = []
+    for trace in (False, True):
+        sb = StaticBlocks(G.to(dev).contiguous(), wl.block, wl.lam, trace=trace)
+        d64 = sb.inv_diag(fp64=True)
+        mask, sc = sb.obs_mask(theta, wl.d // 2)
+        torch.cuda.synchronize()
+        assert sb.status() == 0
+        ms, cnt = sb.trace_read()
+        outs.append((d64.cpu().numpy(), mask.cpu().numpy(), sc.cpu().numpy(), list(ms), list(cnt)))
+        sb.close()
+    (d0, m0, s0, ms0, c0), (d1, m1, s1, ms1, c1) = outs
+    np.testing.assert_array_equal(d0, d1)
+    np.testing.assert_array_equal(m0, m1)
+    np.testing.assert_array_equal(s0, s1)
+    assert c0 == [0, 0, 0, 0] and ms0 == [0.0] * 4
+    assert c1 == [3, 3, 3, 1]                  # 5 blocks in batches of 2, 2, 1; one mask call
+    assert all(t > 0.0 for t in ms1)
