@@ -84,8 +84,8 @@ size_t mfac_window_storage_bytes(int64_t d, int32_t m);
 size_t mfac_window_workspace_bytes(int64_t d, int32_t m, int32_t max_queries);
 
 /* Create a window handle.
- *   d >= 1, m >= 1, lambda > 0 finite (kept in fp64: the coefficient phase
- *   runs in fp64), 0 <= max_queries <= 16,
+ *   1 <= d <= 2^34, m >= 1, lambda > 0 finite (kept in fp64: the
+ *   coefficient phase runs in fp64), 0 <= max_queries <= 16,
  *   m * (max_queries + 1) <= 16384.
  *   storage:   >= mfac_window_storage_bytes(d, m), 256-byte aligned.
  *   workspace: >= mfac_window_workspace_bytes(d, m, max_queries), 256-byte aligned.
@@ -195,8 +195,8 @@ size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m);
  * diag(F_b^-1) = (1 - sum_i W_b[i,:]^2) / lambda is formed in fp64 from the
  * unrounded W and kept in the workspace.
  * Requirements: 1 <= m <= 8192, 4 <= block, block % 4 == 0,
- * d % block == 0, lambda > 0 finite, G 16-byte aligned, workspace 256-byte
- * aligned, flags a combination of MFAC_STATIC_* bits. */
+ * d % block == 0, d <= 2^32 - 256, lambda > 0 finite, G 16-byte aligned,
+ * workspace 256-byte aligned, flags a combination of MFAC_STATIC_* bits. */
 mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m,
                                    double lambda, float* G, void* workspace,
                                    size_t workspace_bytes, uint32_t flags, hipStream_t stream);

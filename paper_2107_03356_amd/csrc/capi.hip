@@ -117,8 +117,9 @@ size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
 }
 
 bool window_sizes_ok(int64_t d, int32_t m, int32_t max_q) {
+    // d <= 2^34: the row copy kernels launch d/4 work-items (a 32-bit count)
     return d >= 1 && m >= 1 && max_q >= 0 && max_q <= MAX_QUERIES && (int64_t)m * (max_q + 1) <= MAX_MNV &&
-           d <= (int64_t(1) << 40);
+           d <= (int64_t(1) << 34);
 }
 
 #define HIPCHK(x)                                  \
@@ -455,8 +456,10 @@ MFAC_API mfac_status mfac_window_destroy(mfac_window w) {
 namespace {
 
 bool static_sizes_ok(int64_t d, int32_t B, int32_t m) {
-    return d >= 1 && B >= 4 && m >= 1 && (B % 4) == 0 && d % B == 0 && m <= 8192 && d <= (int64_t(1) << 40) &&
-           d / B <= (int64_t(1) << 30);
+    // d <= 2^32 - 256: the element-wise kernels launch one work-item per
+    // coordinate (a 32-bit count)
+    return d >= 1 && B >= 4 && m >= 1 && (B % 4) == 0 && d % B == 0 && m <= 8192 &&
+           d <= (int64_t(1) << 32) - 256;
 }
 
 int static_batch(int64_t d, int B, int m) {

@@ -172,25 +172,26 @@ __global__ __launch_bounds__(256) void k_static_element(const float* __restrict_
                                                         int64_t nq, const int64_t* __restrict__ ij, double inv_lam,
                                                         double* __restrict__ out, int* __restrict__ err) {
     const int lane = threadIdx.x & 63;
-    const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (q >= nq) return;
-    const int64_t i = ij[2 * q], j = ij[2 * q + 1];
-    if (i < 0 || i >= d || j < 0 || j >= d) {
-        if (lane == 0) {
-            out[q] = __longlong_as_double(0x7ff8000000000000ll);
-            atomicOr(err, 32);
+    // one wave per query, grid-strided (the grid is capped)
+    for (int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); q < nq; q += (int64_t)gridDim.x * 4) {
+        const int64_t i = ij[2 * q], j = ij[2 * q + 1];
+        if (i < 0 || i >= d || j < 0 || j >= d) {
+            if (lane == 0) {
+                out[q] = __longlong_as_double(0x7ff8000000000000ll);
+                atomicOr(err, 32);
+            }
+            continue;
         }
-        return;
-    }
-    if (i / B != j / B) {
-        if (lane == 0) out[q] = 0.0;
-        return;
-    }
-    double s = 0.0;
-    for (int k = lane; k < m; k += 64) s += (double)W[(int64_t)k * d + i] * (double)W[(int64_t)k * d + j];
+        if (i / B != j / B) {
+            if (lane == 0) out[q] = 0.0;
+            continue;
+        }
+        double s = 0.0;
+        for (int k = lane; k < m; k += 64) s += (double)W[(int64_t)k * d + i] * (double)W[(int64_t)k * d + j];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-    if (lane == 0) out[q] = ((i == j ? 1.0 : 0.0) - s) * inv_lam;
+        for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+        if (lane == 0) out[q] = ((i == j ? 1.0 : 0.0) - s) * inv_lam;
+    }
 }
 
 template <int NV>
@@ -260,7 +261,9 @@ hipError_t launch_obs_x(const float* theta, const uint8_t* keep, const double* d
 hipError_t launch_static_element(const float* W, int m, int64_t d, int B, int64_t nq, const int64_t* ij, double lam,
                                  double* out, int* err, hipStream_t st) {
     if (nq <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_static_element, dim3((unsigned)ceil_div(nq, 4)), dim3(256), 0, st, W, m, d, B, nq, ij,
+    int64_t grid = ceil_div(nq, 4);
+    if (grid > 65536) grid = 65536;
+    hipLaunchKernelGGL(k_static_element, dim3((unsigned)grid), dim3(256), 0, st, W, m, d, B, nq, ij,
                        1.0 / lam, out, err);
     return hipGetLastError();
 }

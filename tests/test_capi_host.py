@@ -58,6 +58,7 @@ def _init(**kw):
     (dict(lam=float("nan")), B.MFAC_EINVAL),
     (dict(lam=float("inf")), B.MFAC_EINVAL),
     (dict(q=17), B.MFAC_EINVAL),
+    (dict(d=(1 << 34) + 4), B.MFAC_EINVAL),          # past the 32-bit work-item count of d/4 launches
     (dict(storage=None), B.MFAC_EINVAL),
     (dict(ws=None), B.MFAC_EINVAL),
     (dict(storage=256 * 1000 + 4), B.MFAC_EINVAL),     # not 256-byte aligned
@@ -92,6 +93,7 @@ def test_null_handles_and_out_pointers():
     ((4096, 256, 0, 1e-4), B.MFAC_EINVAL),
     ((4096, 256, 64, 0.0), B.MFAC_EINVAL),
     ((4096, 256, 64, float("nan")), B.MFAC_EINVAL),
+    (((1 << 32), 1 << 20, 64, 1e-4), B.MFAC_EINVAL),   # d past 2^32 - 256 (one work-item per coordinate)
 ])
 def test_static_precompute_rejects_on_host(args, expect):
     lib = B.load()

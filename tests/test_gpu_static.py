@@ -198,6 +198,64 @@ def test_nonfinite_gradient_latches_and_other_blocks_stay_exact(dev):
     assert rel_l2(got, dref) < 1e-11
 
 
+def test_many_element_queries(dev):
+    """300,000 element queries (more than one query per wave of the capped
+    grid) against dense per-block inverses."""
+    from paper_2107_03356_amd import StaticBlocks
+    from oracle import bruteforce
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=4 * 256, m=16, block=256, lam=1e-3, scale_d=256)
+    gs = GradientStream(wl, seed=44)
+    G = gs.rows(0, wl.m)
+    say("static many element queries")
+    sb = StaticBlocks(G.to(dev).contiguous(), wl.block, wl.lam)
+    rng = np.random.default_rng(8)
+    nq = 300_000
+    i = rng.integers(0, wl.d, nq)
+    same = rng.random(nq) < 0.8
+    j = np.where(same, i // wl.block * wl.block + rng.integers(0, wl.block, nq), rng.integers(0, wl.d, nq))
+    ij = torch.tensor(np.stack([i, j], axis=1), dtype=torch.int64)
+    el = sb.element(ij).cpu().numpy()
+    assert sb.status() == 0
+    Gn = G.numpy()
+    inv = [np.linalg.inv(bruteforce.fisher(Gn[:, b * wl.block:(b + 1) * wl.block], wl.lam, wl.m))
+           for b in range(wl.d // wl.block)]
+    bi, bj = i // wl.block, j // wl.block
+    ref = np.zeros(nq)
+    for b in range(wl.d // wl.block):
+        sel = (bi == b) & (bj == b)
+        ref[sel] = inv[b][i[sel] - b * wl.block, j[sel] - b * wl.block]
+    assert np.max(np.abs(el - ref)) < 1e-5 * np.abs(ref).max()
+    assert np.all(el[bi != bj] == 0.0)
+
+
+def test_nonfinite_theta_latches_and_mask_keeps_its_count(dev):
+    """Non-finite weights latch MFAC_ENONFINITE from the score stage; the mask
+    still keeps exactly `keep` coordinates, and the finite coordinates' scores
+    match the oracle."""
+    from paper_2107_03356_amd import MFAC_ENONFINITE, StaticBlocks
+    base = get_workload("static_d4.19m_b2048_m1024")
+    wl = base.scaled(d=4 * 256, m=32, block=256, lam=1e-3, scale_d=256)
+    gs = GradientStream(wl, seed=43)
+    G = gs.rows(0, wl.m)
+    theta = gs.theta()
+    theta[5] = float("nan")
+    theta[300] = float("inf")
+    theta[301] = float("-inf")
+    say("static nonfinite theta")
+    sb = StaticBlocks(G.to(dev).contiguous(), wl.block, wl.lam)
+    assert sb.status() == 0
+    keep = wl.d // 2
+    mask, sc = sb.obs_mask(theta.to(dev), keep)
+    mk, sc = mask.cpu().numpy(), sc.cpu().numpy()
+    assert sb.status() == MFAC_ENONFINITE
+    assert sb.status() == 0
+    assert int(mk.sum()) == keep
+    fin = np.isfinite(theta.numpy())
+    sref = omask.scores(theta.numpy(), ostatic.inv_diag(G.numpy(), wl.lam, wl.block))
+    assert rel_l2(sc[fin], sref[fin]) < 1e-11
+
+
 def test_stage_trace_counts_and_unchanged_results(dev, monkeypatch):
     """MFAC_STATIC_TRACE: one interval per batch for the Gram, factor and W
     stages and one per mask call; tracing leaves every output bit-identical."""
