@@ -105,6 +105,16 @@ def test_d1m_m256_full_size(dev):
     assert max(errs) < REL_TOL
 
 
+def test_largest_window_m16384(dev):
+    """The largest window the library accepts without queries (m = 16384: the
+    pass-1 row sums fill 64 KB of LDS), over a short d; two sliding steps."""
+    base = get_workload("dyn_tiny_d4096_m16")
+    wl = base.scaled(d=2048, m=16384, lam=1e-2, fill_by_replace=False)
+    say("largest window m16384")
+    _, _, errs, _ = _sliding(dev, wl, seed=5, nsteps=2)
+    assert max(errs) < REL_TOL
+
+
 def test_correlated_rows_resnet50_recipe_small(dev):
     """10% correlated rows (ResNet50 recipe) at reduced d, full m = 1024."""
     base = get_workload("dyn_resnet50_d25.6m_m1024")
