@@ -295,12 +295,66 @@ def resnet20(num_classes=10):
     return Net()
 
 
+def wide_resnet(depth=40, k=2, num_classes=100):
+    """CIFAR Wide ResNet WRN-depth-k: a 3x3 stem with 16 channels, three groups
+    of (depth - 4) / 6 pre-activation basic blocks with 16k, 32k, 64k channels
+    (strides 1, 2, 2; 1x1 projection shortcuts where the shape changes), then
+    BN-ReLU, global average pooling and a linear classifier. WRN-40-2 on
+    CIFAR-100: 2,255,156 weights."""
+    import torch
+    import torch.nn as nn
+    import torch.nn.functional as F
+
+    class Block(nn.Module):
+        def __init__(self, cin, cout, stride):
+            super().__init__()
+            self.b1 = nn.BatchNorm2d(cin)
+            self.c1 = nn.Conv2d(cin, cout, 3, stride, 1, bias=False)
+            self.b2 = nn.BatchNorm2d(cout)
+            self.c2 = nn.Conv2d(cout, cout, 3, 1, 1, bias=False)
+            self.proj = nn.Conv2d(cin, cout, 1, stride, 0, bias=False) if (cin != cout or stride != 1) else None
+
+        def forward(self, x):
+            o = F.relu(self.b1(x))
+            sc = self.proj(o) if self.proj is not None else x
+            o = self.c1(o)
+            o = self.c2(F.relu(self.b2(o)))
+            return o + sc
+
+    class Net(nn.Module):
+        def __init__(self):
+            super().__init__()
+            n = (depth - 4) // 6
+            self.stem = nn.Conv2d(3, 16, 3, 1, 1, bias=False)
+            layers, cin = [], 16
+            for cout, stride in ((16 * k, 1), (32 * k, 2), (64 * k, 2)):
+                for i in range(n):
+                    layers.append(Block(cin, cout, stride if i == 0 else 1))
+                    cin = cout
+            self.layers = nn.Sequential(*layers)
+            self.bn = nn.BatchNorm2d(cin)
+            self.fc = nn.Linear(cin, num_classes)
+
+        def forward(self, x):
+            x = F.relu(self.bn(self.layers(self.stem(x))))
+            return self.fc(torch.flatten(F.adaptive_avg_pool2d(x, 1), 1))
+
+    return Net()
+
+
+OPTIM_MODELS = {
+    # workload model key -> (builder, classes, description)
+    "resnet20": (lambda: resnet20(10), 10, "CIFAR-shaped ResNet-20"),
+    "wrn40_2": (lambda: wide_resnet(40, 2, 100), 100, "CIFAR-100-shaped WRN-40-2"),
+}
+
+
 def bench_optimizer(args, wl, dev):
     """Training steps (forward + backward + optimizer) of a CIFAR-shaped
-    ResNet-20 with M-FAC (window m) and, in the same process, with SGD
-    (momentum 0.9): M-FAC steps/s and its overhead over SGD (Section 4.2,
-    Table 4's metric). Random-init weights, random inputs and labels resident
-    in HBM."""
+    network (ResNet-20 or WRN-40-2) with M-FAC (window m) and, in the same
+    process, with SGD (momentum 0.9): M-FAC steps/s and its overhead over SGD
+    (Section 4.2, Table 4's metric). Random-init weights, random inputs and
+    labels resident in HBM."""
     import torch
 
     import paper_2107_03356_amd as P
@@ -312,13 +366,14 @@ def bench_optimizer(args, wl, dev):
     g = torch.Generator(device="cpu")
     g.manual_seed(args.seed)
     nb = 16
+    build, ncls, desc = OPTIM_MODELS[wl.model]
     xs = torch.randn((nb, wl.batch, 3, 32, 32), generator=g).to(dev)
-    ys = torch.randint(0, 10, (nb, wl.batch), generator=g).to(dev)
+    ys = torch.randint(0, ncls, (nb, wl.batch), generator=g).to(dev)
     lossf = torch.nn.CrossEntropyLoss()
 
     def make(opt_name):
         torch.manual_seed(args.seed)
-        net = resnet20().to(dev)
+        net = build().to(dev)
         d = sum(p.numel() for p in net.parameters())
         assert d == wl.d, d
         if opt_name == "sgd":
@@ -363,11 +418,11 @@ def bench_optimizer(args, wl, dev):
     gbs2 = b2 / (avg[2] * 1e-3) / 1e9
     kname, achieved = ("k_pass1", gbs1) if avg[0] >= avg[2] else ("k_pass2", gbs2)
     out = {
-        "metric": "M-FAC training steps/s on a CIFAR-shaped ResNet-20, batch 128, m = 512 (overhead over SGD)",
+        "metric": f"M-FAC training steps/s on a {desc}, batch {wl.batch}, m = {wl.m} (overhead over SGD)",
         "value": 1000.0 / res["mfac"], "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": res["mfac"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": wl.name, "model": "resnet20 (random init)", "d": wl.d, "m": wl.m,
+        "config": {"workload": wl.name, "model": f"{wl.model} (random init)", "d": wl.d, "m": wl.m,
                    "global_batch": wl.batch, "image": [3, 32, 32], "damp": wl.lam},
         "sgd_ms_per_step": res["sgd"],
         "overhead_over_sgd": res["mfac"] / res["sgd"],
@@ -428,14 +483,16 @@ def cpu_optimizer_baseline(wl, seed, nsteps):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         cores = os.cpu_count()
-    gs = GradientStream(wl, seed=seed)
+    from oracle.dynamic import WindowOracle
+
+    gs = GradientStream(wl, seed=seed, device="cuda")   # rows drawn on the GPU, copied to the host
     orc = MFACOracle(wl.d, wl.m, wl.lam)
-    for r in range(wl.m):
-        orc.window.replace(r, gs.row(r).numpy())
+    orc.window = WindowOracle(wl.d, wl.m, wl.lam, G0=gs.window().cpu().numpy())   # a full window
+    steps = [gs.step_row(t).cpu().numpy() for t in range(nsteps)]
     w = np.zeros(wl.d)
     t0 = time.perf_counter()
     for t in range(nsteps):
-        w, _ = orc.step(w, gs.step_row(t).numpy(), 1e-3)
+        w, _ = orc.step(w, steps[t], 1e-3)
     sec = (time.perf_counter() - t0) / nsteps
     return {"value": 1.0 / sec, "unit": "optimizer steps/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{nsteps} oracle M-FAC steps (fp64 window insert + F^-1 g) at d={wl.d}, m={wl.m}, "

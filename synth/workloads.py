@@ -35,6 +35,7 @@ class Workload:
     scale_d: int = 0     # d in the 1/sqrt(d) entry scale (0: the workload's own d);
                          # reduced-size parity cases keep the full-size scale
     batch: int = 0       # optim: mini-batch size of the model's synthetic batches
+    model: str = ""      # optim: the network trained
 
     def scaled(self, **kw) -> "Workload":
         """Same recipe at another size (parity cases the oracle finishes in seconds)."""
@@ -71,7 +72,12 @@ WORKLOADS = {
     # window m = 512 (Section 4.2, Table 4 settings); random inputs and labels
     "optim_resnet20_cifar_b128_m512": Workload(
         "optim_resnet20_cifar_b128_m512", "optim", d=269_722, m=512, lam=1e-4,
-        dist="gauss", steps=100, batch=128),
+        dist="gauss", steps=100, batch=128, model="resnet20"),
+    # the same loop on a CIFAR-100-shaped WRN-40-2 (2,255,156 weights; Section 4.2,
+    # Table 4's wide-ResNet runs)
+    "optim_wrn40_2_cifar100_b128_m512": Workload(
+        "optim_wrn40_2_cifar100_b128_m512", "optim", d=2_255_156, m=512, lam=1e-4,
+        dist="gauss", steps=50, batch=128, model="wrn40_2"),
 }
 
 HEADLINE = "dyn_resnet50_d25.6m_m1024"

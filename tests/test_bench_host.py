@@ -18,12 +18,14 @@ def test_more_than_one_gpu_exits_with_a_message():
     assert r.stdout == ""
 
 
-def test_resnet20_has_the_workload_size():
+def test_optimizer_models_have_the_workload_sizes():
     sys.path.insert(0, ROOT)
     import bench
-    from synth import get_workload
-    net = bench.resnet20()
-    assert sum(p.numel() for p in net.parameters()) == get_workload("optim_resnet20_cifar_b128_m512").d
+    from synth import WORKLOADS
+    for wl in WORKLOADS.values():
+        if wl.kind == "optim":
+            net = bench.OPTIM_MODELS[wl.model][0]()
+            assert sum(p.numel() for p in net.parameters()) == wl.d, wl.name
 
 
 def test_pass_bytes_match_the_survey_budget():
