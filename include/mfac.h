@@ -201,9 +201,37 @@ mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, i
                                    double lambda, float* G, void* workspace,
                                    size_t workspace_bytes, uint32_t flags, hipStream_t stream);
 
-/* flags of mfac_static_precompute */
+/* flags of mfac_static_precompute and mfac_static_precompute_paged */
 #define MFAC_STATIC_TRACE 1u /* record HIP events around the precompute's stages and
                                 mfac_obs_mask; read with mfac_static_trace_read */
+
+/* Host-paged static precompute, for a G larger than the device should hold
+ * (Appendix C, swapping gradient blocks between host and GPU memory; here
+ * the pages are column ranges, which the block structure makes independent).
+ * Computes the same W (written back over G on the host), inverse diagonal
+ * and handle as mfac_static_precompute.
+ *   G_host:    m x d row-major fp32 in pinned host memory (hipHostMalloc or
+ *              a pinned torch tensor), 16-byte aligned; overwritten by W.
+ *              Pageable memory is rejected (MFAC_EINVAL).
+ *   page_cols: columns per page, a multiple of 4 and, when block < d, of
+ *              block (a page holds whole blocks, at most 65535); values above
+ *              d mean d. Two device page buffers of m * page_cols floats
+ *              live in the workspace.
+ * block < d: one sweep; each page is uploaded, its blocks go through Gram,
+ * factor and W, and W is downloaded (G crosses the host link twice).
+ * block == d: the one block's Gram is summed page by page, factored, and a
+ * second sweep forms W page by page (G crosses three times).
+ * Uploads and downloads run on two streams the handle creates (default
+ * priority) and overlap each other and the kernels on `stream`, which waits
+ * for the last download before any later call on the handle. The queries
+ * (mfac_static_ihvp, mfac_static_element, mfac_obs_update) of a paged
+ * handle read W directly from the pinned host buffer over the host link;
+ * mfac_inv_diag, mfac_inv_diag64 and mfac_obs_mask use the device diagonal.
+ * Other requirements as mfac_static_precompute. */
+size_t mfac_static_paged_workspace_bytes(int64_t d, int32_t block, int32_t m, int64_t page_cols);
+mfac_status mfac_static_precompute_paged(mfac_static* out, int64_t d, int32_t block, int32_t m,
+                                         double lambda, float* G_host, int64_t page_cols, void* workspace,
+                                         size_t workspace_bytes, uint32_t flags, hipStream_t stream);
 
 /* Per-stage device time of a static handle created with MFAC_STATIC_TRACE,
  * since creation or the last read (synchronises the stream). ms_out and

@@ -50,6 +50,9 @@ SIGNATURES = {
     "mfac_window_destroy": (_c.c_int, [_VP]),
     "mfac_static_workspace_bytes": (_SZ, [_I64, _I32, _I32]),
     "mfac_static_precompute": (_c.c_int, [_PVP, _I64, _I32, _I32, _F64, _VP, _VP, _SZ, _c.c_uint32, _VP]),
+    "mfac_static_paged_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I64]),
+    "mfac_static_precompute_paged": (_c.c_int, [_PVP, _I64, _I32, _I32, _F64, _VP, _I64, _VP, _SZ, _c.c_uint32,
+                                                _VP]),
     "mfac_static_trace_read": (_c.c_int, [_VP, _c.POINTER(_F64), _c.POINTER(_I64)]),
     "mfac_inv_diag": (_c.c_int, [_VP, _VP]),
     "mfac_inv_diag64": (_c.c_int, [_VP, _VP]),
@@ -241,28 +244,45 @@ class Window:
 class StaticBlocks:
     """Static block-wise precompute over a caller's m x d gradient matrix.
 
-    G is overwritten in place by W (W_b = R_b^-1 G_b per block).
+    G is overwritten in place by W (W_b = R_b^-1 G_b per block). G is either a
+    device tensor, or (``page_cols`` given) a pinned host tensor
+    (``pin_memory=True``) larger than the device should hold: it then passes
+    through the device in pages of ``page_cols`` columns (whole blocks when
+    block < d), and the queries read W from host memory.
     """
 
-    def __init__(self, G, block, lam, stream=None, trace=False):
+    def __init__(self, G, block, lam, stream=None, trace=False, page_cols=None, device=None):
         import torch
         self.torch = torch
         assert G.dtype == torch.float32 and G.is_contiguous() and G.dim() == 2
         self.G = G
         self.m, self.d = G.shape
         self.block, self.lam = int(block), float(lam)
-        self.device = G.device
         lib = load()
-        wb = lib.mfac_static_workspace_bytes(self.d, self.block, self.m)
-        if wb == 0:
-            raise MfacError("mfac_static_workspace_bytes", MFAC_EINVAL)
-        self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
-        self.stream = _stream_handle(torch, self.device, stream)
-        h = ctypes.c_void_p()
         flags = MFAC_STATIC_TRACE if trace else 0
-        st = lib.mfac_static_precompute(ctypes.byref(h), self.d, self.block, self.m, self.lam, _ptr(G),
-                                        _ptr(self.workspace), wb, flags, self.stream)
-        _check("mfac_static_precompute", st)
+        h = ctypes.c_void_p()
+        if page_cols is None:
+            self.device = G.device
+            wb = lib.mfac_static_workspace_bytes(self.d, self.block, self.m)
+            if wb == 0:
+                raise MfacError("mfac_static_workspace_bytes", MFAC_EINVAL)
+            self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
+            self.stream = _stream_handle(torch, self.device, stream)
+            st = lib.mfac_static_precompute(ctypes.byref(h), self.d, self.block, self.m, self.lam, _ptr(G),
+                                            _ptr(self.workspace), wb, flags, self.stream)
+            _check("mfac_static_precompute", st)
+        else:
+            if G.device.type != "cpu" or not G.is_pinned():
+                raise ValueError("StaticBlocks: a paged G must be a pinned host tensor (pin_memory=True)")
+            self.device = torch.device(device if device is not None else "cuda")
+            wb = lib.mfac_static_paged_workspace_bytes(self.d, self.block, self.m, int(page_cols))
+            if wb == 0:
+                raise MfacError("mfac_static_paged_workspace_bytes", MFAC_EINVAL)
+            self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
+            self.stream = _stream_handle(torch, self.device, stream)
+            st = lib.mfac_static_precompute_paged(ctypes.byref(h), self.d, self.block, self.m, self.lam, _ptr(G),
+                                                  int(page_cols), _ptr(self.workspace), wb, flags, self.stream)
+            _check("mfac_static_precompute_paged", st)
         self.handle = h
 
     def trace_read(self):

@@ -82,6 +82,13 @@ struct mfac_static_s {
     bool trace;
     std::vector<mfac_window_s::Mark>* marks;
     hipEvent_t open_ev;
+    // host-paged precompute: G lives in pinned host memory (G above is its
+    // device-visible address), pages of it pass through two device buffers
+    bool paged;
+    float* Ghost;
+    float* page[2];
+    hipStream_t up, down;  // host-to-device and device-to-host copy streams
+    hipEvent_t pev[9];     // fork, factor done, join, uploaded[2], computed[2], downloaded[2]
 };
 
 namespace {
@@ -521,6 +528,23 @@ size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
     return c.off;
 }
 
+// Frees the host-side handle: trace events, and for a paged handle its copy
+// streams (after their work has finished) and events.
+void static_release(mfac_static_s* s) {
+    if (s->up) {
+        (void)hipStreamSynchronize(s->up);
+        (void)hipStreamDestroy(s->up);
+    }
+    if (s->down) {
+        (void)hipStreamSynchronize(s->down);
+        (void)hipStreamDestroy(s->down);
+    }
+    for (int i = 0; i < 9; ++i)
+        if (s->pev[i]) (void)hipEventDestroy(s->pev[i]);
+    marks_free(s);
+    free(s);
+}
+
 }  // namespace
 
 MFAC_API size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m) {
@@ -557,8 +581,7 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
     const double mu = (double)m * lambda;
     auto fail = [&]() {
         (void)hipStreamSynchronize(s->st);
-        marks_free(s);
-        free(s);
+        static_release(s);
         return MFAC_EHIP;
     };
     if (launch_fill_zero((float*)s->err, 1, s->st) != hipSuccess) return fail();
@@ -652,7 +675,223 @@ MFAC_API mfac_status mfac_static_status(mfac_static s) {
 
 MFAC_API mfac_status mfac_static_destroy(mfac_static s) {
     if (!s) return MFAC_OK;
-    marks_free(s);
-    free(s);
+    static_release(s);
+    return MFAC_OK;
+}
+
+// ====================================================================== paged static
+
+namespace {
+
+// Pages of a host-resident G: pc columns each (whole blocks when B < d, any
+// multiple of 4 when the single block spans d), pb blocks per page.
+struct PagedPlan {
+    int64_t pc, npages;
+    int pb;
+};
+
+bool paged_plan(int64_t d, int32_t B, int32_t m, int64_t page_cols, PagedPlan& pl) {
+    if (!static_sizes_ok(d, B, m) || page_cols < 4 || page_cols % 4 != 0) return false;
+    const int64_t pc = page_cols < d ? page_cols : d;
+    if (pc > (int64_t(1) << 30)) return false;  // kernels take a page's width as int
+    if (B < d) {
+        if (pc % B != 0 || pc / B > 65535) return false;
+        pl.pb = (int)(pc / B);
+    } else {
+        pl.pb = 1;
+    }
+    pl.pc = pc;
+    pl.npages = ceil_div(d, pc);
+    return true;
+}
+
+template <typename S>
+size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* base, S* s) {
+    const int mp = padded_m(m);
+    const int64_t nb_last = B < d ? (d - (pl.npages - 1) * pl.pc) / B : 1;
+    const int wide = B < d ? B : (int)pl.pc;  // block width the page's Gram sees
+    const int64_t pa = gram_blocks_part_doubles(pl.pb, mp, wide), pb2 = gram_blocks_part_doubles((int)nb_last, mp, wide);
+    Carve c{base};
+    int* err = c.take<int>(64);
+    double* diag = c.take<double>((size_t)d);
+    double* scores = c.take<double>((size_t)d);
+    char* sel = c.take<char>((size_t)select_scratch_bytes(d));
+    double* A = c.take<double>((size_t)pl.pb * mp * mp);
+    double* Linv = c.take<double>((size_t)pl.pb * mp * mp);
+    double* gpart = c.take<double>((size_t)(pa > pb2 ? pa : pb2));
+    double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
+    float* qcoef = c.take<float>((size_t)(d / B) * m * 4);
+    float* xobs = c.take<float>((size_t)d);
+    float* p0 = c.take<float>((size_t)m * pl.pc);
+    float* p1 = c.take<float>((size_t)m * pl.pc);
+    if (s) {
+        s->err = err;
+        s->diag = diag;
+        s->scores = scores;
+        s->sel = select_scratch_carve(sel, d);
+        s->A = A;
+        s->Linv = Linv;
+        s->gpart = gpart;
+        s->qpart = qpart;
+        s->qcoef = qcoef;
+        s->xobs = xobs;
+        s->page[0] = p0;
+        s->page[1] = p1;
+        s->batch = pl.pb;
+    }
+    return c.off;
+}
+
+#define PCHK(x)                              \
+    do {                                     \
+        if ((x) != hipSuccess) return false; \
+    } while (0)
+
+// The page pipeline. Copies run on their own streams (uploads and downloads
+// overlap each other and the kernels); the kernels run in order on the
+// handle's stream; two device buffers alternate between pages, each reused
+// once the previous page in it has been downloaded (or, in a Gram-only
+// sweep, consumed).
+bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
+    const int64_t d = s->d;
+    const int m = s->m, B = s->B, mp = s->mp;
+    const int64_t bstride = (int64_t)mp * mp;
+    hipStream_t st = s->st;
+    hipEvent_t* E = s->pev;  // 0 fork, 1 factor done, 2 join, 3+b uploaded, 5+b computed, 7+b downloaded
+    auto cols = [&](int64_t p, int64_t& c0) {
+        c0 = p * pl.pc;
+        return (d - c0) < pl.pc ? (d - c0) : pl.pc;
+    };
+    auto upload = [&](int64_t p, int b, hipEvent_t after) {
+        int64_t c0;
+        const int64_t nc = cols(p, c0);
+        if (after) PCHK(hipStreamWaitEvent(s->up, after, 0));
+        PCHK(hipMemcpy2DAsync(s->page[b], (size_t)pl.pc * 4, s->Ghost + c0, (size_t)d * 4, (size_t)nc * 4,
+                              (size_t)m, hipMemcpyHostToDevice, s->up));
+        PCHK(hipEventRecord(E[3 + b], s->up));
+        PCHK(hipStreamWaitEvent(st, E[3 + b], 0));
+        return true;
+    };
+    auto download = [&](int64_t p, int b) {
+        int64_t c0;
+        const int64_t nc = cols(p, c0);
+        PCHK(hipEventRecord(E[5 + b], st));
+        PCHK(hipStreamWaitEvent(s->down, E[5 + b], 0));
+        PCHK(hipMemcpy2DAsync(s->Ghost + c0, (size_t)d * 4, s->page[b], (size_t)pl.pc * 4, (size_t)nc * 4,
+                              (size_t)m, hipMemcpyDeviceToHost, s->down));
+        PCHK(hipEventRecord(E[7 + b], s->down));
+        return true;
+    };
+    PCHK(launch_fill_zero((float*)s->err, 1, st));
+    PCHK(hipEventRecord(E[0], st));
+    PCHK(hipStreamWaitEvent(s->up, E[0], 0));
+    PCHK(hipStreamWaitEvent(s->down, E[0], 0));
+    if (B < d) {
+        // whole blocks per page: Gram, factor, W and diagonal, then back to the host
+        for (int64_t p = 0; p < pl.npages; ++p) {
+            const int b = (int)(p & 1);
+            int64_t c0;
+            const int nbp = (int)(cols(p, c0) / B);
+            if (!upload(p, b, p >= 2 ? E[7 + b] : nullptr)) return false;
+            PCHK(mark_begin(s));
+            PCHK(launch_gram_blocks(s->page[b], m, pl.pc, B, 0, nbp, mu, s->A, mp, s->gpart, st));
+            PCHK(mark_end(s, 0));
+            PCHK(mark_begin(s));
+            PCHK(launch_factor_invert(s->A, s->Linv, mp, nbp, bstride, s->err, st));
+            PCHK(mark_end(s, 1));
+            PCHK(mark_begin(s));
+            PCHK(launch_trmm_diag(s->Linv, mp, bstride, s->page[b], m, pl.pc, B, 0, nbp, s->lambda, s->diag + c0, st));
+            PCHK(mark_end(s, 2));
+            if (!download(p, b)) return false;
+        }
+    } else {
+        // one block over all pages: its Gram summed page by page, the factor,
+        // then a second sweep for W and the diagonal
+        for (int64_t p = 0; p < pl.npages; ++p) {
+            const int b = (int)(p & 1);
+            int64_t c0;
+            const int nc = (int)cols(p, c0);
+            if (!upload(p, b, p >= 2 ? E[5 + b] : nullptr)) return false;
+            PCHK(mark_begin(s));
+            PCHK(launch_gram_blocks(s->page[b], m, pl.pc, nc, 0, 1, mu, s->A, mp, s->gpart, st, p > 0));
+            PCHK(mark_end(s, 0));
+            PCHK(hipEventRecord(E[5 + b], st));
+        }
+        PCHK(mark_begin(s));
+        PCHK(launch_factor_invert(s->A, s->Linv, mp, 1, bstride, s->err, st));
+        PCHK(mark_end(s, 1));
+        PCHK(hipEventRecord(E[1], st));
+        PCHK(hipStreamWaitEvent(s->up, E[1], 0));
+        for (int64_t p = 0; p < pl.npages; ++p) {
+            const int b = (int)(p & 1);
+            int64_t c0;
+            const int nc = (int)cols(p, c0);
+            if (!upload(p, b, p >= 2 ? E[7 + b] : nullptr)) return false;
+            PCHK(mark_begin(s));
+            PCHK(launch_trmm_diag(s->Linv, mp, bstride, s->page[b], m, pl.pc, nc, 0, 1, s->lambda, s->diag + c0, st));
+            PCHK(mark_end(s, 2));
+            if (!download(p, b)) return false;
+        }
+    }
+    PCHK(hipEventRecord(E[2], s->down));
+    PCHK(hipStreamWaitEvent(st, E[2], 0));
+    return true;
+}
+
+#undef PCHK
+
+}  // namespace
+
+MFAC_API size_t mfac_static_paged_workspace_bytes(int64_t d, int32_t block, int32_t m, int64_t page_cols) {
+    PagedPlan pl;
+    if (!paged_plan(d, block, m, page_cols, pl)) return 0;
+    return static_paged_layout<mfac_static_s>(d, block, m, pl, nullptr, nullptr);
+}
+
+MFAC_API mfac_status mfac_static_precompute_paged(mfac_static* out, int64_t d, int32_t block, int32_t m,
+                                                  double lambda, float* G_host, int64_t page_cols, void* workspace,
+                                                  size_t workspace_bytes, uint32_t flags, hipStream_t stream) {
+    if (!out) return MFAC_EINVAL;
+    *out = nullptr;
+    PagedPlan pl;
+    if (!paged_plan(d, block, m, page_cols, pl)) return MFAC_EINVAL;
+    if (flags & ~MFAC_STATIC_TRACE) return MFAC_EINVAL;
+    if (!(lambda > 0.0) || !isfinite(lambda)) return MFAC_EINVAL;
+    if (!G_host || !workspace || !aligned16(G_host) || ((uintptr_t)workspace & 255u)) return MFAC_EINVAL;
+    // G must be pinned host memory (hipHostMalloc): the copies stream from it
+    // and the queries read it in place
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, G_host) != hipSuccess) {
+        (void)hipGetLastError();
+        return MFAC_EINVAL;
+    }
+    if (at.type != hipMemoryTypeHost || !at.devicePointer) return MFAC_EINVAL;
+    if (workspace_bytes < mfac_static_paged_workspace_bytes(d, block, m, page_cols)) return MFAC_EWORKSPACE;
+
+    mfac_static s = (mfac_static)calloc(1, sizeof(mfac_static_s));
+    if (!s) return MFAC_EINVAL;
+    s->d = d;
+    s->B = block;
+    s->m = m;
+    s->mp = padded_m(m);
+    s->nblocks = (int)(d / block);
+    s->lambda = lambda;
+    s->G = (float*)at.devicePointer;
+    s->Ghost = G_host;
+    s->paged = true;
+    s->st = stream;
+    s->trace = (flags & MFAC_STATIC_TRACE) != 0;
+    if (s->trace) s->marks = new std::vector<mfac_window_s::Mark>();
+    static_paged_layout<mfac_static_s>(d, block, m, pl, (char*)workspace, s);
+    bool ok = hipStreamCreateWithFlags(&s->up, hipStreamNonBlocking) == hipSuccess &&
+              hipStreamCreateWithFlags(&s->down, hipStreamNonBlocking) == hipSuccess;
+    for (int i = 0; ok && i < 9; ++i) ok = hipEventCreateWithFlags(&s->pev[i], hipEventDisableTiming) == hipSuccess;
+    if (ok) ok = paged_run(s, pl, (double)m * lambda);
+    if (!ok) {
+        (void)hipStreamSynchronize(s->st);
+        static_release(s);
+        return MFAC_EHIP;
+    }
+    *out = s;
     return MFAC_OK;
 }

@@ -188,12 +188,14 @@ constexpr int GT = 128;
 // Eight waves per 128 x 128 tile, each owning 32 x 64 as 2 x 4 MFMA tiles, and
 // two work-groups per CU (4 waves per SIMD hide each other's LDS and memory
 // waits). Staged chunk values live in named registers. nsplit == 1: the tile
-// goes straight into A (plus mu on the diagonal); otherwise split s of the
-// block's columns [s*kcols, min(B, (s+1)*kcols)) writes its fp64 partial tile
-// to part[(block*nsplit + s)*ntiles + tile].
+// goes straight into A (plus mu on the diagonal; with accum, added to what A
+// holds instead, no mu); otherwise split s of the block's columns
+// [s*kcols, min(B, (s+1)*kcols)) writes its fp64 partial tile to
+// part[(block*nsplit + s)*ntiles + tile].
 __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict__ G, int m, int64_t d, int B,
                                                         int b0, int ntiles, int nsplit, int kcols, double mu,
-                                                        double* __restrict__ A, int mp, double* __restrict__ part) {
+                                                        int accum, double* __restrict__ A, int mp,
+                                                        double* __restrict__ part) {
     __shared__ float As[2][GT][PITCH];
     __shared__ float Bs[2][GT][PITCH];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
@@ -302,7 +304,10 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
                 const int col = rb0 + wc * 64 + y * 16 + rl;
                 if (row < mp && col < mp) {
                     double v = acc[x][y][r];
-                    if (row == col) v += (row < m) ? mu : 1.0;
+                    if (accum)
+                        v += Ab[(int64_t)row * mp + col];
+                    else if (row == col)
+                        v += (row < m) ? mu : 1.0;
                     Ab[(int64_t)row * mp + col] = v;
                 }
             }
@@ -310,9 +315,11 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
 
 // A_b (lower triangle of every tile the factorization reads) = sum over the
 // column splits of the partial tiles, in split order, plus mu on the diagonal
-// (identity on the padding rows). Grid (ntiles, nb).
+// (identity on the padding rows); with accum, the sum is added to A_b instead.
+// Grid (ntiles, nb).
 __global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __restrict__ part, int nsplit, int ntiles,
-                                                            int m, double mu, double* __restrict__ A, int mp) {
+                                                            int m, double mu, int accum, double* __restrict__ A,
+                                                            int mp) {
     const int tile = blockIdx.x, bl = blockIdx.y;
     int ti, tj;
     tile_of(tile, ti, tj);
@@ -325,7 +332,10 @@ __global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __rest
         if (row >= mp || col >= mp || (ti == tj && rr < cc)) continue;
         double v = 0.0;
         for (int s = 0; s < nsplit; ++s) v += src[s * sstride + e];
-        if (row == col) v += (row < m) ? mu : 1.0;
+        if (accum)
+            v += Ab[(int64_t)row * mp + col];
+        else if (row == col)
+            v += (row < m) ? mu : 1.0;
         Ab[(int64_t)row * mp + col] = v;
     }
 }
@@ -394,15 +404,16 @@ int64_t gram_blocks_part_doubles(int nb, int mp, int B) {
 }
 
 hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb, double mu,
-                              double* A, int mp, double* part, hipStream_t st) {
+                              double* A, int mp, double* part, hipStream_t st, bool accumulate) {
     int ntiles, kcols;
     const int ns = gram_blocks_splits(nb, mp, B, ntiles, kcols);
+    const int acc = accumulate ? 1 : 0;
     hipLaunchKernelGGL(k_gram_blocks, dim3((unsigned)(ntiles * ns * nb)), dim3(512), 0, st, G, m, d, B, b0, ntiles,
-                       ns, kcols, mu, A, mp, part);
+                       ns, kcols, mu, acc, A, mp, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || ns == 1) return e;
     hipLaunchKernelGGL(k_gram_blocks_reduce, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part, ns,
-                       ntiles, m, mu, A, mp);
+                       ntiles, m, mu, acc, A, mp);
     return hipGetLastError();
 }
 

@@ -58,12 +58,15 @@ int64_t gram_window_part_doubles(int m, int64_t nslab);
 hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part, double* K,
                               hipStream_t st);
 // Static blocks: A_b = G_b G_b^T + mu I (fp64 MFMA), padded to mp with identity;
-// blocks [b0, b0+nb) of the m x d row-major G, block width B. Batches with few
-// tiles split the columns over work-groups: part must then hold
-// gram_blocks_part_doubles(nb, mp, B) doubles (0 when no split is used).
+// blocks [b0, b0+nb) of the m x d row-major G (row stride d), block width B.
+// Batches with few tiles split the columns over work-groups: part must then
+// hold gram_blocks_part_doubles(nb, mp, B) doubles (0 when no split is used).
+// accumulate: A_b += G_b G_b^T instead (the lower tiles), no mu or padding;
+// a wide block paged through the device in column pages sums its pages so.
 int64_t gram_blocks_part_doubles(int nb, int mp, int B);
 hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb,
-                              double mu, double* A, int mp, double* part, hipStream_t st);
+                              double mu, double* A, int mp, double* part, hipStream_t st,
+                              bool accumulate = false);
 
 // ---------------------------------------------------------------- coefficients
 // A (mp x mp) = K (m x m) + mu I, identity padding; optionally first replaces

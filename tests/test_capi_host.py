@@ -114,3 +114,22 @@ def test_trace_read_rejects_null_arguments():
     cnt = (ctypes.c_int64 * 4)()
     assert lib.mfac_static_trace_read(None, ms, cnt) == B.MFAC_EINVAL
     assert lib.mfac_window_trace_read(None, ms, cnt) == B.MFAC_EINVAL
+
+
+def test_paged_plan_validation_on_host():
+    lib = B.load()
+    ws = lib.mfac_static_paged_workspace_bytes
+    assert ws(4096, 256, 64, 1024) > 0
+    assert ws(4096, 256, 64, 2048) > ws(4096, 256, 64, 1024)     # two bigger page buffers, more blocks per page
+    assert ws(4096, 256, 64, 1000) == 0      # not whole blocks
+    assert ws(4096, 256, 64, 2) == 0         # below 4 columns
+    assert ws(4096, 4096, 64, 1026) == 0     # full-d pages: a multiple of 4
+    assert ws(4096, 4096, 64, 1024) > 0
+    assert ws(4096, 4096, 64, 1 << 20) == ws(4096, 4096, 64, 4096)   # pages wider than d mean d
+    h = ctypes.c_void_p()
+    for page in (1000, 2, 0):
+        assert lib.mfac_static_precompute_paged(ctypes.byref(h), 4096, 256, 64, 1e-4, 256, page, 512, 1 << 40, 0,
+                                                None) == B.MFAC_EINVAL
+        assert h.value is None
+    assert lib.mfac_static_precompute_paged(None, 4096, 256, 64, 1e-4, 256, 1024, 512, 1 << 40, 0,
+                                            None) == B.MFAC_EINVAL
