@@ -132,11 +132,16 @@ def cpu_baseline(wl, seed, sample_div, nsteps):
     }
 
 
+HOST_LINK_PEAK_GBS = 63.0   # PCIe 5.0 x16, per direction
+
+
 def bench_static(args, wl, dev):
     """Static block-wise path: precompute + inverse diagonal + OBD keep-mask.
 
     Each repetition restores G (the precompute overwrites it with W) outside
-    its own HIP-event interval; the reported time is the mean interval.
+    its own HIP-event interval; the reported time is the mean interval. With
+    a paged workload G sits in pinned host memory and the interval includes
+    every page's upload and download.
     """
     import torch
 
@@ -156,7 +161,9 @@ def bench_static(args, wl, dev):
         if r % 256 == 255:
             log(f"rows {r + 1}/{m}")
     theta = gs.theta()
-    G = torch.empty_like(G0)
+    paged = wl.page_cols > 0
+    G = torch.empty((m, d), dtype=torch.float32, pin_memory=True) if paged else torch.empty_like(G0)
+    pages = dict(page_cols=wl.page_cols, device=dev) if paged else {}
     keep = d // 2
     log(f"setup {time.perf_counter() - t0:.1f} s")
     times = []
@@ -167,7 +174,7 @@ def bench_static(args, wl, dev):
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        sb = P.StaticBlocks(G, B, wl.lam, trace=True)
+        sb = P.StaticBlocks(G, B, wl.lam, trace=True, **pages)
         diag = sb.inv_diag()
         mask, _ = sb.obs_mask(theta, keep, scores=False)
         e1.record(stream)
@@ -197,7 +204,7 @@ def bench_static(args, wl, dev):
     X = torch.empty((4, d), dtype=torch.float32, device=dev)
     for q in range(4):
         X[q] = gs.queries(0, 4)[q]
-    reps = 10
+    reps = 2 if paged else 10
     for n in (1, 4):
         Y = torch.empty((n, d), dtype=torch.float32, device=dev)
         sb.ihvp(X[:n], Y)
@@ -224,6 +231,16 @@ def bench_static(args, wl, dev):
     sb.close()
     log(f"queries: {queries}")
     cpu = None
+    link = None
+    if paged:
+        # bytes over the host link per run: every page up and down once, and a
+        # wide block's pages up a second time for W
+        up = 4.0 * m * d * (2 if B == d else 1)
+        down = 4.0 * m * d
+        link = {"upload_bytes": up, "download_bytes": down, "upload_gbs": up / (ms * 1e-3) / 1e9,
+                "download_gbs": down / (ms * 1e-3) / 1e9, "peak_gbs_per_direction": HOST_LINK_PEAK_GBS,
+                "frac_upload": up / (ms * 1e-3) / 1e9 / HOST_LINK_PEAK_GBS}
+        log(f"host link: {link}")
     if not args.no_cpu_baseline:
         del G, X, Y, delta
         torch.cuda.empty_cache()
@@ -231,11 +248,13 @@ def bench_static(args, wl, dev):
         cpu = cpu_static_baseline(wl, G0, theta, wl.lam, args.cpu_blocks)
         log(f"cpu baseline {cpu}")
     out = {
-        "metric": "static block-wise precompute + inverse diagonal + top-50% OBD mask, runs/sec (1 GPU)",
+        "metric": ("static block-wise precompute + inverse diagonal + top-50% OBD mask, runs/sec (1 GPU"
+                   + (", G paged from pinned host memory)" if paged else ")")),
         "value": 1000.0 / ms, "unit": "runs/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep},
+        "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep,
+                   "page_cols": wl.page_cols or None},
         "roofline": {"bound": "mfma", "kernel": "k_gram_blocks", "achieved": gram_tf, "peak": 78.6,
                      "unit": "TFLOP/s", "frac": gram_tf / 78.6, "traffic": read_static_counters(wl.name, "k_gram_blocks")},
         "whole_run": {"achieved_tflops": flops / (ms * 1e-3) / 1e12,
@@ -246,6 +265,7 @@ def bench_static(args, wl, dev):
         "stage_launches_per_run": {"gram": stage_cnt[0] // runs, "factor_inverse": stage_cnt[1] // runs,
                                    "w_and_diag": stage_cnt[2] // runs, "scores_mask": stage_cnt[3] // runs},
         "queries": queries,
+        "host_link": link,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -36,6 +36,7 @@ class Workload:
                          # reduced-size parity cases keep the full-size scale
     batch: int = 0       # optim: mini-batch size of the model's synthetic batches
     model: str = ""      # optim: the network trained
+    page_cols: int = 0   # static: G in pinned host memory, paged through the device in pages of this many columns
 
     def scaled(self, **kw) -> "Workload":
         """Same recipe at another size (parity cases the oracle finishes in seconds)."""
@@ -68,6 +69,14 @@ WORKLOADS = {
     "static_full_d4.19m_m1024": Workload(
         "static_full_d4.19m_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
         dist="lognormal", block=4_194_304, theta_std=0.05),
+    # the two static workloads with G in pinned host memory, paged through the
+    # device (Appendix C's host paging): 64 blocks per page, and 8 column pages
+    "static_paged_d4.19m_b2048_m1024": Workload(
+        "static_paged_d4.19m_b2048_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
+        dist="lognormal", block=2048, theta_std=0.05, page_cols=64 * 2048),
+    "static_paged_full_d4.19m_m1024": Workload(
+        "static_paged_full_d4.19m_m1024", "static", d=4_194_304, m=1024, lam=1e-4,
+        dist="lognormal", block=4_194_304, theta_std=0.05, page_cols=524_288),
     # the optimizer loop on a CIFAR-shaped ResNet-20 (269,722 weights), batch 128,
     # window m = 512 (Section 4.2, Table 4 settings); random inputs and labels
     "optim_resnet20_cifar_b128_m512": Workload(
