@@ -234,8 +234,10 @@ def bench_static(args, wl, dev):
     link = None
     if paged:
         # bytes over the host link per run: every page up and down once, and a
-        # wide block's pages up a second time for W
-        up = 4.0 * m * d * (2 if B == d else 1)
+        # wide block's pages up a second time for W, except the three last
+        # pages, still on the device after the Gram sweep
+        npages = -(-d // wl.page_cols)
+        up = 4.0 * m * (d + (max(0, npages - 3) * wl.page_cols if B == d else 0))
         down = 4.0 * m * d
         link = {"upload_bytes": up, "download_bytes": down, "upload_gbs": up / (ms * 1e-3) / 1e9,
                 "download_gbs": down / (ms * 1e-3) / 1e9, "peak_gbs_per_direction": HOST_LINK_PEAK_GBS,

@@ -215,12 +215,13 @@ mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, i
  *              Pageable memory is rejected (MFAC_EINVAL).
  *   page_cols: columns per page, a multiple of 4 and, when block < d, of
  *              block (a page holds whole blocks, at most 65535); values above
- *              d mean d. Two device page buffers of m * page_cols floats
+ *              d mean d. Three device page buffers of m * page_cols floats
  *              live in the workspace.
  * block < d: one sweep; each page is uploaded, its blocks go through Gram,
  * factor and W, and W is downloaded (G crosses the host link twice).
  * block == d: the one block's Gram is summed page by page, factored, and a
- * second sweep forms W page by page (G crosses three times).
+ * second sweep forms W page by page, starting with the (up to) three last
+ * pages, still on the device (G crosses up to three times).
  * Uploads and downloads run on two streams the handle creates (default
  * priority) and overlap each other and the kernels on `stream`, which waits
  * for the last download before any later call on the handle. The queries

@@ -83,12 +83,12 @@ struct mfac_static_s {
     std::vector<mfac_window_s::Mark>* marks;
     hipEvent_t open_ev;
     // host-paged precompute: G lives in pinned host memory (G above is its
-    // device-visible address), pages of it pass through two device buffers
+    // device-visible address), pages of it pass through three device buffers
     bool paged;
     float* Ghost;
-    float* page[2];
+    float* page[3];
     hipStream_t up, down;  // host-to-device and device-to-host copy streams
-    hipEvent_t pev[9];     // fork, factor done, join, uploaded[2], computed[2], downloaded[2]
+    hipEvent_t pev[12];    // fork, factor done, join, uploaded[3], computed[3], downloaded[3]
 };
 
 namespace {
@@ -539,7 +539,7 @@ void static_release(mfac_static_s* s) {
         (void)hipStreamSynchronize(s->down);
         (void)hipStreamDestroy(s->down);
     }
-    for (int i = 0; i < 9; ++i)
+    for (int i = 0; i < 12; ++i)
         if (s->pev[i]) (void)hipEventDestroy(s->pev[i]);
     marks_free(s);
     free(s);
@@ -722,8 +722,8 @@ size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* b
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
     float* qcoef = c.take<float>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
-    float* p0 = c.take<float>((size_t)m * pl.pc);
-    float* p1 = c.take<float>((size_t)m * pl.pc);
+    float* pg[3];
+    for (int i = 0; i < 3; ++i) pg[i] = c.take<float>((size_t)m * pl.pc);
     if (s) {
         s->err = err;
         s->diag = diag;
@@ -735,8 +735,7 @@ size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* b
         s->qpart = qpart;
         s->qcoef = qcoef;
         s->xobs = xobs;
-        s->page[0] = p0;
-        s->page[1] = p1;
+        for (int i = 0; i < 3; ++i) s->page[i] = pg[i];
         s->batch = pl.pb;
     }
     return c.off;
@@ -749,15 +748,16 @@ size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* b
 
 // The page pipeline. Copies run on their own streams (uploads and downloads
 // overlap each other and the kernels); the kernels run in order on the
-// handle's stream; two device buffers alternate between pages, each reused
-// once the previous page in it has been downloaded (or, in a Gram-only
-// sweep, consumed).
+// handle's stream; three device buffers rotate between pages, each reused
+// once the page before in it has been downloaded (or, in a Gram-only sweep,
+// consumed). With two, a buffer's upload-compute-download cycle, not the
+// host link, set the pace.
 bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
     const int64_t d = s->d;
     const int m = s->m, B = s->B, mp = s->mp;
     const int64_t bstride = (int64_t)mp * mp;
     hipStream_t st = s->st;
-    hipEvent_t* E = s->pev;  // 0 fork, 1 factor done, 2 join, 3+b uploaded, 5+b computed, 7+b downloaded
+    hipEvent_t* E = s->pev;  // 0 fork, 1 factor done, 2 join, 3+b uploaded, 6+b computed, 9+b downloaded
     auto cols = [&](int64_t p, int64_t& c0) {
         c0 = p * pl.pc;
         return (d - c0) < pl.pc ? (d - c0) : pl.pc;
@@ -775,11 +775,11 @@ bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
     auto download = [&](int64_t p, int b) {
         int64_t c0;
         const int64_t nc = cols(p, c0);
-        PCHK(hipEventRecord(E[5 + b], st));
-        PCHK(hipStreamWaitEvent(s->down, E[5 + b], 0));
+        PCHK(hipEventRecord(E[6 + b], st));
+        PCHK(hipStreamWaitEvent(s->down, E[6 + b], 0));
         PCHK(hipMemcpy2DAsync(s->Ghost + c0, (size_t)d * 4, s->page[b], (size_t)pl.pc * 4, (size_t)nc * 4,
                               (size_t)m, hipMemcpyDeviceToHost, s->down));
-        PCHK(hipEventRecord(E[7 + b], s->down));
+        PCHK(hipEventRecord(E[9 + b], s->down));
         return true;
     };
     PCHK(launch_fill_zero((float*)s->err, 1, st));
@@ -789,10 +789,10 @@ bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
     if (B < d) {
         // whole blocks per page: Gram, factor, W and diagonal, then back to the host
         for (int64_t p = 0; p < pl.npages; ++p) {
-            const int b = (int)(p & 1);
+            const int b = (int)(p % 3);
             int64_t c0;
             const int nbp = (int)(cols(p, c0) / B);
-            if (!upload(p, b, p >= 2 ? E[7 + b] : nullptr)) return false;
+            if (!upload(p, b, p >= 3 ? E[9 + b] : nullptr)) return false;
             PCHK(mark_begin(s));
             PCHK(launch_gram_blocks(s->page[b], m, pl.pc, B, 0, nbp, mu, s->A, mp, s->gpart, st));
             PCHK(mark_end(s, 0));
@@ -808,25 +808,37 @@ bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
         // one block over all pages: its Gram summed page by page, the factor,
         // then a second sweep for W and the diagonal
         for (int64_t p = 0; p < pl.npages; ++p) {
-            const int b = (int)(p & 1);
+            const int b = (int)(p % 3);
             int64_t c0;
             const int nc = (int)cols(p, c0);
-            if (!upload(p, b, p >= 2 ? E[5 + b] : nullptr)) return false;
+            if (!upload(p, b, p >= 3 ? E[6 + b] : nullptr)) return false;
             PCHK(mark_begin(s));
             PCHK(launch_gram_blocks(s->page[b], m, pl.pc, nc, 0, 1, mu, s->A, mp, s->gpart, st, p > 0));
             PCHK(mark_end(s, 0));
-            PCHK(hipEventRecord(E[5 + b], st));
+            PCHK(hipEventRecord(E[6 + b], st));
         }
         PCHK(mark_begin(s));
         PCHK(launch_factor_invert(s->A, s->Linv, mp, 1, bstride, s->err, st));
         PCHK(mark_end(s, 1));
         PCHK(hipEventRecord(E[1], st));
         PCHK(hipStreamWaitEvent(s->up, E[1], 0));
-        for (int64_t p = 0; p < pl.npages; ++p) {
-            const int b = (int)(p & 1);
+        // the last (up to) three pages are still in their buffers: they go
+        // first, without a second upload; the others follow in order, each
+        // in the buffer that the page processed three steps earlier freed
+        const int64_t nres = pl.npages < 3 ? pl.npages : 3;
+        int ring[3];
+        for (int64_t q = 0; q < pl.npages; ++q) {
+            const int64_t p = q < nres ? pl.npages - 1 - q : q - nres;
             int64_t c0;
             const int nc = (int)cols(p, c0);
-            if (!upload(p, b, p >= 2 ? E[7 + b] : nullptr)) return false;
+            int b;
+            if (q < nres) {
+                b = (int)(p % 3);
+                ring[q] = b;
+            } else {
+                b = ring[q % 3];
+                if (!upload(p, b, E[9 + b])) return false;
+            }
             PCHK(mark_begin(s));
             PCHK(launch_trmm_diag(s->Linv, mp, bstride, s->page[b], m, pl.pc, nc, 0, 1, s->lambda, s->diag + c0, st));
             PCHK(mark_end(s, 2));
@@ -885,7 +897,7 @@ MFAC_API mfac_status mfac_static_precompute_paged(mfac_static* out, int64_t d, i
     static_paged_layout<mfac_static_s>(d, block, m, pl, (char*)workspace, s);
     bool ok = hipStreamCreateWithFlags(&s->up, hipStreamNonBlocking) == hipSuccess &&
               hipStreamCreateWithFlags(&s->down, hipStreamNonBlocking) == hipSuccess;
-    for (int i = 0; ok && i < 9; ++i) ok = hipEventCreateWithFlags(&s->pev[i], hipEventDisableTiming) == hipSuccess;
+    for (int i = 0; ok && i < 12; ++i) ok = hipEventCreateWithFlags(&s->pev[i], hipEventDisableTiming) == hipSuccess;
     if (ok) ok = paged_run(s, pl, (double)m * lambda);
     if (!ok) {
         (void)hipStreamSynchronize(s->st);
