@@ -625,6 +625,28 @@ def main():
         sys.exit(1)
     log(f"timed {args.steps} steps: {ms_total:.1f} ms (wall {wall * 1e3:.1f} ms)")
 
+    # The periodic full refactor (every R replaces, R = max(m, 1024) by
+    # default) falls outside a 200-step window; its cost is measured here on
+    # a few replaces that each refactor, and reported amortized over R.
+    period = args.refactor_period if args.refactor_period is not None else max(m, 1024)
+    refactor = None
+    if period > 0:
+        win.set_refactor_period(0)
+        win.trace(True)
+        for t in range(3):
+            step(args.warmup + t)
+        torch.cuda.synchronize()
+        win.trace(False)
+        rms, rcnt = win.trace_read()
+        win.set_refactor_period(period)
+        coef_refactor = rms[1] / max(rcnt[1], 1)
+        coef_update = ph_ms[1] / max(ph_cnt[1], 1)
+        refactor = {"period": period, "coefficients_ms_with_refactor": coef_refactor,
+                    "coefficients_ms_with_update": coef_update,
+                    "amortized_ms_per_step": max(coef_refactor - coef_update, 0.0) / period,
+                    "in_timed_region": args.steps >= period}
+        log(f"refactor: {refactor}")
+
     ms_step = ms_total / args.steps
     b1, b2, bw = pass_bytes(d, m)
     if nq:
@@ -661,6 +683,7 @@ def main():
         },
         "achieved_hbm_gbs_step": step_bytes / (ms_step * 1e-3) / 1e9,
         "phases_ms_per_step": {"row_write": avg[3], "pass1": avg[0], "coefficients": avg[1], "pass2": avg[2]},
+        "refactor": refactor,
         "pass_gbs": {"k_pass1": gbs1, "k_pass2": gbs2},
         "roofline": {
             "bound": "hbm",
