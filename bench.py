@@ -529,7 +529,7 @@ def main():
     ap.add_argument("--workload", default="dyn_resnet50_d25.6m_m1024")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-div", type=int, default=64)
+    ap.add_argument("--cpu-sample-div", type=int, default=16)
     ap.add_argument("--cpu-steps", type=int, default=12)
     ap.add_argument("--cpu-blocks", type=int, default=128,
                     help="static workloads: blocks the oracle baseline is timed on")
