@@ -180,6 +180,17 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
         auto crow = [&](int x, int r) { return mrow0 + wr * 32 + x * 16 + kl + 4 * r; };
         auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
         const int nchunk = (khi - klo) / BK;
+        // This wave's own K range: a triangular operand is zero outside it, so
+        // the wave skips the MFMAs of chunks that lie wholly outside (the
+        // trimmed K range above is per 128-tile; this is per 32 rows / 64
+        // columns). A wave whose rows or columns all lie past M / N, or that
+        // sits above the diagonal of a diagonal tile of a lower-triangle
+        // product, computes and stores nothing.
+        int wkhi = khi, wklo = klo;
+        if (g.flags & KHI_ROW) wkhi = min(wkhi, mrow0 + wr * 32 + 32);
+        if (g.flags & KLO_COL) wklo = max(wklo, ncol0 + wc * 64);
+        const bool idle = mrow0 + wr * 32 >= g.M || ncol0 + wc * 64 >= g.N ||
+                          ((g.flags & LOWER_ONLY) && I == J && wr * 32 + 31 < wc * 64);
         if (nchunk > 0) load_chunk(klo);
         // beta C enters as the accumulator's start value (scaled by 1/alpha), so
         // its loads issue together with the first chunk's
@@ -192,7 +203,7 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
     #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     double v = 0.0;
-                    if (g.beta != 0.0) {
+                    if (g.beta != 0.0 && !idle) {
                         const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
                         v = cs * C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
                     }
@@ -205,6 +216,8 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
         for (int c = 0; c < nchunk; ++c) {
             const int buf = c & 1;
             if (c + 1 < nchunk) load_chunk(klo + (c + 1) * BK);
+            const int k0 = klo + c * BK;
+            if (!idle && k0 + BK > wklo && k0 < wkhi) {
     #pragma unroll
             for (int kk = 0; kk < BK / 4; ++kk) {
                 double av[2], bv[4];
@@ -220,9 +233,11 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
                     for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
+            }
             if (c + 1 < nchunk) store_chunk(buf ^ 1);
             __syncthreads();
         }
+        if (idle) return;
     #pragma unroll
         for (int x = 0; x < 2; ++x)
     #pragma unroll
