@@ -203,6 +203,30 @@ def test_checkpoint_resume(dev):
     assert win.info() == win2.info()
 
 
+def test_checkpoint_resume_bitwise_after_rebuild(dev):
+    """The derived state (K, the explicit inverse, the refactor counter) is
+    rebuilt from the rows on resume; rebuilding the original at the
+    checkpoint too makes both continue bitwise identically."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=40000, m=64, scale_d=base.d)
+    gs = GradientStream(wl, seed=10)
+    say("checkpoint/resume bitwise")
+    win = Window(wl.d, wl.m, wl.lam, G0=gs.window().to(dev), device=dev)
+    for t in range(5):
+        win.replace(gs.row(wl.m + t).to(dev))
+    rows = win.get_rows()
+    head, steps = win.info()
+    win.rebuild()
+    win2 = Window(wl.d, wl.m, wl.lam, G0=rows, device=dev)
+    win2.set_head(head, steps)
+    for t in range(5, 12):
+        g = gs.row(wl.m + t).to(dev)
+        assert torch.equal(win.replace(g), win2.replace(g))
+    assert win.info() == win2.info()
+    assert win.status() == 0 and win2.status() == 0
+
+
 def test_nonfinite_latched_and_rebuild_recovers(dev):
     from paper_2107_03356_amd import MFAC_ENONFINITE, Window
     base = get_workload("dyn_d1m_m256")
@@ -327,3 +351,36 @@ def test_two_windows_on_two_streams_interleaved(dev):
             yo = orcs[i].slide(g.numpy())
             assert rel_l2(y.cpu().numpy(), yo) < REL_TOL
         assert wins[i].status() == 0
+
+
+def test_step_cost_is_linear_in_d_and_coefficients_independent_of_d(dev):
+    """The complexity claims of Section 3.2: the two passes cost O(dm) (4x the
+    columns, ~4x the pass time) and the coefficient phase O(m^2), independent
+    of d. Phase times from the library's own HIP-event tracing."""
+    from paper_2107_03356_amd import Window
+    m = 256
+    phases = {}
+    for d in (1 << 21, 1 << 23):
+        say("complexity", d, m)
+        win = Window(d, m, 1e-4, device=dev)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(d)
+        g = torch.randn((24, d), device=dev, generator=gen) / d ** 0.5
+        for t in range(4):
+            win.replace(g[t])
+        torch.cuda.synchronize()
+        win.trace_read()
+        win.trace(True)
+        for t in range(4, 24):
+            win.replace(g[t])
+        torch.cuda.synchronize()
+        win.trace(False)
+        ms, cnt = win.trace_read()
+        phases[d] = [ms[i] / max(cnt[i], 1) for i in range(4)]
+        assert win.status() == 0
+        win.close()
+    small, big = phases[1 << 21], phases[1 << 23]
+    passes = (big[0] + big[2]) / (small[0] + small[2])
+    coef = big[1] / small[1]
+    assert 3.0 < passes < 5.5, (passes, small, big)
+    assert 0.5 < coef < 2.0, (coef, small, big)
