@@ -215,8 +215,9 @@ mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, i
  *              Pageable memory is rejected (MFAC_EINVAL).
  *   page_cols: columns per page, a multiple of 4 and, when block < d, of
  *              block (a page holds whole blocks, at most 65535); values above
- *              d mean d. Three device page buffers of m * page_cols floats
- *              live in the workspace.
+ *              d mean d; the page width (after that) at most 2^30. Three
+ *              device page buffers of m * page_cols floats live in the
+ *              workspace.
  * block < d: one sweep; each page is uploaded, its blocks go through Gram,
  * factor and W, and W is downloaded (G crosses the host link twice).
  * block == d: the one block's Gram is summed page by page, factored, and a
