@@ -87,6 +87,8 @@ def test_tiny_init_equals_fill(dev):
     (2048, 1, 1e-2, 1, "gauss"),                   # m = 1 (Sherman-Morrison)
     (5, 3, 1e-1, 1, "gauss"),                      # d smaller than one float4 group row
     (8192, 4096, 1e-3, 1, "gauss"),                # m = 4096: 528 Gram tiles, six recursion levels
+    (12000, 1500, 1e-4, 9, "lognormal"),           # 10 vectors at m = 1500: pass-2 coefficient rows left unpadded (LDS bound)
+    (9000, 300, 1e-4, 16, "gauss"),                # the most fused vectors (17), padded rows of 20
 ])
 def test_ragged_and_multitile_with_queries(dev, d, m, lam, q, dist):
     base = get_workload("dyn_resnet18_d11.2m_m1024_q8")
