@@ -52,7 +52,7 @@ def build(verbose: bool = False) -> str:
         # compiler did not keep in registers is a performance bug; the few
         # spills of the MFMA tile kernels under their 4-waves-per-SIMD launch
         # bounds (k_gram_window, k_gram_blocks, k_trmm_diag, k_bgemm with a
-        # transposed B) sit outside their inner loops and are measured wins
+        # transposed B) are measured wins over fewer waves without them
         name = None
         for line in r.stderr.splitlines():
             m = re.search(r"Function Name: (\S+)", line)
