@@ -50,8 +50,7 @@ struct mfac_window_s {
     float* G;
     hipStream_t st;
     int* err;
-    double *K, *A, *Linv, *Ainv, *part, *p, *zv, *gpart;
-    float* coef;
+    double *K, *A, *Linv, *Ainv, *part, *p, *zv, *gpart, *coef;
     int head;
     int64_t steps;
     // coefficient policy: 0 = refactor from K on every replace; R > 0 = O(m^2)
@@ -106,7 +105,7 @@ size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
     double* Ainv = c.take<double>((size_t)mp * mp);
     double* p = c.take<double>((size_t)m * nvmax);
     double* zv = c.take<double>((size_t)mp * 2);
-    float* coef = c.take<float>((size_t)m * nvmax);
+    double* coef = c.take<double>((size_t)m * nvmax);
     double* gpart = c.take<double>((size_t)gram_window_part_doubles(m, nslab_of(d)));
     if (w) {
         w->err = err;

@@ -299,7 +299,7 @@ __global__ __launch_bounds__(256) void k_inv_update(const double* __restrict__ p
 // the other columns p[j*pstride + c]; one wave per row i, lanes along the row.
 __global__ __launch_bounds__(256) void k_coef_from_inv(const double* __restrict__ Ainv, int mp, int m,
                                                        const double* __restrict__ p, int pstride, int nv, int k,
-                                                       double s0, double s1, float* __restrict__ coef,
+                                                       double s0, double s1, double* __restrict__ coef,
                                                        int* __restrict__ err) {
     const int lane = threadIdx.x & 63;
     const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -322,7 +322,7 @@ __global__ __launch_bounds__(256) void k_coef_from_inv(const double* __restrict_
             x *= (c == 0 ? s0 : s1);
             if (lane == 0) {
                 if (!isfinite(x)) atomicOr(err, 4);
-                coef[i * nv + c] = (float)x;
+                coef[i * nv + c] = x;
             }
         }
     }
@@ -369,7 +369,7 @@ hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, in
 }
 
 hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double* p, int pstride, int nv, int k,
-                                double s0, double s1, float* coef, int* err, hipStream_t st) {
+                                double s0, double s1, double* coef, int* err, hipStream_t st) {
     hipLaunchKernelGGL(k_coef_from_inv, dim3((unsigned)ceil_div(m, 4)), dim3(256), 0, st, Ainv, mp, m, p, pstride, nv,
                        k, s0, s1, coef, err);
     return hipGetLastError();

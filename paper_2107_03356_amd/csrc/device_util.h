@@ -45,6 +45,15 @@ __device__ __forceinline__ float dot4(float4 a, float4 b, float s) {
     return s;
 }
 
+// fp64 dot of two fp32 float4 (the products are exact in fp64)
+__device__ __forceinline__ double dot4d(float4 a, float4 b, double s) {
+    s = fma((double)a.x, (double)b.x, s);
+    s = fma((double)a.y, (double)b.y, s);
+    s = fma((double)a.z, (double)b.z, s);
+    s = fma((double)a.w, (double)b.w, s);
+    return s;
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
@@ -57,39 +66,39 @@ __device__ __forceinline__ float wave_sum(float x) {
 // pending values halves while the lanes covered double. Once one value is
 // left, plain butterfly steps finish the sum. On return the lane holds the
 // total of value `base`; exactly one lane per value has writer == true.
-template <int N, int C, int O>
+template <typename T, int N, int C, int O>
 struct WaveReduceMany {
-    static __device__ __forceinline__ void run(float (&s)[N], int lane, int& base, int& creal, bool& dup) {
+    static __device__ __forceinline__ void run(T (&s)[N], int lane, int& base, int& creal, bool& dup) {
         if constexpr (O > 0) {
             const bool up = (lane & O) != 0;
             if constexpr (C > 1) {
                 constexpr int H = (C + 1) / 2;
 #pragma unroll
                 for (int j = 0; j < H; ++j) {
-                    const float lo = s[j];
-                    const float hi = (H + j < C) ? s[(H + j < N) ? H + j : N - 1] : 0.f;
-                    const float send = up ? lo : hi;
-                    const float keep = up ? hi : lo;
+                    const T lo = s[j];
+                    const T hi = (H + j < C) ? s[(H + j < N) ? H + j : N - 1] : T(0);
+                    const T send = up ? lo : hi;
+                    const T keep = up ? hi : lo;
                     s[j] = keep + __shfl_xor(send, O, 64);
                 }
                 base += up ? H : 0;
                 creal = up ? (creal > H ? creal - H : 0) : (creal < H ? creal : H);
-                WaveReduceMany<N, H, O / 2>::run(s, lane, base, creal, dup);
+                WaveReduceMany<T, N, H, O / 2>::run(s, lane, base, creal, dup);
             } else {
                 s[0] += __shfl_xor(s[0], O, 64);
                 dup = dup || up;
-                WaveReduceMany<N, 1, O / 2>::run(s, lane, base, creal, dup);
+                WaveReduceMany<T, N, 1, O / 2>::run(s, lane, base, creal, dup);
             }
         }
     }
 };
 
-template <int N>
-__device__ __forceinline__ float wave_reduce_many(float (&s)[N], int lane, int& base, bool& writer) {
+template <int N, typename T>
+__device__ __forceinline__ T wave_reduce_many(T (&s)[N], int lane, int& base, bool& writer) {
     base = 0;
     int creal = N;
     bool dup = false;
-    WaveReduceMany<N, N, 32>::run(s, lane, base, creal, dup);
+    WaveReduceMany<T, N, N, 32>::run(s, lane, base, creal, dup);
     writer = !dup && creal > 0;
     return s[0];
 }

@@ -7,10 +7,10 @@
 // staged through double-buffered LDS in 128 x 32 fp32 panels (row pitch 36
 // floats: the 16-row x 4-k read pattern of one MFMA operand is conflict-free).
 //
-// Window Gram: fp32 MFMA (v_mfma_f32_16x16x4f32). The column range of the
-// window is split over work-groups; each work-group flushes its fp32 MFMA
-// accumulators into fp64 registers after every 2048-column slab, and the
-// split partials are summed in fp64, in a fixed order, by k_gram_reduce.
+// Window Gram: fp64 MFMA (v_mfma_f64_16x16x4f64) on the fp32 window values
+// (exact products, fp64 sums, as in the passes that keep K up to date). The
+// column range of the window is split over work-groups and the split
+// partials are summed in fp64, in a fixed order, by k_gram_reduce.
 // Static blocks: fp64 MFMA (v_mfma_f64_16x16x4f64) over the block's columns
 // in 128 x 128 tiles, written straight into the block's padded fp64 matrix
 // with m*lambda added on the diagonal, because the keep-mask is decided in fp64.
@@ -24,7 +24,6 @@
 namespace mfac {
 namespace {
 
-typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int KB = 32;     // columns per LDS stage
 constexpr int PITCH = 36;  // LDS row pitch (floats)
 
@@ -38,17 +37,15 @@ __device__ __forceinline__ void tile_of(int idx, int& ti, int& tj) {
 
 // Window Gram partials. Grid (ntiles, nsplit): work-group (t, s) computes the
 // 128 x 128 lower tile t of K over slabs [s*sps, min(nslab, (s+1)*sps)). Eight
-// waves, each owning a 32 x 64 piece as 2 x 4 fp32 MFMA tiles (two waves per
-// SIMD hide each other's LDS and memory waits); the fp32 accumulators are
-// added into fp64 registers after every slab (2048 columns). The slab's rows
-// stream through double-buffered LDS in 32-column chunks (128 x 32 fp32 per
-// operand), the next chunk's global loads in flight during the MFMAs. Rows
-// past m load clamped, in-bounds data; only rows and columns below m of the
-// partial are ever summed into K.
+// waves, each owning a 32 x 64 piece as 2 x 4 fp64 MFMA tiles (two waves per
+// SIMD hide each other's LDS and memory waits), operands converted from fp32
+// as they are read from LDS. The slab's rows stream through double-buffered
+// LDS in 32-column chunks (128 x 32 fp32 per operand), the next chunk's global
+// loads in flight during the MFMAs. Rows past m load clamped, in-bounds data;
+// only rows and columns below m of the partial are ever summed into K.
 constexpr int WT = 128;  // window Gram tile
 
-// Two work-groups per CU (4 waves per SIMD): the 128-VGPR cap costs a few
-// spilled registers outside the inner loop and measured 7% faster than one.
+// Two work-groups per CU (4 waves per SIMD).
 __global__ __launch_bounds__(512, 4) void k_gram_window(const float* __restrict__ G, int m, int64_t nslab,
                                                      int64_t sps, double* __restrict__ part, int ntiles) {
     __shared__ float As[2][WT][PITCH];
@@ -103,11 +100,6 @@ __global__ __launch_bounds__(512, 4) void k_gram_window(const float* __restrict_
     }
     int buf = 0;
     for (int64_t s = s0; s < s1; ++s) {
-        v4f acc[2][4];
-#pragma unroll
-        for (int x = 0; x < 2; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
         for (int c = 0; c < NCH; ++c) {
             // next chunk: the following columns of this slab, or the next slab's first
             const bool more = c + 1 < NCH || s + 1 < s1;
@@ -119,28 +111,22 @@ __global__ __launch_bounds__(512, 4) void k_gram_window(const float* __restrict_
             if (!upper_wave) {
 #pragma unroll
                 for (int kk = 0; kk < KB / 4; ++kk) {
-                    float av[2], bv[4];
+                    double av[2], bv[4];
 #pragma unroll
-                    for (int x = 0; x < 2; ++x) av[x] = Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
+                    for (int x = 0; x < 2; ++x) av[x] = (double)Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                    for (int y = 0; y < 4; ++y) bv[y] = Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
+                    for (int y = 0; y < 4; ++y) bv[y] = (double)Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
 #pragma unroll
                     for (int x = 0; x < 2; ++x)
 #pragma unroll
                         for (int y = 0; y < 4; ++y)
-                            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+                            accd[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], accd[x][y], 0, 0, 0);
                 }
             }
             if (more) MFAC_GW_STORE(buf ^ 1)
             __syncthreads();
             buf ^= 1;
         }
-#pragma unroll
-        for (int x = 0; x < 2; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) accd[x][y][r] += (double)acc[x][y][r];
     }
 
     if (upper_wave) return;
@@ -151,8 +137,8 @@ __global__ __launch_bounds__(512, 4) void k_gram_window(const float* __restrict_
         for (int y = 0; y < 4; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                // fp32 MFMA result: lane l register r is row 4(l/16) + r
-                const int row = wr * 32 + x * 16 + kl * 4 + r;
+                // fp64 MFMA result: lane l register r is row (l/16) + 4r
+                const int row = wr * 32 + x * 16 + kl + 4 * r;
                 const int col = wc * 64 + y * 16 + rl;
                 out[row * WT + col] = accd[x][y][r];
             }

@@ -47,9 +47,10 @@ hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv,
 // p[t] = sum_b part[b][t] for t < mnv (fixed order, fp64)
 hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double* p,
                                   hipStream_t st);
-// Pass 2: y_v = alpha_v x_v - sum_i coef[i*nv+v] G[i,:]
+// Pass 2: y_v = alpha_v x_v - sum_i coef[i*nv+v] G[i,:] (fp64 coefficients and
+// accumulation, fp32 output)
 hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv,
-                        const float* coef, const VecOut& vout, bool aligned, hipStream_t st);
+                        const double* coef, const VecOut& vout, bool aligned, hipStream_t st);
 
 // ---------------------------------------------------------------- Gram
 // Window Gram: K (m x m, fp64, full symmetric) = sum over slabs of G_s G_s^T,
@@ -90,7 +91,7 @@ hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, in
 // coef[i*nv+c] = scale_c (Ainv rhs_c)_i: rhs_0 = e_k if k >= 0 (scale s0); the
 // other columns rhs_c[j] = p[j*pstride + c] (scale s1; also column 0 if k < 0).
 hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double* p, int pstride, int nv, int k,
-                                double s0, double s1, float* coef, int* err, hipStream_t st);
+                                double s0, double s1, double* coef, int* err, hipStream_t st);
 
 // ---------------------------------------------------------------- static
 // W_b = Linv_b G_b in place over G (fp32), colsum of squares in fp64 -> diag

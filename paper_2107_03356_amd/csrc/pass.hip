@@ -21,6 +21,8 @@
 // Pass 2: each wave owns one column chunk of the output and walks all m rows,
 // accumulating coef[i] * G[i, chunk] in registers (coefficients staged in LDS);
 // no cross-lane traffic.
+#include <type_traits>
+
 #include "device_util.h"
 #include "internal.h"
 
@@ -59,11 +61,20 @@ __global__ __launch_bounds__(256) void k_get_rows(const float* __restrict__ G, i
     st4(rows + (int64_t)r * ld, j, d, aligned, v);
 }
 
+// Accumulation precision of the passes: fp64 (exact products, fp64 sums) for
+// up to 4 fused vectors, fp32 per lane for wider fusions; the sums across
+// lanes, chunks and work-groups are fp64 either way.
+template <int NV>
+struct AccType {
+    static constexpr bool f64 = NV <= 4;
+    using T = typename std::conditional<f64, double, float>::type;
+};
+
 template <int NV, int U, int R>
 __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int m, int64_t d,
                                                int64_t nchunk, VecIn vin, int aligned,
                                                double* __restrict__ part) {
-    extern __shared__ float acc[];  // m * NV running sums
+    extern __shared__ double acc[];  // m * NV running sums (fp64)
     constexpr int CW = 256 * U;     // chunk width (floats): 64 lanes x float4 x U
     constexpr int CPS = SLAB / CW;  // chunks per slab
     static_assert(SLAB % CW == 0, "chunk must tile the slab");
@@ -71,7 +82,7 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int mnv = m * NV;
-    for (int t = threadIdx.x; t < mnv; t += 256) acc[t] = 0.f;
+    for (int t = threadIdx.x; t < mnv; t += 256) acc[t] = 0.0;
     __syncthreads();
 
     for (int64_t c = blockIdx.x; c < nchunk; c += gridDim.x) {
@@ -100,20 +111,29 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
             // keep all R*U loads in flight before the first use (the scheduler
             // otherwise recycles a few load registers and waits on each load)
             __builtin_amdgcn_sched_barrier(0);
-            // per-lane partial dots: value r*NV + v is row r's dot with vector v
-            float sv[R * NV];
+            // per-lane partial dots (value r*NV + v is row r's dot with vector
+            // v): in fp64, exact products of the fp32 values, for up to 4
+            // vectors; in fp32 for wider fusions, which would otherwise be
+            // bound by the fp64 conversions and FMAs
+            using T = typename AccType<NV>::T;
+            T sv[R * NV];
 #pragma unroll
             for (int v = 0; v < NV; ++v)
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
-                    float a = 0.f;
+                    T a = 0;
 #pragma unroll
-                    for (int u = 0; u < U; ++u) a = dot4(g[r][u], vr[v][u], a);
+                    for (int u = 0; u < U; ++u) {
+                        if constexpr (AccType<NV>::f64)
+                            a = dot4d(g[r][u], vr[v][u], a);
+                        else
+                            a = dot4(g[r][u], vr[v][u], a);
+                    }
                     sv[r * NV + v] = a;
                 }
             int idx;
             bool writer;
-            const float tot = wave_reduce_many<R * NV>(sv, lane, idx, writer);
+            const double tot = (double)wave_reduce_many<R * NV>(sv, lane, idx, writer);
             if (writer) {
                 const int r = idx / NV, v = idx - (idx / NV) * NV;
                 if (i + 4 * r < m) acc[(i + 4 * r) * NV + v] += tot;
@@ -122,7 +142,7 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
     }
     __syncthreads();
     double* out = part + (int64_t)blockIdx.x * mnv;
-    for (int t = threadIdx.x; t < mnv; t += 256) out[t] = (double)acc[t];
+    for (int t = threadIdx.x; t < mnv; t += 256) out[t] = acc[t];
 }
 
 __global__ __launch_bounds__(256) void k_reduce_partials(const double* __restrict__ part, int grid,
@@ -143,25 +163,32 @@ __global__ __launch_bounds__(256) void k_reduce_partials(const double* __restric
     }
 }
 
-// Row stride of the coefficients staged in LDS: with 3 or more vectors each
-// row is padded to a multiple of 4 so that it is read as 16-byte words (one
-// ds_read_b128 per 4 vectors instead of 4 scalar reads; +3% at 9 vectors),
-// when the padded table still fits the 64 KB the unpadded one is held to.
-template <int NV, bool PAD>
+// Row stride of the coefficients staged in LDS (in the accumulation type):
+// padded so that a row is read as 16-byte words (pairs of fp64, quads of
+// fp32 from 3 vectors on: +3% at 9 vectors over scalar reads).
+template <int NV>
 struct CoefStride {
-    static constexpr int P = (PAD && NV >= 3) ? (NV + 3) / 4 * 4 : NV;
+    static constexpr int W = AccType<NV>::f64 ? 2 : 4;  // values per 16 bytes
+    static constexpr int P = NV >= W / 2 + 1 ? (NV + W - 1) / W * W : NV;
 };
 
-template <int NV, int NP>
-__device__ __forceinline__ void coef_row(const float* __restrict__ row, float (&cv)[NP]) {
-    if constexpr (NP != NV) {
+template <int NV, int NP, typename T>
+__device__ __forceinline__ void coef_row(const T* __restrict__ row, T (&cv)[NP]) {
+    constexpr int W = 16 / sizeof(T);
+    if constexpr (NP % W == 0) {
 #pragma unroll
-        for (int q = 0; q < NP / 4; ++q) {
-            const float4 t = *reinterpret_cast<const float4*>(row + 4 * q);
-            cv[4 * q] = t.x;
-            cv[4 * q + 1] = t.y;
-            cv[4 * q + 2] = t.z;
-            cv[4 * q + 3] = t.w;
+        for (int q = 0; q < NP / W; ++q) {
+            if constexpr (W == 2) {
+                const double2 t = *reinterpret_cast<const double2*>(row + 2 * q);
+                cv[2 * q] = t.x;
+                cv[2 * q + 1] = t.y;
+            } else {
+                const float4 t = *reinterpret_cast<const float4*>(row + 4 * q);
+                cv[4 * q] = t.x;
+                cv[4 * q + 1] = t.y;
+                cv[4 * q + 2] = t.z;
+                cv[4 * q + 3] = t.w;
+            }
         }
     } else {
 #pragma unroll
@@ -169,18 +196,24 @@ __device__ __forceinline__ void coef_row(const float* __restrict__ row, float (&
     }
 }
 
-template <int NV, int U, bool PAD>
+// Pass 2: y_v = alpha_v x_v - sum_i coef[i][v] G[i, :], the coefficients and
+// sums in the accumulation type of AccType (fp64: each window value converted
+// once per row), rounded to fp32 on the store. Each wave owns a 256*U-column
+// chunk and walks all m rows with RB rows of loads in flight.
+template <int NV, int U>
 __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int m, int64_t d,
-                                               int64_t nwchunk, const float* __restrict__ coef,
+                                               int64_t nwchunk, const double* __restrict__ coef,
                                                VecOut vout, int aligned) {
-    constexpr int NP = CoefStride<NV, PAD>::P;
-    extern __shared__ float cl[];  // m rows of NP coefficients (NV used)
-    constexpr int WCW = 256 * U;   // wave chunk width (floats)
+    using T = typename AccType<NV>::T;
+    constexpr int NP = CoefStride<NV>::P;
+    extern __shared__ __align__(16) unsigned char cl_raw[];
+    T* cl = reinterpret_cast<T*>(cl_raw);  // m rows of NP coefficients (NV used)
+    constexpr int WCW = 256 * U;    // wave chunk width (floats)
     constexpr int CPS = SLAB / WCW;
     static_assert(SLAB % WCW == 0, "chunk must tile the slab");
     for (int t = threadIdx.x; t < m * NP; t += 256) {
         const int i = t / NP, v = t - (t / NP) * NP;
-        cl[t] = v < NV ? coef[i * NV + v] : 0.f;
+        cl[t] = v < NV ? (T)coef[i * NV + v] : T(0);
     }
     __syncthreads();
     const int lane = threadIdx.x & 63;
@@ -191,14 +224,29 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
     const int64_t j0 = slab * SLAB + off;
     const float* Gs = G + slab * (int64_t)m * SLAB + off + lane * 4;
 
-    float4 acc[NV][U];
+    T acc[NV][U][4];
 #pragma unroll
     for (int v = 0; v < NV; ++v)
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc[v][u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int u = 0; u < U; ++u) acc[v][u][0] = acc[v][u][1] = acc[v][u][2] = acc[v][u][3] = T(0);
 
     // RB rows per batch: all RB*U loads are issued before the first FMA
-    constexpr int RB = 8;
+    constexpr int RB = (AccType<NV>::f64 && NV > 2) ? 4 : 8;
+    auto fold = [&](const float4 (&g)[U], const T* crow) {
+        T cv[NP];
+        coef_row<NV, NP>(crow, cv);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const T gx = g[u].x, gy = g[u].y, gz = g[u].z, gw = g[u].w;
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                acc[v][u][0] = fma(cv[v], gx, acc[v][u][0]);
+                acc[v][u][1] = fma(cv[v], gy, acc[v][u][1]);
+                acc[v][u][2] = fma(cv[v], gz, acc[v][u][2]);
+                acc[v][u][3] = fma(cv[v], gw, acc[v][u][3]);
+            }
+        }
+    };
     int i = 0;
     for (; i + RB <= m; i += RB) {
         float4 g[RB][U];
@@ -208,37 +256,13 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
             for (int u = 0; u < U; ++u) g[r][u] = ld_stream(Gs + (int64_t)(i + r) * SLAB + u * 256);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int r = 0; r < RB; ++r) {
-            float cv[NP];
-            coef_row<NV, NP>(cl + (i + r) * NP, cv);
-#pragma unroll
-            for (int v = 0; v < NV; ++v) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    acc[v][u].x = fmaf(cv[v], g[r][u].x, acc[v][u].x);
-                    acc[v][u].y = fmaf(cv[v], g[r][u].y, acc[v][u].y);
-                    acc[v][u].z = fmaf(cv[v], g[r][u].z, acc[v][u].z);
-                    acc[v][u].w = fmaf(cv[v], g[r][u].w, acc[v][u].w);
-                }
-            }
-        }
+        for (int r = 0; r < RB; ++r) fold(g[r], cl + (i + r) * NP);
     }
     for (; i < m; ++i) {
         float4 g[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) g[u] = ld_stream(Gs + (int64_t)i * SLAB + u * 256);
-        float cv[NP];
-        coef_row<NV, NP>(cl + i * NP, cv);
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                acc[v][u].x = fmaf(cv[v], g[u].x, acc[v][u].x);
-                acc[v][u].y = fmaf(cv[v], g[u].y, acc[v][u].y);
-                acc[v][u].z = fmaf(cv[v], g[u].z, acc[v][u].z);
-                acc[v][u].w = fmaf(cv[v], g[u].w, acc[v][u].w);
-            }
-        }
+        fold(g, cl + i * NP);
     }
 
 #pragma unroll
@@ -250,10 +274,10 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
             float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
             if (a != 0.f) x = ld4(vout.x[v], j, d, aligned);
             float4 y;
-            y.x = a * x.x - acc[v][u].x;
-            y.y = a * x.y - acc[v][u].y;
-            y.z = a * x.z - acc[v][u].z;
-            y.w = a * x.w - acc[v][u].w;
+            y.x = (float)((T)a * (T)x.x - acc[v][u][0]);
+            y.y = (float)((T)a * (T)x.y - acc[v][u][1]);
+            y.z = (float)((T)a * (T)x.z - acc[v][u][2]);
+            y.w = (float)((T)a * (T)x.w - acc[v][u][3]);
             st4(vout.y[v], j, d, aligned, y);
         }
     }
@@ -274,10 +298,10 @@ struct PassCfg {
     // float4 per lane per row. Pass 1 keeps the vector chunks in registers
     // (<= ~72 VGPRs); pass 2 uses narrow 512-column wave chunks with 8 rows in
     // flight, which measured fastest on the 105 GB window.
-    static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 9 ? 2 : 1;
+    static constexpr int U = NV == 1 ? 8 : NV <= 3 ? 4 : NV <= 9 ? 2 : 1;
     // rows per pass-1 iteration: 4 where the register-resident vectors leave
     // room, so 2U-wide rows keep 4R loads in flight per lane
-    static constexpr int R = (NV >= 3 && NV <= 16) ? 4 : 2;
+    static constexpr int R = NV <= 3 ? 1 : NV <= 16 ? (NV == 4 ? 2 : 4) : 2;
     static constexpr int U2 = NV <= 2 ? 2 : 1;
 };
 
@@ -287,7 +311,17 @@ hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn
     constexpr int U = PassCfg<NV>::U, R = PassCfg<NV>::R;
     const int64_t nchunk = nslab * (SLAB / (256 * U));
     const int grid = (int)(nchunk < PASS1_MAX_GRID ? nchunk : PASS1_MAX_GRID);
-    const size_t lds = (size_t)m * NV * sizeof(float);
+    const size_t lds = (size_t)m * NV * sizeof(double);
+    if (lds > 65536) {
+        // fp64 row sums of up to 16384 values: up to 128 KB of the 160 KB LDS
+        static bool raised = false;
+        if (!raised) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass1<NV, U, R>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            if (e != hipSuccess) return e;
+            raised = true;
+        }
+    }
     hipLaunchKernelGGL((k_pass1<NV, U, R>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
                        aligned ? 1 : 0, part);
     *grid_out = grid;
@@ -295,22 +329,26 @@ hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn
 }
 
 template <int NV>
-hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const float* coef,
+hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const double* coef,
                     const VecOut& vout, bool aligned, hipStream_t st) {
     constexpr int U = PassCfg<NV>::U2;
     const int64_t nwchunk = nslab * (SLAB / (256 * U));
     const int64_t grid = ceil_div(nwchunk, 4);
-    if ((int64_t)m * CoefStride<NV, true>::P <= 16384) {
-        const size_t lds = (size_t)m * CoefStride<NV, true>::P * sizeof(float);
-        hipLaunchKernelGGL((k_pass2<NV, U, true>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk,
-                           coef, vout, aligned ? 1 : 0);
-    } else {
-        const size_t lds = (size_t)m * NV * sizeof(float);
-        hipLaunchKernelGGL((k_pass2<NV, U, false>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk,
-                           coef, vout, aligned ? 1 : 0);
+    const size_t lds = (size_t)m * CoefStride<NV>::P * sizeof(typename AccType<NV>::T);
+    if (lds > 65536) {
+        static bool raised = false;
+        if (!raised) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2<NV, U>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            if (e != hipSuccess) return e;
+            raised = true;
+        }
     }
+    hipLaunchKernelGGL((k_pass2<NV, U>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk, coef, vout,
+                       aligned ? 1 : 0);
     return hipGetLastError();
 }
+
 
 }  // namespace
 
@@ -370,7 +408,7 @@ hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double*
     return hipGetLastError();
 }
 
-hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv, const float* coef,
+hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv, const double* coef,
                         const VecOut& vout, bool aligned, hipStream_t st) {
     switch (nv) {
 #define CASE(N) \

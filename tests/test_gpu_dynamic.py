@@ -298,6 +298,44 @@ def test_long_run_inverse_updates_do_not_drift(dev):
     assert max(errs) < 1e-5, errs
 
 
+@pytest.mark.parametrize("d,m,lam,q", [
+    (96, 256, 1e-6, 0),      # m > d: K has rank 96 of 256, A's condition number ~1e5
+    (300, 512, 1e-7, 0),     # rank 300 of 512, condition number ~1e6
+    (96, 256, 1e-6, 3),      # the same with 3 fused queries (4 vectors: fp64 passes)
+])
+def test_rank_deficient_window_long_run(dev, d, m, lam, q):
+    """More gradients than coordinates and a small damping: A = K + m*lambda*I
+    is ill-conditioned; 700 replaces of O(m^2) inverse updates, no refactor.
+    With fp32 sums in the passes the IHVP error grows with the condition
+    number (1e-3 here); fp64 sums keep it at the fp32 rounding of the data."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_tiny_d4096_m16")
+    wl = base.scaled(d=d, m=m, lam=lam, fill_by_replace=False)
+    gs = GradientStream(wl, seed=15)
+    G0 = gs.window()
+    say("rank-deficient long run", d, m, lam, q)
+    win = Window(wl.d, wl.m, wl.lam, max_queries=q, G0=G0.to(dev), device=dev)
+    win.set_refactor_period(100000)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    errs = []
+    for t in range(700):
+        g = gs.row(wl.m + t)
+        check = t % 50 == 49
+        if q:
+            X = gs.queries(t, q)
+            y, Y = win.replace(g.to(dev), X=X.to(dev))
+        else:
+            y = win.replace(g.to(dev))
+        yo = orc.slide(g.numpy())
+        if check:
+            errs.append(rel_l2(y.cpu().numpy(), yo))
+            if q:
+                Yo = orc.ihvp(X.numpy())
+                errs += [rel_l2(Y[j].cpu().numpy(), Yo[j]) for j in range(q)]
+    assert win.status() == 0
+    assert max(errs) < 1e-5, max(errs)
+
+
 def test_default_policy_over_a_refactor_boundary_m1024(dev):
     """m = 1024 with the default coefficient policy (O(m^2) inverse updates,
     full refactor every 1024 replaces): 1100 steps, checked right before,
