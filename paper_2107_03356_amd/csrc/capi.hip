@@ -75,7 +75,8 @@ struct mfac_static_s {
     hipStream_t st;
     int* err;
     double *A, *Linv, *gpart, *diag, *scores, *qpart;
-    float *qcoef, *xobs;
+    double* qcoef;
+    float* xobs;
     SelectScratch sel;
     // stage tracing (MFAC_STATIC_TRACE): events recorded around the stages
     bool trace;
@@ -509,7 +510,7 @@ size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
     double* Linv = c.take<double>((size_t)batch * mp * mp);
     double* gpart = c.take<double>((size_t)static_gram_part(d / B, batch, mp, B));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
-    float* qcoef = c.take<float>((size_t)(d / B) * m * 4);
+    double* qcoef = c.take<double>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
     if (s) {
         s->qpart = qpart;
@@ -719,7 +720,7 @@ size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* b
     double* Linv = c.take<double>((size_t)pl.pb * mp * mp);
     double* gpart = c.take<double>((size_t)(pa > pb2 ? pa : pb2));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
-    float* qcoef = c.take<float>((size_t)(d / B) * m * 4);
+    double* qcoef = c.take<double>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
     float* pg[3];
     for (int i = 0; i < 3; ++i) pg[i] = c.take<float>((size_t)m * pl.pc);

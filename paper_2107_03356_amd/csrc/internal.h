@@ -117,7 +117,7 @@ hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, Selec
 int64_t static_query_part_doubles(int64_t d, int B, int m);
 // Y = alpha X - W_b^T (pscale W_b X) per block, n <= 4 vectors (row-major, stride d)
 hipError_t launch_static_ihvp(const float* W, int m, int64_t d, int B, int n, const float* X, float alpha,
-                              double pscale, float* Y, double* part, float* coef, hipStream_t st);
+                              double pscale, float* Y, double* part, double* coef, hipStream_t st);
 hipError_t launch_obs_x(const float* theta, const uint8_t* keep, const double* diag, int64_t d, float* x,
                         hipStream_t st);
 hipError_t launch_static_element(const float* W, int m, int64_t d, int B, int64_t nq, const int64_t* ij, double lam,

@@ -17,11 +17,12 @@ namespace {
 int64_t static_query_main_doubles(int64_t d, int B, int m) { return (d / B) * ceil_div(B, 512) * (int64_t)m * 4; }
 
 // Pass 1: one work-group per column chunk of width 256*U inside one block.
-// part[c][i*NV + v] = sum_{j in chunk c} W[i, j] x_v[j].
+// part[c][i*NV + v] = sum_{j in chunk c} W[i, j] x_v[j]: exact products of the
+// fp32 values summed in fp64; each (row, vector) sum of the chunk comes from
+// one wave and is stored directly.
 template <int NV, int U>
 __global__ __launch_bounds__(256) void k_sq_pass1(const float* __restrict__ W, int m, int64_t d, int B, int cpb,
                                                   const float* __restrict__ X, double* __restrict__ part) {
-    extern __shared__ float acc[];
     constexpr int CW = 256 * U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int mnv = m * NV;
@@ -30,14 +31,13 @@ __global__ __launch_bounds__(256) void k_sq_pass1(const float* __restrict__ W, i
     const int64_t j0 = (int64_t)b * B + (int64_t)cb * CW;
     int64_t jend = (int64_t)(b + 1) * B;
     if (jend > j0 + CW) jend = j0 + CW;
-    for (int t = threadIdx.x; t < mnv; t += 256) acc[t] = 0.f;
+    double* out = part + (int64_t)c * mnv;
 
     float4 vr[NV][U];
 #pragma unroll
     for (int v = 0; v < NV; ++v)
 #pragma unroll
         for (int u = 0; u < U; ++u) vr[v][u] = ld4(X + (int64_t)v * d, j0 + u * 256 + lane * 4, jend, 1);
-    __syncthreads();
 
     for (int i = wave; i < m; i += 8) {
         const bool has2 = i + 4 < m;
@@ -49,42 +49,39 @@ __global__ __launch_bounds__(256) void k_sq_pass1(const float* __restrict__ W, i
             ga[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
             gb[u] = (j < jend) ? ld_stream(W + (int64_t)i2 * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        float sv[2 * NV];
+        double sv[2 * NV];
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-            float a = 0.f, bb = 0.f;
+            double a = 0.0, bb = 0.0;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                a = dot4(ga[u], vr[v][u], a);
-                bb = dot4(gb[u], vr[v][u], bb);
+                a = dot4d(ga[u], vr[v][u], a);
+                bb = dot4d(gb[u], vr[v][u], bb);
             }
             sv[v] = a;
             sv[NV + v] = bb;
         }
         int idx;
         bool writer;
-        const float tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
+        const double tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
         if (writer) {
             if (idx < NV)
-                acc[i * NV + idx] += tot;
+                out[i * NV + idx] = tot;
             else if (has2)
-                acc[i2 * NV + (idx - NV)] += tot;
+                out[i2 * NV + (idx - NV)] = tot;
         }
     }
-    __syncthreads();
-    double* out = part + (int64_t)c * mnv;
-    for (int t = threadIdx.x; t < mnv; t += 256) out[t] = (double)acc[t];
 }
 
 // coef[b][t] = scale * sum_{cb < cpb} part[b*cpb + cb][t]   (fixed order, fp64)
 __global__ __launch_bounds__(256) void k_sq_reduce(const double* __restrict__ part, int cpb, int mnv, double scale,
-                                                   float* __restrict__ coef) {
+                                                   double* __restrict__ coef) {
     const int b = blockIdx.y;
     const int t = blockIdx.x * 256 + threadIdx.x;
     if (t >= mnv) return;
     double s = 0.0;
     for (int cb = 0; cb < cpb; ++cb) s += part[((int64_t)b * cpb + cb) * mnv + t];
-    coef[(int64_t)b * mnv + t] = (float)(scale * s);
+    coef[(int64_t)b * mnv + t] = scale * s;
 }
 
 // Wide blocks (many chunks per block): first sum segments of SEG chunks in
@@ -104,10 +101,11 @@ __global__ __launch_bounds__(256) void k_sq_reduce_seg(const double* __restrict_
 }
 
 // Pass 2: one wave per 256*U-column chunk of one block:
-// y_v[j] = alpha * x_v[j] - sum_i coef[b][i*NV + v] W[i, j].
+// y_v[j] = alpha * x_v[j] - sum_i coef[b][i*NV + v] W[i, j], summed in fp64
+// (fp64 coefficients times fp32 W) and rounded to fp32 once.
 template <int NV, int U>
 __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, int m, int64_t d, int B, int cpb2,
-                                                  int64_t nwchunk, const float* __restrict__ coef,
+                                                  int64_t nwchunk, const double* __restrict__ coef,
                                                   const float* __restrict__ X, float alpha, float* __restrict__ Y) {
     constexpr int WCW = 256 * U;
     const int lane = threadIdx.x & 63;
@@ -117,13 +115,15 @@ __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, i
     const int64_t j0 = (int64_t)b * B + (int64_t)cb * WCW;
     int64_t jend = (int64_t)(b + 1) * B;
     if (jend > j0 + WCW) jend = j0 + WCW;
-    const float* cf = coef + (int64_t)b * m * NV;
+    const double* cf = coef + (int64_t)b * m * NV;
 
-    float4 acc[NV][U];
+    double acc[NV][U][4];
 #pragma unroll
     for (int v = 0; v < NV; ++v)
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc[v][u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc[v][u][k] = 0.0;
     for (int i = 0; i < m; ++i) {
         float4 g[U];
 #pragma unroll
@@ -133,13 +133,13 @@ __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, i
         }
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-            const float cv = cf[i * NV + v];
+            const double cv = cf[i * NV + v];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                acc[v][u].x = fmaf(cv, g[u].x, acc[v][u].x);
-                acc[v][u].y = fmaf(cv, g[u].y, acc[v][u].y);
-                acc[v][u].z = fmaf(cv, g[u].z, acc[v][u].z);
-                acc[v][u].w = fmaf(cv, g[u].w, acc[v][u].w);
+                acc[v][u][0] = fma(cv, (double)g[u].x, acc[v][u][0]);
+                acc[v][u][1] = fma(cv, (double)g[u].y, acc[v][u][1]);
+                acc[v][u][2] = fma(cv, (double)g[u].z, acc[v][u][2]);
+                acc[v][u][3] = fma(cv, (double)g[u].w, acc[v][u][3]);
             }
         }
     }
@@ -151,10 +151,11 @@ __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, i
             if (j < jend) {
                 const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)v * d + j);
                 float4 y;
-                y.x = alpha * x.x - acc[v][u].x;
-                y.y = alpha * x.y - acc[v][u].y;
-                y.z = alpha * x.z - acc[v][u].z;
-                y.w = alpha * x.w - acc[v][u].w;
+                const double a = alpha;
+                y.x = (float)(a * x.x - acc[v][u][0]);
+                y.y = (float)(a * x.y - acc[v][u][1]);
+                y.z = (float)(a * x.z - acc[v][u][2]);
+                y.w = (float)(a * x.w - acc[v][u][3]);
                 *reinterpret_cast<float4*>(Y + (int64_t)v * d + j) = y;
             }
         }
@@ -202,12 +203,11 @@ struct SqCfg {
 
 template <int NV>
 hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, float alpha, double pscale, float* Y,
-                      double* part, float* coef, hipStream_t st) {
+                      double* part, double* coef, hipStream_t st) {
     constexpr int U = SqCfg<NV>::U, U2 = SqCfg<NV>::U2;
     const int nblocks = (int)(d / B);
     const int cpb = (int)ceil_div(B, 256 * U);
-    const size_t lds = (size_t)m * NV * sizeof(float);
-    hipLaunchKernelGGL((k_sq_pass1<NV, U>), dim3((unsigned)(nblocks * cpb)), dim3(256), lds, st, W, m, d, B, cpb, X,
+    hipLaunchKernelGGL((k_sq_pass1<NV, U>), dim3((unsigned)(nblocks * cpb)), dim3(256), 0, st, W, m, d, B, cpb, X,
                        part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -242,7 +242,7 @@ int64_t static_query_part_doubles(int64_t d, int B, int m) {
 }
 
 hipError_t launch_static_ihvp(const float* W, int m, int64_t d, int B, int n, const float* X, float alpha,
-                              double pscale, float* Y, double* part, float* coef, hipStream_t st) {
+                              double pscale, float* Y, double* part, double* coef, hipStream_t st) {
     switch (n) {
         case 1: return sq_ihvp_nv<1>(W, m, d, B, X, alpha, pscale, Y, part, coef, st);
         case 2: return sq_ihvp_nv<2>(W, m, d, B, X, alpha, pscale, Y, part, coef, st);
