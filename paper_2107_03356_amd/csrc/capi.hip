@@ -18,7 +18,7 @@ using namespace mfac;
 namespace {
 
 constexpr int MAX_QUERIES = 16;
-constexpr int64_t MAX_MNV = 16384;  // m * (max_queries + 1), bounds the pass-1 LDS (64 KB)
+constexpr int64_t MAX_MNV = 16384;  // m * (max_queries + 1): the pass LDS stays within 128 KB
 constexpr int64_t STATIC_BATCH_BYTES = int64_t(8) << 30;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }

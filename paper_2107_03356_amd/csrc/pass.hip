@@ -163,13 +163,15 @@ __global__ __launch_bounds__(256) void k_reduce_partials(const double* __restric
     }
 }
 
-// Row stride of the coefficients staged in LDS (in the accumulation type):
-// padded so that a row is read as 16-byte words (pairs of fp64, quads of
-// fp32 from 3 vectors on: +3% at 9 vectors over scalar reads).
+// Row stride of the coefficients staged in LDS (in the accumulation type).
+// fp32 rows from 3 vectors on are padded to quads and read as 16-byte words
+// (+3% at 9 vectors over scalar reads); at most m * (NV + 3) * 4 <= 105 KB
+// under m * NV <= 16384. fp64 rows stay unpadded (2 and 4 vectors are still
+// read as pairs): m * NV * 8 <= 128 KB, where padding 3 vectors to 4 would
+// pass the 160 KB of LDS above m = 5120.
 template <int NV>
 struct CoefStride {
-    static constexpr int W = AccType<NV>::f64 ? 2 : 4;  // values per 16 bytes
-    static constexpr int P = NV >= W / 2 + 1 ? (NV + W - 1) / W * W : NV;
+    static constexpr int P = AccType<NV>::f64 ? NV : NV >= 3 ? (NV + 3) / 4 * 4 : NV;
 };
 
 template <int NV, int NP, typename T>

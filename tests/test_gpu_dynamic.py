@@ -89,6 +89,7 @@ def test_tiny_init_equals_fill(dev):
     (8192, 4096, 1e-3, 1, "gauss"),                # m = 4096: 528 Gram tiles, six recursion levels
     (12000, 1500, 1e-4, 9, "lognormal"),           # 10 vectors at m = 1500: pass-2 coefficient rows left unpadded (LDS bound)
     (9000, 300, 1e-4, 16, "gauss"),                # the most fused vectors (17), padded rows of 20
+    (4000, 5461, 1e-2, 2, "gauss"),                # 3 vectors at the largest m (m * 3 = 16383): fp64 LDS rows
 ])
 def test_ragged_and_multitile_with_queries(dev, d, m, lam, q, dist):
     base = get_workload("dyn_resnet18_d11.2m_m1024_q8")
@@ -109,7 +110,7 @@ def test_d1m_m256_full_size(dev):
 
 def test_largest_window_m16384(dev):
     """The largest window the library accepts without queries (m = 16384: the
-    pass-1 row sums fill 64 KB of LDS), over a short d; two sliding steps."""
+    fp64 pass-1 row sums fill 128 KB of LDS), over a short d; two sliding steps."""
     base = get_workload("dyn_tiny_d4096_m16")
     wl = base.scaled(d=2048, m=16384, lam=1e-2, fill_by_replace=False)
     say("largest window m16384")
