@@ -315,14 +315,12 @@ hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn
     const int grid = (int)(nchunk < PASS1_MAX_GRID ? nchunk : PASS1_MAX_GRID);
     const size_t lds = (size_t)m * NV * sizeof(double);
     if (lds > 65536) {
-        // fp64 row sums of up to 16384 values: up to 128 KB of the 160 KB LDS
-        static bool raised = false;
-        if (!raised) {
-            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass1<NV, U, R>),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-            if (e != hipSuccess) return e;
-            raised = true;
-        }
+        // fp64 row sums of up to 16384 values: up to 128 KB of the 160 KB LDS.
+        // Set on every such launch: the attribute is per device, and the call
+        // is cheap next to a pass over the window.
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass1<NV, U, R>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL((k_pass1<NV, U, R>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
                        aligned ? 1 : 0, part);
@@ -338,13 +336,10 @@ hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const doubl
     const int64_t grid = ceil_div(nwchunk, 4);
     const size_t lds = (size_t)m * CoefStride<NV>::P * sizeof(typename AccType<NV>::T);
     if (lds > 65536) {
-        static bool raised = false;
-        if (!raised) {
-            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2<NV, U>),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-            if (e != hipSuccess) return e;
-            raised = true;
-        }
+        // set on every such launch (per device; cheap next to the pass)
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2<NV, U>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL((k_pass2<NV, U>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk, coef, vout,
                        aligned ? 1 : 0);
