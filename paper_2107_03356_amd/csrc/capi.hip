@@ -318,7 +318,7 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
     for (int q = 0; q < n; ++q) vin.v[1 + q] = X + (int64_t)q * d;
     if (n > 0) al = al && aligned16(X) && aligned16(Y) && (d % 4 == 0);
 
-    int grid = 0;
+    Pass1Grid grid{};
     HIPCHK(mark_begin(w));
     HIPCHK(launch_write_row(w->G, w->m, d, w->nslab, k, g_new, w->st));
     HIPCHK(mark_end(w, 3));
@@ -326,7 +326,7 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
     HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, nv, vin, al, w->part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_reduce_partials(w->part, grid, w->m * nv, w->p, w->st));
+    HIPCHK(launch_reduce_partials(w->part, grid, w->m, nv, w->p, w->st));
     mfac_status rc = window_slot_update(w, nv, k);
     if (rc != MFAC_OK) return rc;
 
@@ -378,12 +378,12 @@ MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* 
         vout.y[q] = Y + (int64_t)q * d;
         vout.alpha[q] = (float)inv_lam;
     }
-    int grid = 0;
+    Pass1Grid grid{};
     HIPCHK(mark_begin(w));
     HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, n, vin, al, w->part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_reduce_partials(w->part, grid, w->m * n, w->p, w->st));
+    HIPCHK(launch_reduce_partials(w->part, grid, w->m, n, w->p, w->st));
     HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p, n, n, -1, inv_lam, inv_lam, w->coef, w->err, w->st));
     HIPCHK(mark_end(w, 1));
     HIPCHK(mark_begin(w));

@@ -40,12 +40,18 @@ hipError_t launch_get_rows(const float* G, int m, int64_t d, int first, int coun
                            float* rows, int64_t ld, hipStream_t st);
 // Row k of the window <- g (d floats; zero padding past d).
 hipError_t launch_write_row(float* G, int m, int64_t d, int64_t nslab, int k, const float* g, hipStream_t st);
-// Pass 1: part[b][i*nv+v] = partial sums of G[i,:] . vec_v over the chunks of
-// work-group b. Returns the grid size.
+// Pass-1 launch shape: gx work-groups per row group, ng row groups of mg rows
+// (the last may hold fewer); gx * ng <= PASS1_MAX_GRID.
+struct Pass1Grid {
+    int gx, ng, mg;
+};
+// Pass 1: partial sums of G[i,:] . vec_v over the chunks of each work-group,
+// part[(g * gx + b) * mg * nv + (i - g * mg) * nv + v] for work-group b of
+// row group g = i / mg. Returns the launch shape.
 hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv,
-                        const VecIn& vin, bool aligned, double* part, int* grid_out, hipStream_t st);
-// p[t] = sum_b part[b][t] for t < mnv (fixed order, fp64)
-hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double* p,
+                        const VecIn& vin, bool aligned, double* part, Pass1Grid* grid_out, hipStream_t st);
+// p[i*nv + v] = sum over the work-groups of row i's group (fixed order, fp64)
+hipError_t launch_reduce_partials(const double* part, const Pass1Grid& pg, int m, int nv, double* p,
                                   hipStream_t st);
 // Pass 2: y_v = alpha_v x_v - sum_i coef[i*nv+v] G[i,:] (fp64 coefficients and
 // accumulation, fp32 output)
@@ -54,7 +60,7 @@ hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv,
 
 // ---------------------------------------------------------------- Gram
 // Window Gram: K (m x m, fp64, full symmetric) = sum over slabs of G_s G_s^T,
-// fp32 MFMA tiles with fp64 flushes; part must hold gram_window_part_doubles().
+// fp64 MFMA tiles; part must hold gram_window_part_doubles().
 int64_t gram_window_part_doubles(int m, int64_t nslab);
 hipError_t launch_gram_window(const float* G, int m, int64_t nslab, double* part, double* K,
                               hipStream_t st);

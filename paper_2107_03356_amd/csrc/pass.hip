@@ -10,17 +10,21 @@
 // floats of traffic), so both passes below are pure read streams: interleaving
 // that write with pass 1's reads cost ~8% of pass 1's bandwidth on gfx950.
 //
-// Pass 1: every work-group owns a set of column chunks and keeps per-row
-// running sums in LDS. A wave takes R rows at a time, loads U float4 per lane
-// and row (128-bit coalesced loads), multiplies with the register-resident
-// vector chunks and reduces the R x NV sums across the wave with lane
-// shuffles. Work-group partials go to a
-// [grid][m*nv] fp64 buffer, summed in a fixed order by the reduce kernel
-// (deterministic, no float atomics).
+// Pass 1: every work-group owns a set of column chunks (and, when m * NV is
+// large, one group of rows) and keeps per-row running sums in LDS. A wave
+// takes R rows at a time, loads U float4 per lane and row (128-bit coalesced
+// loads), multiplies with the register-resident vector chunks and reduces the
+// R x NV sums across the wave with lane shuffles. Work-group partials go to a
+// fp64 buffer, summed in a fixed order by the reduce kernel (deterministic,
+// no float atomics).
 //
-// Pass 2: each wave owns one column chunk of the output and walks all m rows,
-// accumulating coef[i] * G[i, chunk] in registers (coefficients staged in LDS);
-// no cross-lane traffic.
+// Pass 2, one vector (m <= 4096): each work-group owns whole slabs; its four
+// waves take interleaved rows across the full slab width, so the work-group
+// streams 32 KB-contiguous blocks as pass 1 does, and the four fp64 column
+// partials of a slab are summed through LDS. Pass 2, several vectors: each
+// wave owns one column chunk of the output and walks all m rows, accumulating
+// coef[i] * G[i, chunk] in registers (coefficients staged in LDS); no
+// cross-lane traffic.
 #include <type_traits>
 
 #include "device_util.h"
@@ -70,19 +74,24 @@ struct AccType {
     using T = typename std::conditional<f64, double, float>::type;
 };
 
+// Work-group (x, y) takes chunks x, x + gridDim.x, ... of rows
+// [y * mg, min(m, (y + 1) * mg)) and writes its row sums to
+// part[(y * gridDim.x + x) * mg * NV + (row - y * mg) * NV + v].
 template <int NV, int U, int R>
-__global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int m, int64_t d,
+__global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int m, int mg, int64_t d,
                                                int64_t nchunk, VecIn vin, int aligned,
                                                double* __restrict__ part) {
-    extern __shared__ double acc[];  // m * NV running sums (fp64)
+    extern __shared__ double acc[];  // mg * NV running sums (fp64)
     constexpr int CW = 256 * U;     // chunk width (floats): 64 lanes x float4 x U
     constexpr int CPS = SLAB / CW;  // chunks per slab
     static_assert(SLAB % CW == 0, "chunk must tile the slab");
     static_assert(R * NV <= 64, "one wave reduces at most 64 sums at a time");
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int mnv = m * NV;
-    for (int t = threadIdx.x; t < mnv; t += 256) acc[t] = 0.0;
+    const int r0 = blockIdx.y * mg;
+    const int r1 = r0 + mg < m ? r0 + mg : m;
+    const int nv_rows = (r1 - r0) * NV;
+    for (int t = threadIdx.x; t < nv_rows; t += 256) acc[t] = 0.0;
     __syncthreads();
 
     for (int64_t c = blockIdx.x; c < nchunk; c += gridDim.x) {
@@ -99,10 +108,10 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
 
         // R rows per iteration: rows i, i + 4, ..., i + 4(R-1) of this wave; a
         // missing row re-reads row i and its sums are dropped (no branch around loads)
-        for (int i = wave; i < m; i += 4 * R) {
+        for (int i = r0 + wave; i < r1; i += 4 * R) {
             int row[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) row[r] = i + 4 * r < m ? i + 4 * r : i;
+            for (int r = 0; r < R; ++r) row[r] = i + 4 * r < r1 ? i + 4 * r : i;
             float4 g[R][U];
 #pragma unroll
             for (int r = 0; r < R; ++r)
@@ -136,24 +145,31 @@ __global__ __launch_bounds__(256) void k_pass1(const float* __restrict__ G, int 
             const double tot = (double)wave_reduce_many<R * NV>(sv, lane, idx, writer);
             if (writer) {
                 const int r = idx / NV, v = idx - (idx / NV) * NV;
-                if (i + 4 * r < m) acc[(i + 4 * r) * NV + v] += tot;
+                if (i + 4 * r < r1) acc[(i + 4 * r - r0) * NV + v] += tot;
             }
         }
     }
     __syncthreads();
-    double* out = part + (int64_t)blockIdx.x * mnv;
-    for (int t = threadIdx.x; t < mnv; t += 256) out[t] = acc[t];
+    double* out = part + ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * mg * NV;
+    for (int t = threadIdx.x; t < nv_rows; t += 256) out[t] = acc[t];
 }
 
-__global__ __launch_bounds__(256) void k_reduce_partials(const double* __restrict__ part, int grid,
+// p[row * nv + v] = sum over the gx work-groups of the row's group of their
+// partials (layout of k_pass1), in a fixed order.
+__global__ __launch_bounds__(256) void k_reduce_partials(const double* __restrict__ part, Pass1Grid pg, int nv,
                                                          int mnv, double* __restrict__ p) {
     __shared__ double red[16][17];
     const int to = threadIdx.x & 15;
     const int bg = threadIdx.x >> 4;
     const int t = blockIdx.x * 16 + to;
     double s = 0.0;
-    if (t < mnv)
-        for (int b = bg; b < grid; b += 16) s += part[(int64_t)b * mnv + t];
+    if (t < mnv) {
+        const int row = t / nv, v = t - (t / nv) * nv;
+        const int g = row / pg.mg;
+        const int64_t stride = (int64_t)pg.mg * nv;
+        const double* src = part + (int64_t)g * pg.gx * stride + (int64_t)(row - g * pg.mg) * nv + v;
+        for (int b = bg; b < pg.gx; b += 16) s += src[b * stride];
+    }
     red[bg][to] = s;
     __syncthreads();
     if (bg == 0 && t < mnv) {
@@ -285,6 +301,89 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
     }
 }
 
+// Pass 2 for one vector, y = alpha x - G^T coef, m <= 4096. Work-group b
+// takes slabs b, b + gridDim.x, ...; wave w folds rows w, w + 4, ... over the
+// full slab width (8 float4 per lane), issuing the next row's loads as soon
+// as a row is folded and the next slab's first row before the slab's
+// reduction. The four fp64 column partials of a slab go through LDS (two
+// buffers, so one LDS barrier per slab) and are summed in a fixed order.
+__device__ __forceinline__ void load_slab_row(float4 (&g)[8], const float* __restrict__ G, int m, int64_t s, int i,
+                                              int lane) {
+    const float* p = G + (s * m + i) * (int64_t)SLAB + lane * 4;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) g[u] = ld_stream(p + u * 256);
+}
+
+// Waits for this wave's LDS operations, then for every wave of the
+// work-group; outstanding global loads stay in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+constexpr int PASS2_ROWS_MAX_M = 4096;  // m coefficients + 2 x 4 x SLAB partials = 160 KB of LDS
+constexpr int PASS2_ROWS_GRID = 256;    // one work-group per CU (the LDS holds one)
+
+__global__ __launch_bounds__(256) void k_pass2_rows(const float* __restrict__ G, int m, int64_t d, int64_t nslab,
+                                                    const double* __restrict__ coef, VecOut vout, int aligned) {
+    extern __shared__ __align__(16) double sh[];
+    const int mpad = (m + 1) & ~1;  // keeps the partials 16-byte aligned
+    double* cl = sh;
+    double* red = sh + mpad;  // [2][4][SLAB]
+    for (int t = threadIdx.x; t < m; t += 256) cl[t] = coef[t];
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float alpha = vout.alpha[0];
+    const float* __restrict__ x = vout.x[0];
+    float* __restrict__ y = vout.y[0];
+    float4 g[8];
+    int64_t s = blockIdx.x;
+    if (s < nslab && wave < m) load_slab_row(g, G, m, s, wave, lane);
+    for (int t = 0; s < nslab; s += gridDim.x, ++t) {
+        double acc[8][4];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[u][0] = acc[u][1] = acc[u][2] = acc[u][3] = 0.0;
+        for (int i = wave; i < m; i += 4) {
+            const double cv = cl[i];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                acc[u][0] = fma(cv, (double)g[u].x, acc[u][0]);
+                acc[u][1] = fma(cv, (double)g[u].y, acc[u][1]);
+                acc[u][2] = fma(cv, (double)g[u].z, acc[u][2]);
+                acc[u][3] = fma(cv, (double)g[u].w, acc[u][3]);
+            }
+            if (i + 4 < m)
+                load_slab_row(g, G, m, s, i + 4, lane);
+            else if (s + gridDim.x < nslab)
+                load_slab_row(g, G, m, s + gridDim.x, wave, lane);
+        }
+        double* rb = red + (t & 1) * 4 * SLAB;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            double* q = rb + wave * SLAB + u * 256 + lane * 4;
+            *reinterpret_cast<double2*>(q) = make_double2(acc[u][0], acc[u][1]);
+            *reinterpret_cast<double2*>(q + 2) = make_double2(acc[u][2], acc[u][3]);
+        }
+        lds_barrier();
+        // wave w writes columns [512 w, 512 w + 512) of the slab
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int col = wave * 512 + h * 256 + lane * 4;
+            const int64_t j = s * SLAB + col;
+            double sum[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                sum[k] = rb[col + k] + rb[SLAB + col + k] + rb[2 * SLAB + col + k] + rb[3 * SLAB + col + k];
+            float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (alpha != 0.f) xv = ld4(x, j, d, aligned);
+            const double a = alpha;
+            float4 o;
+            o.x = (float)(a * xv.x - sum[0]);
+            o.y = (float)(a * xv.y - sum[1]);
+            o.z = (float)(a * xv.z - sum[2]);
+            o.w = (float)(a * xv.w - sum[3]);
+            st4(y, j, d, aligned, o);
+        }
+    }
+}
+
 // The new gradient into row k of the window (padding past d stays zero).
 __global__ __launch_bounds__(256) void k_write_row(float* __restrict__ G, int m, int64_t d, int64_t ncolpad,
                                                    int k, const float* __restrict__ g, int aligned) {
@@ -297,40 +396,73 @@ __global__ __launch_bounds__(256) void k_write_row(float* __restrict__ G, int m,
 
 template <int NV>
 struct PassCfg {
-    // float4 per lane per row. Pass 1 keeps the vector chunks in registers
-    // (<= ~72 VGPRs); pass 2 uses narrow 512-column wave chunks with 8 rows in
-    // flight, which measured fastest on the 105 GB window.
-    static constexpr int U = NV == 1 ? 8 : NV <= 3 ? 4 : NV <= 9 ? 2 : 1;
-    // rows per pass-1 iteration: 4 where the register-resident vectors leave
-    // room, so 2U-wide rows keep 4R loads in flight per lane
-    static constexpr int R = NV <= 3 ? 1 : NV <= 16 ? (NV == 4 ? 2 : 4) : 2;
+    // Pass 1: U float4 per lane and row (the vector chunks stay in registers),
+    // R rows per wave iteration, GRID work-groups. Measured on the 105 GB
+    // window (m = 1024) over U in {1, 2, 4, 8}, R in {1, ..., 8} and grids of
+    // 256 / 384 / 512: one or two vectors stream best from one work-group per
+    // CU (7.4 TB/s against 6.95 at two per CU); wider fusions need two.
+    static constexpr int U = NV <= 4 ? 4 : 2;
+    static constexpr int R = NV <= 2 ? 2 : NV <= 4 ? 1 : NV <= 7 ? 2 : NV <= 10 ? 3 : 2;
+    static constexpr int GRID = NV <= 2 ? 256 : 512;
+    // pass 2 (several vectors): 512-column wave chunks up to 2 vectors, 256 above
     static constexpr int U2 = NV <= 2 ? 2 : 1;
 };
 
+// Pass-1 rows per work-group: the fp64 row sums of a work-group stay within
+// 80 KB of LDS (two work-groups per CU); larger m * NV splits the rows into
+// groups, each re-reading the vector chunks (NV * 4 bytes per column per extra
+// group, under 2% of the pass).
+constexpr int64_t ROWSUM_LDS = 80 * 1024;
+inline Pass1Grid pass1_grid(int m, int nv, int64_t nchunk, int target) {
+    const int64_t bytes = (int64_t)m * nv * 8;
+    const int ng = (int)((bytes + ROWSUM_LDS - 1) / ROWSUM_LDS);
+    Pass1Grid pg;
+    pg.mg = (m + ng - 1) / ng;
+    pg.ng = (m + pg.mg - 1) / pg.mg;
+    int64_t gx = target / pg.ng;
+    if (gx > nchunk) gx = nchunk;
+    if (gx < 1) gx = 1;
+    pg.gx = (int)gx;
+    return pg;
+}
+
 template <int NV>
 hipError_t pass1_nv(const float* G, int m, int64_t d, int64_t nslab, const VecIn& vin, bool aligned,
-                    double* part, int* grid_out, hipStream_t st) {
+                    double* part, Pass1Grid* grid_out, hipStream_t st) {
     constexpr int U = PassCfg<NV>::U, R = PassCfg<NV>::R;
+    static_assert(PassCfg<NV>::GRID <= PASS1_MAX_GRID, "partials sized for PASS1_MAX_GRID work-groups");
     const int64_t nchunk = nslab * (SLAB / (256 * U));
-    const int grid = (int)(nchunk < PASS1_MAX_GRID ? nchunk : PASS1_MAX_GRID);
-    const size_t lds = (size_t)m * NV * sizeof(double);
+    const Pass1Grid pg = pass1_grid(m, NV, nchunk, PassCfg<NV>::GRID);
+    const size_t lds = (size_t)pg.mg * NV * sizeof(double);
     if (lds > 65536) {
-        // fp64 row sums of up to 16384 values: up to 128 KB of the 160 KB LDS.
-        // Set on every such launch: the attribute is per device, and the call
-        // is cheap next to a pass over the window.
+        // fp64 row sums of a row group: just above 80 KB at most. Set on every
+        // such launch: the attribute is per device, and the call is cheap next
+        // to a pass over the window.
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass1<NV, U, R>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((k_pass1<NV, U, R>), dim3(grid), dim3(256), lds, st, G, m, d, nchunk, vin,
+    hipLaunchKernelGGL((k_pass1<NV, U, R>), dim3(pg.gx, pg.ng), dim3(256), lds, st, G, m, pg.mg, d, nchunk, vin,
                        aligned ? 1 : 0, part);
-    *grid_out = grid;
+    *grid_out = pg;
     return hipGetLastError();
 }
 
 template <int NV>
 hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const double* coef,
                     const VecOut& vout, bool aligned, hipStream_t st) {
+    if constexpr (NV == 1) {
+        if (m <= PASS2_ROWS_MAX_M) {
+            const size_t lds = (size_t)(((m + 1) & ~1) + 8 * SLAB) * sizeof(double);
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2_rows),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            if (e != hipSuccess) return e;
+            const int64_t grid = nslab < PASS2_ROWS_GRID ? nslab : PASS2_ROWS_GRID;
+            hipLaunchKernelGGL(k_pass2_rows, dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nslab, coef, vout,
+                               aligned ? 1 : 0);
+            return hipGetLastError();
+        }
+    }
     constexpr int U = PassCfg<NV>::U2;
     const int64_t nwchunk = nslab * (SLAB / (256 * U));
     const int64_t grid = ceil_div(nwchunk, 4);
@@ -389,7 +521,7 @@ hipError_t launch_write_row(float* G, int m, int64_t d, int64_t nslab, int k, co
 }
 
 hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv, const VecIn& vin,
-                        bool aligned, double* part, int* grid_out, hipStream_t st) {
+                        bool aligned, double* part, Pass1Grid* grid_out, hipStream_t st) {
     switch (nv) {
 #define CASE(N) \
     case N: return pass1_nv<N>(G, m, d, nslab, vin, aligned, part, grid_out, st);
@@ -399,9 +531,11 @@ hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv,
     }
 }
 
-hipError_t launch_reduce_partials(const double* part, int grid, int mnv, double* p, hipStream_t st) {
-    hipLaunchKernelGGL(k_reduce_partials, dim3((unsigned)ceil_div(mnv, 16)), dim3(256), 0, st, part,
-                       grid, mnv, p);
+hipError_t launch_reduce_partials(const double* part, const Pass1Grid& pg, int m, int nv, double* p,
+                                  hipStream_t st) {
+    const int mnv = m * nv;
+    hipLaunchKernelGGL(k_reduce_partials, dim3((unsigned)ceil_div(mnv, 16)), dim3(256), 0, st, part, pg, nv,
+                       mnv, p);
     return hipGetLastError();
 }
 
