@@ -218,7 +218,7 @@ __device__ __forceinline__ void coef_row(const T* __restrict__ row, T (&cv)[NP])
 // sums in the accumulation type of AccType (fp64: each window value converted
 // once per row), rounded to fp32 on the store. Each wave owns a 256*U-column
 // chunk and walks all m rows with RB rows of loads in flight.
-template <int NV, int U>
+template <int NV, int U, int RB>
 __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int m, int64_t d,
                                                int64_t nwchunk, const double* __restrict__ coef,
                                                VecOut vout, int aligned) {
@@ -249,7 +249,6 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
         for (int u = 0; u < U; ++u) acc[v][u][0] = acc[v][u][1] = acc[v][u][2] = acc[v][u][3] = T(0);
 
     // RB rows per batch: all RB*U loads are issued before the first FMA
-    constexpr int RB = (AccType<NV>::f64 && NV > 2) ? 4 : 8;
     auto fold = [&](const float4 (&g)[U], const T* crow) {
         T cv[NP];
         coef_row<NV, NP>(crow, cv);
@@ -401,11 +400,15 @@ struct PassCfg {
     // window (m = 1024) over U in {1, 2, 4, 8}, R in {1, ..., 8} and grids of
     // 256 / 384 / 512: one or two vectors stream best from one work-group per
     // CU (7.4 TB/s against 6.95 at two per CU); wider fusions need two.
+    // Above 10 vectors the rows split into two groups of 256 work-groups.
     static constexpr int U = NV <= 4 ? 4 : 2;
-    static constexpr int R = NV <= 2 ? 2 : NV <= 4 ? 1 : NV <= 7 ? 2 : NV <= 10 ? 3 : 2;
+    static constexpr int R = NV <= 2 ? 2 : NV <= 4 ? 1 : NV <= 7 ? 2 : NV <= 10 ? 3 : NV <= 16 ? 4 : 3;
     static constexpr int GRID = NV <= 2 ? 256 : 512;
-    // pass 2 (several vectors): 512-column wave chunks up to 2 vectors, 256 above
-    static constexpr int U2 = NV <= 2 ? 2 : 1;
+    // Pass 2 (the per-wave column chunk kernel): U2 float4 per lane (chunks of
+    // 256 * U2 columns), RB2 rows of loads in flight per wave; measured over
+    // U2 in {1, 2, 4} and RB2 in {2, ..., 16}.
+    static constexpr int U2 = NV == 2 ? 4 : NV <= 5 ? 2 : 1;
+    static constexpr int RB2 = NV == 1 ? 8 : NV == 2 ? 4 : NV <= 4 ? 2 : NV == 5 ? 4 : 8;
 };
 
 // Pass-1 rows per work-group: the fp64 row sums of a work-group stay within
@@ -463,17 +466,17 @@ hipError_t pass2_nv(const float* G, int m, int64_t d, int64_t nslab, const doubl
             return hipGetLastError();
         }
     }
-    constexpr int U = PassCfg<NV>::U2;
+    constexpr int U = PassCfg<NV>::U2, RB = PassCfg<NV>::RB2;
     const int64_t nwchunk = nslab * (SLAB / (256 * U));
     const int64_t grid = ceil_div(nwchunk, 4);
     const size_t lds = (size_t)m * CoefStride<NV>::P * sizeof(typename AccType<NV>::T);
     if (lds > 65536) {
         // set on every such launch (per device; cheap next to the pass)
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2<NV, U>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2<NV, U, RB>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((k_pass2<NV, U>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk, coef, vout,
+    hipLaunchKernelGGL((k_pass2<NV, U, RB>), dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nwchunk, coef, vout,
                        aligned ? 1 : 0);
     return hipGetLastError();
 }
