@@ -337,6 +337,41 @@ def test_rank_deficient_window_long_run(dev, d, m, lam, q):
     assert max(errs) < 1e-5, max(errs)
 
 
+@pytest.mark.parametrize("d,m", [
+    (3 * 2048 + 5, 1),       # one row: three of the four waves fold nothing
+    (1000, 3),               # d below one slab, m < 4
+    (4 * 2048 + 777, 7),     # ragged last slab (d % 4 != 0)
+    (6000, 4096),            # the largest m of the one-vector split-row pass 2 (160 KB of LDS)
+])
+def test_single_vector_pass2_shapes(dev, d, m):
+    """One inserted gradient and no queries (the one-vector pass 2), with
+    its output at an unaligned address (scalar tail stores) on one step, and
+    a one-vector IHVP (reads x, alpha = 1/lambda) with an unaligned output."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_tiny_d4096_m16")
+    wl = base.scaled(d=d, m=m, lam=1e-2, fill_by_replace=False)
+    gs = GradientStream(wl, seed=17)
+    G0 = gs.window()
+    say("single-vector pass 2", d, m)
+    win = Window(wl.d, wl.m, wl.lam, max_queries=0, G0=G0.to(dev), device=dev)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    buf = torch.full((d + 1,), float("nan"), device=dev)
+    for t in range(3):
+        g = gs.row(m + t)
+        y = win.replace(g.to(dev), y_out=buf[1:] if t == 1 else None)
+        yo = orc.slide(g.numpy())
+        assert rel_l2(y.cpu().numpy(), yo) < REL_TOL, t
+    assert torch.isnan(buf[0]).item()                       # nothing written before the output
+    x = gs.queries(0, 1)[0]
+    xo = orc.ihvp(x[None].numpy())[0]
+    assert rel_l2(win.ihvp(x.to(dev)).cpu().numpy(), xo) < REL_TOL
+    buf2 = torch.full((d + 1,), float("nan"), device=dev)
+    y2 = win.ihvp(x.to(dev), Y=buf2[1:])
+    assert rel_l2(y2.cpu().numpy(), xo) < REL_TOL
+    assert torch.isnan(buf2[0]).item()
+    assert win.status() == 0
+
+
 def test_default_policy_over_a_refactor_boundary_m1024(dev):
     """m = 1024 with the default coefficient policy (O(m^2) inverse updates,
     full refactor every 1024 replaces): 1100 steps, checked right before,
