@@ -13,62 +13,64 @@
 namespace mfac {
 namespace {
 
-// pass-1 partials for up to 4 vectors at the narrowest chunk width (512)
-int64_t static_query_main_doubles(int64_t d, int B, int m) { return (d / B) * ceil_div(B, 512) * (int64_t)m * 4; }
+// pass-1 partials for up to 4 vectors at the narrowest chunk width (1024)
+int64_t static_query_main_doubles(int64_t d, int B, int m) { return (d / B) * ceil_div(B, 1024) * (int64_t)m * 4; }
 
-// Pass 1: one work-group per column chunk of width 256*U inside one block.
+// Pass 1: column chunks of width 256*U inside the blocks, taken by a
+// persistent grid (chunk c by work-group c mod gridDim.x).
 // part[c][i*NV + v] = sum_{j in chunk c} W[i, j] x_v[j]: exact products of the
 // fp32 values summed in fp64; each (row, vector) sum of the chunk comes from
 // one wave and is stored directly.
 template <int NV, int U>
 __global__ __launch_bounds__(256) void k_sq_pass1(const float* __restrict__ W, int m, int64_t d, int B, int cpb,
-                                                  const float* __restrict__ X, double* __restrict__ part) {
+                                                  int nchunk, const float* __restrict__ X, double* __restrict__ part) {
     constexpr int CW = 256 * U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int mnv = m * NV;
-    const int c = blockIdx.x;
-    const int b = c / cpb, cb = c - (c / cpb) * cpb;
-    const int64_t j0 = (int64_t)b * B + (int64_t)cb * CW;
-    int64_t jend = (int64_t)(b + 1) * B;
-    if (jend > j0 + CW) jend = j0 + CW;
-    double* out = part + (int64_t)c * mnv;
+    for (int c = blockIdx.x; c < nchunk; c += gridDim.x) {
+        const int b = c / cpb, cb = c - (c / cpb) * cpb;
+        const int64_t j0 = (int64_t)b * B + (int64_t)cb * CW;
+        int64_t jend = (int64_t)(b + 1) * B;
+        if (jend > j0 + CW) jend = j0 + CW;
+        double* out = part + (int64_t)c * mnv;
 
-    float4 vr[NV][U];
+        float4 vr[NV][U];
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
+        for (int v = 0; v < NV; ++v)
 #pragma unroll
-        for (int u = 0; u < U; ++u) vr[v][u] = ld4(X + (int64_t)v * d, j0 + u * 256 + lane * 4, jend, 1);
+            for (int u = 0; u < U; ++u) vr[v][u] = ld4(X + (int64_t)v * d, j0 + u * 256 + lane * 4, jend, 1);
 
-    for (int i = wave; i < m; i += 8) {
-        const bool has2 = i + 4 < m;
-        const int i2 = has2 ? i + 4 : i;
-        float4 ga[U], gb[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t j = j0 + u * 256 + lane * 4;
-            ga[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
-            gb[u] = (j < jend) ? ld_stream(W + (int64_t)i2 * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        double sv[2 * NV];
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-            double a = 0.0, bb = 0.0;
+        for (int i = wave; i < m; i += 8) {
+            const bool has2 = i + 4 < m;
+            const int i2 = has2 ? i + 4 : i;
+            float4 ga[U], gb[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                a = dot4d(ga[u], vr[v][u], a);
-                bb = dot4d(gb[u], vr[v][u], bb);
+                const int64_t j = j0 + u * 256 + lane * 4;
+                ga[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+                gb[u] = (j < jend) ? ld_stream(W + (int64_t)i2 * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            sv[v] = a;
-            sv[NV + v] = bb;
-        }
-        int idx;
-        bool writer;
-        const double tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
-        if (writer) {
-            if (idx < NV)
-                out[i * NV + idx] = tot;
-            else if (has2)
-                out[i2 * NV + (idx - NV)] = tot;
+            double sv[2 * NV];
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                double a = 0.0, bb = 0.0;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    a = dot4d(ga[u], vr[v][u], a);
+                    bb = dot4d(gb[u], vr[v][u], bb);
+                }
+                sv[v] = a;
+                sv[NV + v] = bb;
+            }
+            int idx;
+            bool writer;
+            const double tot = wave_reduce_many<2 * NV>(sv, lane, idx, writer);
+            if (writer) {
+                if (idx < NV)
+                    out[i * NV + idx] = tot;
+                else if (has2)
+                    out[i2 * NV + (idx - NV)] = tot;
+            }
         }
     }
 }
@@ -102,8 +104,9 @@ __global__ __launch_bounds__(256) void k_sq_reduce_seg(const double* __restrict_
 
 // Pass 2: one wave per 256*U-column chunk of one block:
 // y_v[j] = alpha * x_v[j] - sum_i coef[b][i*NV + v] W[i, j], summed in fp64
-// (fp64 coefficients times fp32 W) and rounded to fp32 once.
-template <int NV, int U>
+// (fp64 coefficients times fp32 W) and rounded to fp32 once. Rows go in
+// batches of RB, all RB*U loads issued before the batch's first FMA.
+template <int NV, int U, int RB>
 __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, int m, int64_t d, int B, int cpb2,
                                                   int64_t nwchunk, const double* __restrict__ coef,
                                                   const float* __restrict__ X, float alpha, float* __restrict__ Y) {
@@ -124,13 +127,7 @@ __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, i
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int k = 0; k < 4; ++k) acc[v][u][k] = 0.0;
-    for (int i = 0; i < m; ++i) {
-        float4 g[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t j = j0 + u * 256 + lane * 4;
-            g[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+    auto fold = [&](const float4 (&g)[U], int i) {
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
             const double cv = cf[i * NV + v];
@@ -142,6 +139,27 @@ __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, i
                 acc[v][u][3] = fma(cv, (double)g[u].w, acc[v][u][3]);
             }
         }
+    };
+    auto load = [&](float4 (&g)[U], int i) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t j = j0 + u * 256 + lane * 4;
+            g[u] = (j < jend) ? ld_stream(W + (int64_t)i * d + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    };
+    int i = 0;
+    for (; i + RB <= m; i += RB) {
+        float4 g[RB][U];
+#pragma unroll
+        for (int r = 0; r < RB; ++r) load(g[r], i + r);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int r = 0; r < RB; ++r) fold(g[r], i + r);
+    }
+    for (; i < m; ++i) {
+        float4 g[U];
+        load(g, i);
+        fold(g, i);
     }
 #pragma unroll
     for (int v = 0; v < NV; ++v)
@@ -197,17 +215,28 @@ __global__ __launch_bounds__(256) void k_static_element(const float* __restrict_
 
 template <int NV>
 struct SqCfg {
-    static constexpr int U = NV == 1 ? 8 : NV == 2 ? 4 : 2;  // pass 1
-    static constexpr int U2 = NV <= 2 ? 2 : 1;               // pass 2
+    // Measured on the 17 GB W of the 2048-block workload (m = 1024) over chunk
+    // widths, grids and rows in flight. Pass 1: 2048-column chunks up to 3
+    // vectors (1024 for 4, which would spill at 2048) on a persistent grid of
+    // GRID1 work-groups (0: one per chunk); pass 2: 512-column wave chunks
+    // with RB2 rows of loads in flight.
+    static constexpr int U = NV <= 3 ? 8 : 4;
+    static constexpr int GRID1 = NV == 1 ? 256 : NV <= 3 ? 512 : 0;
+    static constexpr int U2 = 2;
+    static constexpr int RB2 = NV == 2 ? 8 : 4;
 };
 
 template <int NV>
 hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, float alpha, double pscale, float* Y,
                       double* part, double* coef, hipStream_t st) {
-    constexpr int U = SqCfg<NV>::U, U2 = SqCfg<NV>::U2;
+    constexpr int U = SqCfg<NV>::U, U2 = SqCfg<NV>::U2, RB2 = SqCfg<NV>::RB2;
+    static_assert(256 * U >= 1024, "partials are sized for chunks of at least 1024 columns");
     const int nblocks = (int)(d / B);
     const int cpb = (int)ceil_div(B, 256 * U);
-    hipLaunchKernelGGL((k_sq_pass1<NV, U>), dim3((unsigned)(nblocks * cpb)), dim3(256), 0, st, W, m, d, B, cpb, X,
+    const int nchunk = nblocks * cpb;
+    constexpr int target = SqCfg<NV>::GRID1;
+    const int grid = (target == 0 || nchunk < target) ? nchunk : target;
+    hipLaunchKernelGGL((k_sq_pass1<NV, U>), dim3((unsigned)grid), dim3(256), 0, st, W, m, d, B, cpb, nchunk, X,
                        part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -229,7 +258,7 @@ hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, f
     if (e != hipSuccess) return e;
     const int cpb2 = (int)ceil_div(B, 256 * U2);
     const int64_t nw = (int64_t)nblocks * cpb2;
-    hipLaunchKernelGGL((k_sq_pass2<NV, U2>), dim3((unsigned)ceil_div(nw, 4)), dim3(256), 0, st, W, m, d, B, cpb2, nw,
+    hipLaunchKernelGGL((k_sq_pass2<NV, U2, RB2>), dim3((unsigned)ceil_div(nw, 4)), dim3(256), 0, st, W, m, d, B, cpb2, nw,
                        coef, X, alpha, Y);
     return hipGetLastError();
 }
@@ -238,7 +267,7 @@ hipError_t sq_ihvp_nv(const float* W, int m, int64_t d, int B, const float* X, f
 
 int64_t static_query_part_doubles(int64_t d, int B, int m) {
     // pass-1 partials, then the per-segment sums of wide blocks
-    return static_query_main_doubles(d, B, m) + (d / B) * ceil_div(ceil_div(B, 512), SEG) * (int64_t)m * 4;
+    return static_query_main_doubles(d, B, m) + (d / B) * ceil_div(ceil_div(B, 1024), SEG) * (int64_t)m * 4;
 }
 
 hipError_t launch_static_ihvp(const float* W, int m, int64_t d, int B, int n, const float* X, float alpha,
