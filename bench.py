@@ -547,8 +547,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the design for sharding d over GPUs is described in DESIGN.md).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(a window would shard its columns over GPUs; not implemented).", file=sys.stderr)
         sys.exit(2)
 
     import torch

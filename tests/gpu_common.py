@@ -21,7 +21,7 @@ def require_gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2107_03356_amd import _binding as B
-    B.load()  # must not fall back: a missing library is an error on a GPU machine
+    B.load()  # must not fall back: a missing library is an error where a GPU is present
     return torch.device("cuda:0")
 
 

@@ -28,7 +28,7 @@ def test_optimizer_models_have_the_workload_sizes():
             assert sum(p.numel() for p in net.parameters()) == wl.d, wl.name
 
 
-def test_pass_bytes_match_the_survey_budget():
+def test_pass_bytes_match_the_algorithmic_budget():
     """2 m d 4 + 3 d 4 bytes per step at the ResNet50-sized window (210.0 GB)."""
     sys.path.insert(0, ROOT)
     import bench
