@@ -295,7 +295,7 @@ __global__ __launch_bounds__(256) void k_pass2(const float* __restrict__ G, int 
             y.y = (float)((T)a * (T)x.y - acc[v][u][1]);
             y.z = (float)((T)a * (T)x.z - acc[v][u][2]);
             y.w = (float)((T)a * (T)x.w - acc[v][u][3]);
-            st4(vout.y[v], j, d, aligned, y);
+            st4_stream(vout.y[v], j, d, aligned, y);
         }
     }
 }
@@ -378,7 +378,7 @@ __global__ __launch_bounds__(256) void k_pass2_rows(const float* __restrict__ G,
             o.y = (float)(a * xv.y - sum[1]);
             o.z = (float)(a * xv.z - sum[2]);
             o.w = (float)(a * xv.w - sum[3]);
-            st4(y, j, d, aligned, o);
+            st4_stream(y, j, d, aligned, o);
         }
     }
 }

@@ -174,7 +174,7 @@ __global__ __launch_bounds__(256) void k_sq_pass2(const float* __restrict__ W, i
                 y.y = (float)(a * x.y - acc[v][u][1]);
                 y.z = (float)(a * x.z - acc[v][u][2]);
                 y.w = (float)(a * x.w - acc[v][u][3]);
-                *reinterpret_cast<float4*>(Y + (int64_t)v * d + j) = y;
+                st_stream(Y + (int64_t)v * d + j, y);
             }
         }
 }
