@@ -656,6 +656,41 @@ def main():
                     "in_timed_region": args.steps >= period}
         log(f"refactor: {refactor}")
 
+    # The same kind of steps when the gradients are all known in advance
+    # (mfac_window_replace_seq): the window read of each step's IHVP also forms
+    # the next gradient's Gram column, so a step reads the window once. It
+    # continues the sliding sequence over the same pre-generated gradients.
+    # Not the headline: an optimizer's next gradient depends on this step.
+    sequence = None
+    if not nq:
+        Yseq = torch.empty((args.steps, d), dtype=torch.float32, device=dev)
+        win.trace(True)
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        win.replace_seq(steps_g[args.warmup:nsteps], Yseq)
+        s1.record(stream)
+        torch.cuda.synchronize()
+        win.trace(False)
+        sms, scnt = win.trace_read()
+        st = win.status()
+        if st != 0:
+            log(f"device error after the sequence: {P.status_string(st)}")
+            sys.exit(1)
+        del Yseq
+        ms_seq = s0.elapsed_time(s1) / args.steps
+        fused = m <= 2048
+        p2avg = sms[2] / max(scnt[2], 1)
+        sequence = {
+            "entry_point": "mfac_window_replace_seq", "steps": args.steps,
+            "steps_per_s": 1000.0 / ms_seq, "ms_per_step": ms_seq,
+            "window_reads_per_step": 1 if fused else 2,
+            "ihvp_pass_ms": p2avg,
+            # fused pass: reads the window and the next gradient, writes y
+            "ihvp_pass_gbs": (4.0 * (m + 2) * d if fused else 4.0 * (m + 1) * d) / (p2avg * 1e-3) / 1e9,
+        }
+        log(f"sequence: {sequence}")
+
     ms_step = ms_total / args.steps
     b1, b2, bw = pass_bytes(d, m)
     if nq:
@@ -693,6 +728,7 @@ def main():
         "achieved_hbm_gbs_step": step_bytes / (ms_step * 1e-3) / 1e9,
         "phases_ms_per_step": {"row_write": avg[3], "pass1": avg[0], "coefficients": avg[1], "pass2": avg[2]},
         "refactor": refactor,
+        "sequence": sequence,
         "pass_gbs": {"k_pass1": gbs1, "k_pass2": gbs2},
         "roofline": {
             "bound": "hbm",

@@ -124,6 +124,23 @@ mfac_status mfac_window_rebuild(mfac_window w);
 mfac_status mfac_window_replace(mfac_window w, int32_t slot, const float* g_new,
                                 float* y_out, int32_t n, const float* X, float* Y);
 
+/* A sequence of sliding steps whose gradients are all known in advance:
+ * gradient t of Gn (n x d row-major) enters the ring head, then Yn row t =
+ * F_t^-1 Gn[t] for the window F_t that holds gradients 0..t of the sequence
+ * (Section 3.2 update and multiplication, as n calls of mfac_window_replace
+ * with slot -1, no extra queries). The window read that forms Yn[t] also
+ * forms the Gram column of Gn[t+1] (Appendix B reuses one product of the
+ * window for the update and the multiplication; here the reuse spans two
+ * consecutive steps): the row Gn[t+1] replaces is still read for Yn[t], and
+ * its dot with Gn[t+1] is taken as Gn[t+1] . Gn[t+1], its value after the
+ * replacement. One read of the window per step instead of two for m <= 2048;
+ * larger m runs the two passes per step of mfac_window_replace. Results equal
+ * those of the separate calls up to the order of fp64 sums in the Gram
+ * column. Not for an optimizer loop, whose next gradient depends on this
+ * step's output. n >= 1; Gn and Yn must not alias each other or the window
+ * storage. The ring head and step count advance by n. */
+mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const float* Gn, float* Yn);
+
 /* Y = F^-1 X for n x d row-major X (Section 3.2 multiplication; Algorithm 2's
  * role): two passes over the window and an O(m^2) solve with the cached
  * factor. 1 <= n <= max_queries + 1 (the vectors one replace carries). */

@@ -38,6 +38,7 @@ SIGNATURES = {
     "mfac_window_set_rows": (_c.c_int, [_VP, _I32, _I32, _VP]),
     "mfac_window_rebuild": (_c.c_int, [_VP]),
     "mfac_window_replace": (_c.c_int, [_VP, _I32, _VP, _VP, _I32, _VP, _VP]),
+    "mfac_window_replace_seq": (_c.c_int, [_VP, _I32, _VP, _VP]),
     "mfac_ihvp": (_c.c_int, [_VP, _I32, _VP, _VP]),
     "mfac_window_get_rows": (_c.c_int, [_VP, _I32, _I32, _VP]),
     "mfac_window_info": (_c.c_int, [_VP, _c.POINTER(_I32), _c.POINTER(_I64)]),
@@ -180,6 +181,18 @@ class Window:
         st = load().mfac_window_replace(self.handle, int(slot), _ptr(g), _ptr(y_out), n, _ptr(X), _ptr(Y))
         _check("mfac_window_replace", st)
         return (y_out, Y) if X is not None else y_out
+
+    def replace_seq(self, Gn, Yn=None):
+        """Insert the rows of Gn (n x d) one after another into the ring head;
+        row t of the result is F^-1 Gn[t] right after Gn[t] went in."""
+        t = self.torch
+        n = Gn.shape[0]
+        self._vec(Gn, n)
+        if Yn is None:
+            Yn = t.empty_like(Gn)
+        self._vec(Yn, n)
+        _check("mfac_window_replace_seq", load().mfac_window_replace_seq(self.handle, n, _ptr(Gn), _ptr(Yn)))
+        return Yn
 
     def ihvp(self, X, Y=None):
         t = self.torch

@@ -363,6 +363,87 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
     return MFAC_OK;
 }
 
+MFAC_API mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const float* Gn, float* Yn) {
+    if (!w || !Gn || !Yn || n < 1) return MFAC_EINVAL;
+    if (!aligned4(Gn) || !aligned4(Yn)) return MFAC_EINVAL;
+    const int64_t d = w->d;
+    const int m = w->m;
+    const bool al = aligned16(Gn) && aligned16(Yn) && (n == 1 || d % 4 == 0);
+    const double inv_lam = 1.0 / w->lambda;
+    const bool fused = m <= PASS21_MAX_M;
+
+    // coefficients of gradient t once its Gram column is in p (slot k)
+    auto coefficients = [&](int k) -> mfac_status {
+        mfac_status rc = window_slot_update(w, 1, k);
+        if (rc != MFAC_OK) return rc;
+        HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, m, w->p, 1, 1, k, -(double)m, inv_lam, w->coef, w->err, w->st));
+        return MFAC_OK;
+    };
+
+    int k = w->head;
+    Pass1Grid grid{};
+    VecIn vin{};
+    vin.v[0] = Gn;
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_write_row(w->G, m, d, w->nslab, k, Gn, w->st));
+    HIPCHK(mark_end(w, 3));
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_pass1(w->G, m, d, w->nslab, 1, vin, al, w->part, &grid, w->st));
+    HIPCHK(mark_end(w, 0));
+    HIPCHK(mark_begin(w));
+    HIPCHK(launch_reduce_partials(w->part, grid, m, 1, w->p, w->st));
+    w->head = (k + 1) % m;
+    w->steps += 1;
+    mfac_status rc = coefficients(k);
+    if (rc != MFAC_OK) return rc;
+    HIPCHK(mark_end(w, 1));
+
+    for (int32_t t = 0; t < n; ++t) {
+        float* y = Yn + (int64_t)t * d;
+        VecOut vout{};
+        vout.x[0] = nullptr;
+        vout.y[0] = y;
+        vout.alpha[0] = 0.0f;
+        if (t + 1 == n) {
+            HIPCHK(mark_begin(w));
+            HIPCHK(launch_pass2(w->G, m, d, w->nslab, 1, w->coef, vout, al, w->st));
+            HIPCHK(mark_end(w, 2));
+            break;
+        }
+        const float* gnext = Gn + (int64_t)(t + 1) * d;
+        const int knext = (k + 1) % m;
+        HIPCHK(mark_begin(w));
+        if (fused) {
+            // y_t and the next gradient's Gram column in one read of the
+            // window; the next gradient enters its slot only after that read
+            HIPCHK(launch_pass2_next(w->G, m, d, w->nslab, w->coef, y, gnext, knext, al, w->part, &grid, w->st));
+            HIPCHK(mark_end(w, 2));
+            HIPCHK(mark_begin(w));
+            HIPCHK(launch_write_row(w->G, m, d, w->nslab, knext, gnext, w->st));
+            HIPCHK(mark_end(w, 3));
+        } else {
+            HIPCHK(launch_pass2(w->G, m, d, w->nslab, 1, w->coef, vout, al, w->st));
+            HIPCHK(mark_end(w, 2));
+            HIPCHK(mark_begin(w));
+            HIPCHK(launch_write_row(w->G, m, d, w->nslab, knext, gnext, w->st));
+            HIPCHK(mark_end(w, 3));
+            HIPCHK(mark_begin(w));
+            vin.v[0] = gnext;
+            HIPCHK(launch_pass1(w->G, m, d, w->nslab, 1, vin, al, w->part, &grid, w->st));
+            HIPCHK(mark_end(w, 0));
+        }
+        HIPCHK(mark_begin(w));
+        HIPCHK(launch_reduce_partials(w->part, grid, m, 1, w->p, w->st));
+        w->head = (knext + 1) % m;
+        w->steps += 1;
+        rc = coefficients(knext);
+        if (rc != MFAC_OK) return rc;
+        HIPCHK(mark_end(w, 1));
+        k = knext;
+    }
+    return MFAC_OK;
+}
+
 MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* Y) {
     if (!w || !X || !Y) return MFAC_EINVAL;
     if (n < 1 || n > w->max_q + 1) return MFAC_EINVAL;

@@ -58,6 +58,15 @@ hipError_t launch_reduce_partials(const double* part, const Pass1Grid& pg, int m
 hipError_t launch_pass2(const float* G, int m, int64_t d, int64_t nslab, int nv,
                         const double* coef, const VecOut& vout, bool aligned, hipStream_t st);
 
+// Pass 2 of one step fused with pass 1 of the next (one vector each, m <=
+// PASS21_MAX_M): y = -G^T coef and the partial dots of the rows with gn, row
+// knext counted as gn . gn; partials in the layout of launch_pass1 (returned
+// shape: one row group).
+constexpr int PASS21_MAX_M = 2048;  // coefficients, row sums and 2 x 4 x SLAB fp64 partials: 160 KB of LDS
+hipError_t launch_pass2_next(const float* G, int m, int64_t d, int64_t nslab, const double* coef, float* y,
+                             const float* gn, int knext, bool aligned, double* part, Pass1Grid* grid_out,
+                             hipStream_t st);
+
 // ---------------------------------------------------------------- Gram
 // Window Gram: K (m x m, fp64, full symmetric) = sum over slabs of G_s G_s^T,
 // fp64 MFMA tiles; part must hold gram_window_part_doubles().

@@ -383,6 +383,107 @@ __global__ __launch_bounds__(256) void k_pass2_rows(const float* __restrict__ G,
     }
 }
 
+// Pass 2 of one step fused with pass 1 of the next, for a sequence of
+// gradients that are all known in advance (m <= PASS21_MAX_M). In the one
+// read of the window it forms y = -G^T coef exactly as k_pass2_rows does
+// (same order of every sum, so y is bitwise the same for the same
+// coefficients) and the dots of every row with the next gradient gn. Row
+// knext, the slot gn will take after this pass, gets gn . gn instead of its
+// current row's dot, which makes the dots those of the window after the
+// insertion. The dots follow the precision of k_pass1 for one vector (exact
+// fp32 products summed in fp64): each wave reduces the per-lane sums of RB
+// of its rows at a time across its lanes, and the work-group keeps fp64 row
+// sums in LDS, written out in the partial layout of k_pass1 (one row group).
+constexpr int PASS21_RB = 8;
+
+__global__ __launch_bounds__(256) void k_pass2_next(const float* __restrict__ G, int m, int64_t d, int64_t nslab,
+                                                    const double* __restrict__ coef, float* __restrict__ y,
+                                                    const float* __restrict__ gn, int knext, int aligned,
+                                                    double* __restrict__ part) {
+    extern __shared__ __align__(16) double sh[];
+    const int mpad = (m + 1) & ~1;  // keeps the partials 16-byte aligned
+    double* cl = sh;
+    double* rs = sh + mpad;    // row sums of this work-group's slabs
+    double* red = rs + mpad;   // [2][4][SLAB]
+    for (int t = threadIdx.x; t < m; t += 256) {
+        cl[t] = coef[t];
+        rs[t] = 0.0;
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    float4 g[8], gv[8];
+    int64_t s = blockIdx.x;
+    if (s < nslab && wave < m) load_slab_row(g, G, m, s, wave, lane);
+    for (int t = 0; s < nslab; s += gridDim.x, ++t) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) gv[u] = ld4(gn, s * SLAB + u * 256 + lane * 4, d, aligned);
+        double acc[8][4];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[u][0] = acc[u][1] = acc[u][2] = acc[u][3] = 0.0;
+        for (int i0 = wave; i0 < m; i0 += 4 * PASS21_RB) {
+            double sv[PASS21_RB];
+#pragma unroll
+            for (int r = 0; r < PASS21_RB; ++r) {
+                const int i = i0 + 4 * r;
+                double dv = 0.0;
+                if (i < m) {
+                    const double cv = cl[i];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        acc[u][0] = fma(cv, (double)g[u].x, acc[u][0]);
+                        acc[u][1] = fma(cv, (double)g[u].y, acc[u][1]);
+                        acc[u][2] = fma(cv, (double)g[u].z, acc[u][2]);
+                        acc[u][3] = fma(cv, (double)g[u].w, acc[u][3]);
+                    }
+                    if (i == knext) {
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) dv = dot4d(gv[u], gv[u], dv);
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) dv = dot4d(g[u], gv[u], dv);
+                    }
+                    if (i + 4 < m)
+                        load_slab_row(g, G, m, s, i + 4, lane);
+                    else if (s + gridDim.x < nslab)
+                        load_slab_row(g, G, m, s + gridDim.x, wave, lane);
+                }
+                sv[r] = dv;
+            }
+            int idx;
+            bool writer;
+            const double tot = wave_reduce_many<PASS21_RB>(sv, lane, idx, writer);
+            if (writer && i0 + 4 * idx < m) rs[i0 + 4 * idx] += tot;
+        }
+        double* rb = red + (t & 1) * 4 * SLAB;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            double* q = rb + wave * SLAB + u * 256 + lane * 4;
+            *reinterpret_cast<double2*>(q) = make_double2(acc[u][0], acc[u][1]);
+            *reinterpret_cast<double2*>(q + 2) = make_double2(acc[u][2], acc[u][3]);
+        }
+        lds_barrier();
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int col = wave * 512 + h * 256 + lane * 4;
+            const int64_t j = s * SLAB + col;
+            double sum[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                sum[k] = rb[col + k] + rb[SLAB + col + k] + rb[2 * SLAB + col + k] + rb[3 * SLAB + col + k];
+            // y = 0 - sum (not -sum: an exact zero sum stores +0, as in k_pass2_rows)
+            float4 o;
+            o.x = (float)(0.0 - sum[0]);
+            o.y = (float)(0.0 - sum[1]);
+            o.z = (float)(0.0 - sum[2]);
+            o.w = (float)(0.0 - sum[3]);
+            st4_stream(y, j, d, aligned, o);
+        }
+    }
+    __syncthreads();
+    double* out = part + (int64_t)blockIdx.x * m;
+    for (int t = threadIdx.x; t < m; t += 256) out[t] = rs[t];
+}
+
 // The new gradient into row k of the window (padding past d stays zero).
 __global__ __launch_bounds__(256) void k_write_row(float* __restrict__ G, int m, int64_t d, int64_t ncolpad,
                                                    int k, const float* __restrict__ g, int aligned) {
@@ -532,6 +633,23 @@ hipError_t launch_pass1(const float* G, int m, int64_t d, int64_t nslab, int nv,
 #undef CASE
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_pass2_next(const float* G, int m, int64_t d, int64_t nslab, const double* coef, float* y,
+                             const float* gn, int knext, bool aligned, double* part, Pass1Grid* grid_out,
+                             hipStream_t st) {
+    if (m > PASS21_MAX_M) return hipErrorInvalidValue;
+    const size_t lds = (size_t)(2 * ((m + 1) & ~1) + 8 * SLAB) * sizeof(double);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pass2_next),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    const int64_t grid = nslab < PASS2_ROWS_GRID ? nslab : PASS2_ROWS_GRID;
+    hipLaunchKernelGGL(k_pass2_next, dim3((unsigned)grid), dim3(256), lds, st, G, m, d, nslab, coef, y, gn, knext,
+                       aligned ? 1 : 0, part);
+    grid_out->gx = (int)grid;
+    grid_out->ng = 1;
+    grid_out->mg = m;
+    return hipGetLastError();
 }
 
 hipError_t launch_reduce_partials(const double* part, const Pass1Grid& pg, int m, int nv, double* p,

@@ -76,6 +76,7 @@ def test_null_handles_and_out_pointers():
     lib = B.load()
     assert lib.mfac_window_init(None, 4096, 16, 1e-3, 0, 256, 1 << 30, 512, 1 << 30, None, None) == B.MFAC_EINVAL
     assert lib.mfac_window_replace(None, -1, 256, 512, 0, None, None) == B.MFAC_EINVAL
+    assert lib.mfac_window_replace_seq(None, 2, 256, 512) == B.MFAC_EINVAL
     assert lib.mfac_ihvp(None, 1, 256, 512) == B.MFAC_EINVAL
     assert lib.mfac_window_rebuild(None) == B.MFAC_EINVAL
     assert lib.mfac_window_status(None) == B.MFAC_EINVAL
