@@ -143,6 +143,26 @@ def test_resnet50_window_sliding_step_matches_oracle(dev):
     _step_and_compare(_S["r50"], 0)
 
 
+def test_resnet50_window_known_sequence_matches_oracle(dev):
+    """Three further steps as one mfac_window_replace_seq call (the fused
+    pass the bench's sequence figure times), each output against the oracle."""
+    st = _S.get("r50")
+    if st is None or "orc" not in st:
+        pytest.skip("setup failed")
+    gs, win, orc = st["gs"], st["win"], st["orc"]
+    Gn = torch.stack([gs.step_row(t) for t in (1, 2, 3)])
+    Yn = win.replace_seq(Gn)
+    torch.cuda.synchronize()
+    assert win.status() == 0
+    errs = []
+    for i in range(3):
+        t0 = time.perf_counter()
+        yo = orc.slide(Gn[i].cpu().numpy())
+        errs.append(rel_l2(Yn[i].cpu().numpy(), yo))
+        _log(f"sequence step {i + 1}: rel L2 {errs[-1]:.2e} (oracle {time.perf_counter() - t0:.1f} s)")
+    assert max(errs) < REL_TOL, errs
+
+
 def test_resnet50_window_release(dev):
     _S.pop("r50", None)
     torch.cuda.empty_cache()
