@@ -176,8 +176,10 @@ mfac_status mfac_window_set_stream(mfac_window w, hipStream_t stream);
  * off by default). Phases: 0 = pass-1 kernel (G x), 1 = coefficient phase
  * (partial-sum reduction, Gram row, inverse update or refactor, coefficients),
  * 2 = pass-2 kernel (G^T c), 3 = the write of the new gradient into its slot.
- * enable != 0 starts recording around every replace and ihvp; 0 stops
- * (recorded events are kept until read). */
+ * enable != 0 starts recording around every replace, replace_seq and ihvp;
+ * 0 stops (recorded events are kept until read). In mfac_window_replace_seq
+ * phase 2 is the fused pass (G^T c of one step with G x of the next) for all
+ * but the last step, and phase 0 runs once, for the first gradient. */
 #define MFAC_NPHASES 4
 mfac_status mfac_window_trace(mfac_window w, int32_t enable);
 
