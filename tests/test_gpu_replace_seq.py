@@ -19,7 +19,7 @@ def dev():
     return require_gpu()
 
 
-def _case(dev, d, m, lam, n, dist, from_empty, seed=5, chunks=(None,)):
+def _case(dev, d, m, lam, n, dist, from_empty, seed=5, chunks=(None,), period=None):
     from paper_2107_03356_amd import Window
     base = get_workload("dyn_resnet18_d11.2m_m1024_q8")
     wl = base.scaled(d=d, m=m, lam=lam, dist=dist, queries=0, scale_d=(base.d if dist == "lognormal" else 0))
@@ -32,6 +32,9 @@ def _case(dev, d, m, lam, n, dist, from_empty, seed=5, chunks=(None,)):
     seq = Window(d, m, lam, G0=None if G0 is None else G0.to(dev), device=dev)
     one = Window(d, m, lam, G0=None if G0 is None else G0.to(dev), device=dev)
     orc = WindowOracle(d, m, lam, G0=None if G0 is None else G0.numpy())
+    if period is not None:
+        seq.set_refactor_period(period)
+        one.set_refactor_period(period)
     Gd = Gn.to(dev)
     # the sequence in one call, or in consecutive calls of the given lengths
     Ys, t0 = [], 0
@@ -93,3 +96,30 @@ def test_replace_seq_rejects_bad_arguments(dev):
     assert lib.mfac_window_replace_seq(w.handle, 2, G.data_ptr() + 2, G.data_ptr()) == B.MFAC_EINVAL
     assert w.info() == (0, 0)
     assert w.status() == 0
+
+
+@pytest.mark.parametrize("period", [0, 2, 5])
+def test_replace_seq_under_refactor_policies(dev, period):
+    """Refactor on every replace, every second, every fifth: the sequence
+    takes the same coefficient path per step as single replaces."""
+    say("replace_seq refactor period", period)
+    e_orc, e_one, e_after = _case(dev, 6000, 24, 1e-3, 17, "gauss", False, period=period)
+    assert e_orc < REL_TOL and e_one < 1e-6 and e_after < REL_TOL, (e_orc, e_one, e_after)
+
+
+@pytest.mark.parametrize("m,fused", [(16, True), (2049, False)])
+def test_replace_seq_phase_trace_counts(dev, m, fused):
+    from paper_2107_03356_amd import Window
+    say("replace_seq trace", m)
+    d, n = 4096, 5
+    w = Window(d, m, 1e-3, device=dev)
+    Gn = torch.randn(n, d, device=dev) / 64.0
+    w.trace(True)
+    w.replace_seq(Gn)
+    w.trace(False)
+    ms, cnt = w.trace_read()
+    # phases: 0 pass 1, 1 coefficients, 2 pass 2 (fused with the next pass 1), 3 row write
+    assert cnt == [1 if fused else n, n, n, n], cnt
+    assert all(t >= 0.0 for t in ms)
+    assert w.status() == 0
+    assert w.info() == (n % m, n)
