@@ -501,9 +501,11 @@ struct PassCfg {
     // window (m = 1024) over U in {1, 2, 4, 8}, R in {1, ..., 8} and grids of
     // 256 / 384 / 512: one or two vectors stream best from one work-group per
     // CU (7.4 TB/s against 6.95 at two per CU); wider fusions need two.
+    // A later re-sweep of R at 8-10 vectors gave R = 4 for 9 and 10 vectors
+    // (6.75 and 6.67 TB/s against 6.66 and 6.36 with R = 3) and kept 3 for 8.
     // Above 10 vectors the rows split into two groups of 256 work-groups.
     static constexpr int U = NV <= 4 ? 4 : 2;
-    static constexpr int R = NV <= 2 ? 2 : NV <= 4 ? 1 : NV <= 7 ? 2 : NV <= 10 ? 3 : NV <= 16 ? 4 : 3;
+    static constexpr int R = NV <= 2 ? 2 : NV <= 4 ? 1 : NV <= 7 ? 2 : NV == 8 ? 3 : NV <= 16 ? 4 : 3;
     static constexpr int GRID = NV <= 2 ? 256 : 512;
     // Pass 2 (the per-wave column chunk kernel): U2 float4 per lane (chunks of
     // 256 * U2 columns), RB2 rows of loads in flight per wave; measured over
