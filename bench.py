@@ -7,7 +7,12 @@ Default workload: d = 25,600,000, m = 1024, lambda = 1e-5, ResNet50-sized
 log-normal-scaled synthetic gradients with 10% correlated rows; the ~105 GB
 window and every step's gradient are resident in HBM before timing starts.
 
-Prints one JSON line (metric, value, ..., roofline, cpu_baseline).
+After the timed region the fp64 oracle, at full d on the host, replays the
+same steps from its own Gram matrix and checks the outputs of the first, a
+middle and the last timed step (`parity`); its own sliding step at full d is
+timed as `cpu_baseline`.
+
+Prints one JSON line (metric, value, ..., roofline, parity, cpu_baseline).
 """
 
 import argparse
@@ -95,50 +100,71 @@ def read_static_counters(workload, kernel):
     return float(m.group(1)) if m else None
 
 
-def cpu_baseline(wl, seed, sample_div, nsteps):
-    """The fp64 oracle as it stands, on a column sample of the same workload.
-
-    Times `nsteps` oracle sliding steps on a window of m rows x d/sample_div
-    columns; the O(dm) part is scaled by sample_div to the full d, the O(m^3)
-    Cholesky part is timed separately and added once.
-    """
-    import numpy as np
-    import torch
-
-    from oracle.dynamic import WindowOracle
-    from synth import GradientStream
-
+def blas_info():
+    """(threads, description) of the BLAS the oracle's numpy/scipy calls use."""
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
     except Exception:
-        cores = os.cpu_count()
-    ds = wl.d // sample_div
-    swl = wl.scaled(d=ds, scale_d=wl.d)
-    gs = GradientStream(swl, seed=seed, device="cuda")
-    G0 = gs.window().cpu().numpy()
-    rows = [gs.step_row(t).cpu().numpy() for t in range(nsteps)]
-    orc = WindowOracle(ds, wl.m, wl.lam, G0=G0)
+        libs = []
+    if not libs:
+        return os.cpu_count(), "unknown"
+    threads = max(int(i.get("num_threads", 1)) for i in libs)
+    desc = sorted({f"{i.get('internal_api')} {i.get('version')} ({os.path.basename(i.get('filepath', ''))})"
+                   for i in libs})
+    return threads, "; ".join(desc)
+
+
+def oracle_check(wl, G_host, steps_g, warmup, checked, ys, Xq=None, Yqs=None):
+    """The fp64 oracle at full d, after the timed region: it forms its own Gram
+    matrix of the initial window (host copy of the rows drawn on the GPU,
+    taken before the library saw them), replays every replace of the warm-up
+    and timed steps, and computes F^-1 g for the checked steps, compared with
+    the library's outputs of those steps (and the extra queries' F^-1 X,
+    when the workload has them). The last checked step's oracle slide
+    (replace + IHVP of the new gradient) is timed as the CPU baseline."""
+    import numpy as np
+
+    from oracle import dynamic as odyn
+
+    d, m = wl.d, wl.m
     t0 = time.perf_counter()
-    for g in rows:
-        orc.slide(g)
-    t_steps = (time.perf_counter() - t0) / nsteps
-    P = np.zeros((wl.m, 1))
-    t0 = time.perf_counter()
-    for _ in range(nsteps):
-        orc.coefficients(P)
-    t_coef = (time.perf_counter() - t0) / nsteps
-    t_full = max(t_steps - t_coef, 0.0) * sample_div + t_coef
-    return {
-        "value": 1.0 / t_full,
-        "unit": "steps/s",
-        "cores": int(cores),
-        "kind": "oracle",
-        "sample": (f"{nsteps} oracle sliding steps (numpy fp64, Woodbury + LAPACK Cholesky) on a "
-                   f"{wl.m} x {ds} column sample (d/{sample_div}); O(dm) time x{sample_div} plus the "
-                   f"m^3 coefficient time ({t_coef * 1e3:.1f} ms)"),
-        "sec_per_step_full_d": t_full,
-    }
+    K = np.zeros((m, m), np.float64, order="F")
+    nparts = 8
+    for i in range(nparts):
+        K = odyn.gram_accumulate(G_host, K, d * i // nparts, d * (i + 1) // nparts)
+        log(f"oracle Gram {i + 1}/{nparts} ({time.perf_counter() - t0:.0f} s)")
+    orc = odyn.WindowOracle(d, m, wl.lam, G0=G_host, K=odyn.gram_symmetric(K), copy=False)
+    t_gram = time.perf_counter() - t0
+    errs, t_step = {}, None
+    last = max(checked)
+    for t in range(last + 1):
+        g = steps_g[t].cpu().numpy()
+        if t in checked:
+            t1 = time.perf_counter()
+            yo = orc.slide(g)
+            if t == last:
+                t_step = time.perf_counter() - t1
+            y = ys[t].cpu().numpy().astype(np.float64)
+            e = [float(np.linalg.norm(y - yo) / np.linalg.norm(yo))]
+            if Xq is not None:
+                Yo = orc.ihvp(Xq[t].cpu().numpy())
+                Yl = Yqs[t].cpu().numpy().astype(np.float64)
+                e += [float(np.linalg.norm(Yl[q] - Yo[q]) / np.linalg.norm(Yo[q])) for q in range(Yo.shape[0])]
+            errs[t - warmup] = max(e)
+            log(f"oracle step {t - warmup}: rel L2 {errs[t - warmup]:.2e}")
+        else:
+            orc.replace(orc.steps % m, g)
+            if t % 5 == 4:
+                log(f"oracle replace {t + 1}/{last + 1}")
+    threads, blas = blas_info()
+    parity = {"max_rel_l2": max(errs.values()), "tol": 1e-4, "rel_l2_by_timed_step": errs,
+              "oracle": "fp64 Woodbury at full d (own Gram, every replace replayed)"}
+    cpu = {"value": 1.0 / t_step, "unit": "steps/s", "cores": int(threads), "blas": blas, "kind": "oracle",
+           "sample": (f"one oracle sliding step (replace + F^-1 g, numpy fp64, LAPACK Cholesky) at full d = {d}, "
+                      f"m = {m}: timed step {last - warmup}"),
+           "sec_per_step": t_step, "oracle_gram_s": t_gram}
+    return parity, cpu
 
 
 HOST_LINK_PEAK_GBS = 63.0   # PCIe 5.0 x16, per direction
@@ -477,11 +503,7 @@ def cpu_static_baseline(wl, G0, theta, lam, nsample):
     from oracle import mask as omask
     from oracle import static as ostatic
 
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        cores = os.cpu_count()
+    cores, blas = blas_info()
     d, B = wl.d, wl.block
     if d // B > 1:
         ds, bs = min(nsample, d // B) * B, B
@@ -496,7 +518,7 @@ def cpu_static_baseline(wl, G0, theta, lam, nsample):
     dg = ostatic.inv_diag(Gs, lam, bs)
     omask.keep_mask(omask.scores(ts, dg), ds // 2)
     sec = (time.perf_counter() - t0) * (d / ds)
-    return {"value": 1.0 / sec, "unit": "runs/s", "cores": int(cores), "kind": "oracle",
+    return {"value": 1.0 / sec, "unit": "runs/s", "cores": int(cores), "blas": blas, "kind": "oracle",
             "sample": (f"oracle inverse diagonal + scores + keep-mask (numpy fp64, Cholesky and triangular "
                        f"solve per block) on {what} of the same G, time x{d / ds:.0f}")}
 
@@ -509,11 +531,7 @@ def cpu_optimizer_baseline(wl, seed, nsteps):
     from oracle.optimizer import MFACOracle
     from synth import GradientStream
 
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        cores = os.cpu_count()
+    cores, blas = blas_info()
     from oracle.dynamic import WindowOracle
 
     gs = GradientStream(wl, seed=seed, device="cuda")   # rows drawn on the GPU, copied to the host
@@ -525,7 +543,7 @@ def cpu_optimizer_baseline(wl, seed, nsteps):
     for t in range(nsteps):
         w, _ = orc.step(w, steps[t], 1e-3)
     sec = (time.perf_counter() - t0) / nsteps
-    return {"value": 1.0 / sec, "unit": "optimizer steps/s", "cores": int(cores), "kind": "oracle",
+    return {"value": 1.0 / sec, "unit": "optimizer steps/s", "cores": int(cores), "blas": blas, "kind": "oracle",
             "sample": f"{nsteps} oracle M-FAC steps (fp64 window insert + F^-1 g) at d={wl.d}, m={wl.m}, "
                       "full window, model forward/backward excluded"}
 
@@ -533,13 +551,13 @@ def cpu_optimizer_baseline(wl, seed, nsteps):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dyn_resnet50_d25.6m_m1024")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-div", type=int, default=16)
-    ap.add_argument("--cpu-steps", type=int, default=12)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle: for the dynamic workloads both the full-d parity check and its timing")
+    ap.add_argument("--cpu-steps", type=int, default=12, help="optimizer workloads: oracle steps timed")
     ap.add_argument("--cpu-blocks", type=int, default=128,
                     help="static workloads: blocks the oracle baseline is timed on")
     ap.add_argument("--refactor-period", type=int, default=None,
@@ -572,10 +590,20 @@ def main():
     t0 = time.perf_counter()
     gs = GradientStream(wl, seed=args.seed, device=dev)
     win = P.Window(d, m, wl.lam, max_queries=nq, device=dev)
+    check = not args.no_cpu_baseline
+    # the oracle's copy of the initial window, taken before the library sees the rows
+    G_host = None
+    if check:
+        import numpy as np
+        G_host = np.empty((m, d), np.float32)
     batch = max(1, min(m, (4 << 30) // (4 * d)))
     for r0 in range(0, m, batch):
         n = min(batch, m - r0)
-        win.set_rows(r0, gs.rows(r0, n))
+        rows = gs.rows(r0, n)
+        if G_host is not None:
+            G_host[r0:r0 + n] = rows.cpu().numpy()
+        win.set_rows(r0, rows)
+        del rows
         log(f"window rows {r0 + n}/{m}")
     win.rebuild()
     if args.refactor_period is not None:
@@ -592,15 +620,22 @@ def main():
             Xq[t] = gs.queries(t, nq)
     Yq = torch.empty((nq, d), dtype=torch.float32, device=dev) if nq else None
     y = torch.empty(d, dtype=torch.float32, device=dev)
+    # outputs of the first, a middle and the last timed step are kept (each
+    # in its own buffer) for the oracle check after the timed region
+    checked = sorted({args.warmup, args.warmup + args.steps // 2, nsteps - 1}) if check else []
+    ys = {t: torch.empty(d, dtype=torch.float32, device=dev) for t in checked}
+    Yqs = {t: torch.empty((nq, d), dtype=torch.float32, device=dev) for t in checked} if nq else {}
     torch.cuda.synchronize()
     assert win.status() == 0
     log(f"setup {time.perf_counter() - t0:.1f} s (window {win.storage.numel() / 1e9:.1f} GB)")
 
-    def step(t):
+    def step(t, out=None):
+        outq = Yqs.get(t, Yq) if out is None else Yq
+        out = ys.get(t, y) if out is None else out
         if nq:
-            win.replace(steps_g[t], y_out=y, X=Xq[t], Y=Yq)
+            win.replace(steps_g[t], y_out=out, X=Xq[t], Y=outq)
         else:
-            win.replace(steps_g[t], y_out=y)
+            win.replace(steps_g[t], y_out=out)
 
     for t in range(args.warmup):
         step(t)
@@ -643,7 +678,7 @@ def main():
         win.set_refactor_period(0)
         win.trace(True)
         for t in range(3):
-            step(args.warmup + t)
+            step(args.warmup + t, out=y)
         torch.cuda.synchronize()
         win.trace(False)
         rms, rcnt = win.trace_read()
@@ -681,9 +716,13 @@ def main():
         ms_seq = s0.elapsed_time(s1) / args.steps
         fused = m <= 2048
         p2avg = sms[2] / max(scnt[2], 1)
+        # the sequence's first gradient needs its own pass 1 (phase 0, once);
+        # every later step reads the window once
+        steady = (s0.elapsed_time(s1) - sms[0]) / args.steps
         sequence = {
             "entry_point": "mfac_window_replace_seq", "steps": args.steps,
             "steps_per_s": 1000.0 / ms_seq, "ms_per_step": ms_seq,
+            "steady_ms_per_step": steady, "steady_steps_per_s": 1000.0 / steady,
             "window_reads_per_step": 1 if fused else 2,
             "ihvp_pass_ms": p2avg,
             # fused pass: reads the window and the next gradient, writes y
@@ -742,13 +781,19 @@ def main():
         "cpu_baseline": None,
         "calib_copy": {"kernel": "k_get_rows", "bytes_read": 4 * calib_rows * d, "bytes_written": 4 * calib_rows * d},
     }
-    if not args.no_cpu_baseline:
-        del steps_g, Xq, win
+    if check:
+        del win
         torch.cuda.empty_cache()
-        log("cpu baseline (oracle) ...")
+        log("oracle check at full d ...")
         t0 = time.perf_counter()
-        out["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_sample_div, args.cpu_steps)
-        log(f"cpu baseline took {time.perf_counter() - t0:.1f} s")
+        parity, cpu = oracle_check(wl, G_host, steps_g, args.warmup, set(checked), ys, Xq, Yqs)
+        out["parity"] = parity
+        out["cpu_baseline"] = cpu
+        log(f"oracle check took {time.perf_counter() - t0:.1f} s: {parity}")
+        if parity["max_rel_l2"] > parity["tol"]:
+            log("PARITY FAILURE: the library's outputs differ from the oracle")
+            print(json.dumps(out), flush=True)
+            sys.exit(1)
     print(json.dumps(out), flush=True)
 
 

@@ -55,7 +55,10 @@ typedef enum {
     MFAC_EWORKSPACE = -2,  /* storage or workspace smaller than the *_bytes query   */
     MFAC_EHIP = -3,        /* a HIP runtime call or kernel launch failed              */
     MFAC_ENONFINITE = -4,  /* non-finite data or non-positive pivot seen on device    */
-    MFAC_ESTATE = -5       /* call not valid in the handle's current state            */
+    MFAC_ESTATE = -5,      /* call not valid in the handle's current state            */
+    /* not a status: widens the enum to the full int32 range, so any code a C
+       caller passes (e.g. to mfac_status_string) is a valid value of the type */
+    MFAC_STATUS_INT32_ = 0x7fffffff
 } mfac_status;
 
 typedef struct mfac_window_s* mfac_window;
@@ -93,8 +96,9 @@ size_t mfac_window_workspace_bytes(int64_t d, int32_t m, int32_t max_queries);
  *              (all rows zero; Theorem 1 keeps the 1/m scale for the capacity
  *              m, so empty slots contribute nothing).
  * Enqueues: copy of G0 into the storage (or zero fill), Gram K = G G^T
- * (fp32 MFMA tiles, fp64 reduction), and the coefficient factor. The ring
- * head starts at slot 0. *out receives a host-allocated handle. */
+ * (fp64 MFMA tiles on the exact fp32 values, fp64 reduction), and the
+ * coefficient factor. The ring head starts at slot 0. *out receives a
+ * host-allocated handle. */
 mfac_status mfac_window_init(mfac_window* out, int64_t d, int32_t m, double lambda,
                              int32_t max_queries, void* storage, size_t storage_bytes,
                              void* workspace, size_t workspace_bytes,

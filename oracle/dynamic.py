@@ -35,8 +35,10 @@ class _F64Chunks:
     CPU copy does it with all threads and without fresh page faults.
     """
 
-    def __init__(self, rows, chunk=_CHUNK):
-        self.buf = np.empty((rows, chunk), np.float64)
+    def __init__(self, rows, chunk=_CHUNK, cols=None):
+        # the buffer is as wide as one chunk, or as the matrix when it is narrower
+        width = chunk if cols is None else max(1, min(chunk, cols))
+        self.buf = np.empty((rows, width), np.float64)
         self.chunk = chunk
 
     def __call__(self, A):
@@ -47,25 +49,44 @@ class _F64Chunks:
             yield j0, j1, b
 
 
-def gram(G, chunk=_CHUNK):
-    """K = G G^T in float64 from fp32 rows, accumulated over column chunks.
+def gram_accumulate(G, K, j0, j1, chunk=_CHUNK):
+    """Add the lower triangle of G[:, j0:j1] G[:, j0:j1]^T to K in float64.
 
-    Each chunk's product is the BLAS symmetric rank-k update (dsyrk) of the
-    chunk in float64; only its lower triangle is formed, then mirrored.
+    K is an m x m float64 array in Fortran order (start from zeros). Each
+    column chunk's product is the BLAS symmetric rank-k update (dsyrk) of the
+    chunk converted to float64; only the lower triangle of K is formed.
+    Calling it over consecutive column ranges that cover [0, d) and then
+    ``gram_symmetric`` gives ``gram(G)``; the returned K must be passed on
+    (dsyrk may return a new array).
     """
+    m = G.shape[0]
+    conv = _F64Chunks(m, chunk, j1 - j0)
+    for a in range(j0, j1, chunk):
+        b = conv.buf[:, :min(j1, a + chunk) - a]
+        torch.from_numpy(b).copy_(torch.from_numpy(G[:, a:a + b.shape[1]]))
+        K = sla.blas.dsyrk(1.0, b.T, beta=1.0, c=K, trans=1, lower=1, overwrite_c=1)
+    return K
+
+
+def gram_symmetric(K):
+    """The full symmetric Gram matrix (C order) from its accumulated lower triangle."""
+    L = np.tril(K)
+    return np.ascontiguousarray(L + np.tril(L, -1).T)
+
+
+def gram(G, chunk=_CHUNK):
+    """K = G G^T in float64 from fp32 rows, accumulated over column chunks
+    (``gram_accumulate`` over all d columns, then mirrored)."""
     m, d = G.shape
     K = np.zeros((m, m), np.float64, order="F")
-    for _, _, b in _F64Chunks(m, chunk)(G):
-        K = sla.blas.dsyrk(1.0, b.T, beta=1.0, c=K, trans=1, lower=1, overwrite_c=1)
-    K = np.tril(K)
-    return np.ascontiguousarray(K + np.tril(K, -1).T)
+    return gram_symmetric(gram_accumulate(G, K, 0, d, chunk))
 
 
 def matvec(G, X, chunk=_CHUNK):
     """P = G X^T (m x n) in float64; X is (n, d) fp32."""
     m, d = G.shape
     P = np.zeros((m, X.shape[0]), np.float64)
-    conv = _F64Chunks(m, chunk)
+    conv = _F64Chunks(m, chunk, d)
     for j0, j1, b in conv(G):
         P += b @ X[:, j0:j1].astype(np.float64).T
     return P
@@ -75,17 +96,23 @@ class WindowOracle:
     """The m x d window, its float64 Gram matrix, and exact IHVPs.
 
     ``G0`` (m x d fp32) initialises the window; None starts with zero rows.
+    ``copy=False`` keeps the caller's G0 array as the window (it is then
+    modified in place by replace).
     """
 
-    def __init__(self, d, m, lam, G0=None):
+    def __init__(self, d, m, lam, G0=None, K=None, copy=True):
         self.d, self.m, self.lam = int(d), int(m), float(lam)
         if G0 is None:
             self.G = np.zeros((m, d), np.float32)
             self.K = np.zeros((m, m), np.float64)
         else:
-            self.G = np.array(G0, dtype=np.float32, copy=True)
-            assert self.G.shape == (m, d)
-            self.K = gram(self.G)
+            self.G = np.array(G0, dtype=np.float32, copy=True) if copy else G0
+            assert self.G.shape == (m, d) and self.G.dtype == np.float32
+            # K: the Gram matrix of G0 when the caller formed it already (with
+            # gram_accumulate over column ranges, for windows too large to
+            # redo); otherwise computed here
+            self.K = gram(self.G) if K is None else np.array(K, dtype=np.float64)
+            assert self.K.shape == (m, m)
         self.steps = 0
 
     def replace(self, slot, g):
@@ -133,6 +160,6 @@ class WindowOracle:
             P = matvec(self.G, X)
         U = self.coefficients(P)
         Y = np.empty(X.shape, np.float64)
-        for j0, j1, b in _F64Chunks(self.m)(self.G):
+        for j0, j1, b in _F64Chunks(self.m, cols=self.d)(self.G):
             Y[:, j0:j1] = (X[:, j0:j1].astype(np.float64) - U.T @ b) / self.lam
         return Y[0] if single else Y

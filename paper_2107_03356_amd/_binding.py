@@ -225,6 +225,20 @@ class Window:
     def set_head(self, head, steps):
         _check("mfac_window_set_head", load().mfac_window_set_head(self.handle, int(head), int(steps)))
 
+    def set_stream(self, stream=None):
+        """Bind later calls to ``stream`` (a torch stream; default: the current
+        one). The new stream first waits for the work already enqueued on the
+        old one, so the window's calls stay in order across the switch."""
+        t = self.torch
+        new = stream if stream is not None else t.cuda.current_stream(self.device)
+        if new.cuda_stream == self.stream:
+            return
+        ev = t.cuda.Event()
+        ev.record(t.cuda.ExternalStream(self.stream, device=self.device))
+        new.wait_event(ev)
+        self.stream = new.cuda_stream
+        _check("mfac_window_set_stream", load().mfac_window_set_stream(self.handle, self.stream))
+
     def set_refactor_period(self, period):
         _check("mfac_window_set_refactor_period", load().mfac_window_set_refactor_period(self.handle, int(period)))
 

@@ -136,11 +136,20 @@ bool window_sizes_ok(int64_t d, int32_t m, int32_t max_q) {
     } while (0)
 
 // Tracing: mark_begin before a phase's first launch, mark_end after its last.
+// A phase whose launch failed leaves its begin event open: the next
+// mark_begin (or marks_free) releases it.
 template <typename H>
 hipError_t mark_begin(H* h) {
     if (!h->trace) return hipSuccess;
+    if (h->open_ev) {
+        (void)hipEventDestroy(h->open_ev);
+        h->open_ev = nullptr;
+    }
     hipError_t e = hipEventCreate(&h->open_ev);
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess) {
+        h->open_ev = nullptr;
+        return e;
+    }
     return hipEventRecord(h->open_ev, h->st);
 }
 
@@ -152,8 +161,10 @@ hipError_t mark_end(H* h, int phase) {
     if (e != hipSuccess) return e;
     e = hipEventRecord(b, h->st);
     h->marks->push_back({phase, h->open_ev, b});
+    h->open_ev = nullptr;
     return e;
 }
+
 
 // Sum and release the recorded marks of a handle into ms/count (nph phases).
 template <typename H>
@@ -179,6 +190,10 @@ mfac_status marks_read(H* h, int nph, double* ms_out, int64_t* count_out) {
 
 template <typename H>
 void marks_free(H* h) {
+    if (h->open_ev) {
+        (void)hipEventDestroy(h->open_ev);
+        h->open_ev = nullptr;
+    }
     if (!h->marks) return;
     for (auto& mk : *h->marks) {
         (void)hipEventDestroy(mk.a);
@@ -220,6 +235,7 @@ MFAC_API const char* mfac_status_string(mfac_status s) {
         case MFAC_EHIP: return "HIP runtime or launch failure";
         case MFAC_ENONFINITE: return "non-finite value or non-positive pivot on device";
         case MFAC_ESTATE: return "call not valid in the current state";
+        default: break;
     }
     return "unknown status";
 }

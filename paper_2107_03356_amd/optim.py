@@ -82,6 +82,12 @@ class MFAC(torch.optim.Optimizer):
             torch._foreach_copy_(gv, grads)
             if group["weight_decay"]:
                 torch._foreach_add_(gv, ps, alpha=group["weight_decay"])
+        # the library enqueues on the window's stream: follow the stream this
+        # step runs on, so the copies into _g above and the update below are
+        # ordered with the window's passes
+        cur = torch.cuda.current_stream(self.device).cuda_stream
+        if cur != self.window.stream:
+            self.window.set_stream()
         self.window.replace(self._g, y_out=self._y)
         for group, (_, yv) in zip(self.param_groups, self._views):
             torch._foreach_add_(group["params"], yv, alpha=-group["lr"])

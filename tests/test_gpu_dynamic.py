@@ -399,6 +399,43 @@ def test_default_policy_over_a_refactor_boundary_m1024(dev):
     assert win.info() == (1100 % wl.m, 1100)
 
 
+def test_default_policy_m1024_at_resnet50_conditioning(dev):
+    """The ResNet50 window's conditioning at a size the oracle can follow for
+    1100 steps: m = 1024, lambda = 1e-5, log-normal scales with 10% correlated
+    rows, and entries scaled by 1/sqrt(d) of this d, so |g|^2 / (m lambda) is
+    about 720 as in the full-size workload (the Fisher term far above the
+    damping). Default coefficient policy: O(m^2) inverse updates with the
+    scheduled refactor after 1024 replaces; checked early, every 100 steps,
+    right before, at and after the refactor, and at the end."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_resnet50_d25.6m_m1024")
+    d = 12000
+    wl = base.scaled(d=d, scale_d=d)
+    assert wl.corr_frac == 0.1 and wl.lam == 1e-5 and wl.m == 1024
+    gs = GradientStream(wl, seed=24, device="cpu")
+    G0 = gs.window()
+    ratio = float((G0.double() ** 2).sum(1).mean()) / (wl.m * wl.lam)
+    assert 300 < ratio < 3000, ratio
+    win = Window(wl.d, wl.m, wl.lam, G0=G0.to(dev), device=dev)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    checked = {0, 1, 2, 1021, 1022, 1023, 1024, 1025, 1099} | set(range(99, 1100, 100))
+    say("default policy at the ResNet50 conditioning, m = 1024, d =", d, "|g|^2/(m lambda) =", round(ratio))
+    errs = {}
+    for t in range(1100):
+        g = gs.row(wl.m + t)
+        y = win.replace(g.to(dev))
+        if t in checked:
+            yo = orc.slide(g.numpy())
+            errs[t] = rel_l2(y.cpu().numpy(), yo)
+            assert errs[t] < REL_TOL, (t, errs[t])
+        else:
+            orc.replace(orc.steps % wl.m, g.numpy())
+    assert win.status() == 0
+    say("errors", {k: f"{v:.1e}" for k, v in sorted(errs.items())})
+    # no growth over the 1023 updates before the refactor beyond fp32 rounding
+    assert max(errs.values()) < 1e-5, errs
+
+
 def test_two_windows_on_two_streams_interleaved(dev):
     """Handles are independent: two windows, each bound to its own stream,
     replaced alternately without host synchronisation, both match their oracles."""

@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import require_gpu, say
+from gpu_common import REL_TOL, rel_l2, require_gpu, say
+from oracle.dynamic import WindowOracle
 from oracle.optimizer import MFACOracle
 from synth.optim import linear_problem, mlp_problem
 
@@ -83,6 +84,10 @@ def test_mlp_training_matches_oracle(dev):
     opt = MFAC(params, lr=lr, m=m, damp=lam)
     d = sum(w.numel() for w in ws)
     orc = MFACOracle(d, m, lam)
+    # the library's own gradient sequence through an oracle window: the
+    # per-step IHVP is checked at the 1e-4 bar, apart from the fp32-vs-fp64
+    # autograd drift that the weight comparison below carries
+    win_or = WindowOracle(d, m, lam)
     w_or = _flat(ws)
     w_start = w_or.copy()
     say("optimizer mlp", d, m)
@@ -91,6 +96,9 @@ def test_mlp_training_matches_oracle(dev):
         opt.zero_grad()
         _mlp_loss(params, x.float().to(dev), y.float().to(dev)).backward()
         opt.step()
+        g_lib = opt._g.cpu().numpy()
+        ihvp_err = rel_l2(opt.preconditioned().cpu().numpy(), win_or.slide(g_lib))
+        assert ihvp_err < REL_TOL, (t, ihvp_err)
         # oracle: fp64 autograd at the oracle's own weights
         wt, off = [], 0
         for w in ws:
@@ -103,6 +111,45 @@ def test_mlp_training_matches_oracle(dev):
         assert err < 1e-3, (t, err)
     torch.cuda.synchronize()
     assert opt.status() == 0
+
+
+def test_steps_on_a_side_stream_match_oracle(dev):
+    """The optimizer built on the default stream, stepped under a side stream
+    (forward, backward, gradient copy, window replace and update all on it):
+    the window follows the step's stream. The run equals, bit for bit, the
+    same run on the default stream, and matches the oracle."""
+    from paper_2107_03356_amd.optim import MFAC
+    shapes = [(300, 7), (11,)]
+    steps, m, lam, lr = 9, 4, 0.2, 1.0
+    w0, C = linear_problem(seed=6, shapes=shapes, steps=steps)
+    w0 = [w.float().double() for w in w0]                 # both sides start from the fp32 weights
+    C = [[c.float() for c in ct] for ct in C]             # and see the same fp32 gradients
+
+    def run(stream):
+        params = [torch.nn.Parameter(w.float().to(dev)) for w in w0]
+        opt = MFAC(params, lr=lr, m=m, damp=lam)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            for t in range(steps):
+                opt.zero_grad()
+                sum((c.to(dev) * p).sum() for c, p in zip(C[t], params)).backward()
+                opt.step()
+            assert opt.window.stream == stream.cuda_stream
+        torch.cuda.synchronize()
+        assert opt.status() == 0
+        return _flat(params)
+
+    say("optimizer on a side stream", sum(int(np.prod(s)) for s in shapes), m)
+    on_side = run(torch.cuda.Stream(device=dev))
+    on_default = run(torch.cuda.current_stream(dev))
+    assert np.array_equal(on_side, on_default)
+    d = sum(int(np.prod(s)) for s in shapes)
+    orc = MFACOracle(d, m, lam)
+    w_or = _flat(w0)
+    w_start = w_or.copy()
+    for t in range(steps):
+        w_or, _ = orc.step(w_or, _flat(C[t]), lr)
+    assert _disp_err(on_side, w_or, w_start) < 1e-5
 
 
 def test_checkpoint_resume_continues_the_run(dev):

@@ -243,3 +243,27 @@ def test_oracle_detects_planted_mistakes():
     dropped = x64 / lam
     for bad in (wrong_scale, wrong_sign, dropped):
         assert _rel(bad, truth) > 1e-3
+
+
+def test_gram_accumulate_over_column_ranges_matches_dense_product():
+    """The chunk-range Gram that large-window tests use (uneven ranges, chunks
+    smaller than a range) equals the fp64 product of the whole matrix, and a
+    window built from it gives the dense-solve IHVPs (Section 3.2 initial
+    setup: K = G G^T)."""
+    from oracle import dynamic as odyn
+    rng = np.random.default_rng(31)
+    m, d, lam = 9, 1000, 1e-3
+    G = _rand_window(rng, m, d)
+    K = np.zeros((m, m), np.float64, order="F")
+    for j0, j1 in ((0, 333), (333, 334), (334, 901), (901, 1000)):
+        K = odyn.gram_accumulate(G, K, j0, j1, chunk=128)
+    K = odyn.gram_symmetric(K)
+    G64 = G.astype(np.float64)
+    assert _rel(K, G64 @ G64.T) < 1e-14
+    assert np.array_equal(K, K.T)
+    o = WindowOracle(d, m, lam, G0=G, K=K)
+    X = rng.standard_normal((2, d)).astype(np.float32)
+    assert _rel(o.ihvp(X), bruteforce.ihvp(G, lam, X)) < 1e-10
+    # ranges that miss columns give a different matrix (the test would see it)
+    K2 = odyn.gram_symmetric(odyn.gram_accumulate(G, np.zeros((m, m), order="F"), 0, 999, chunk=128))
+    assert _rel(K2, G64 @ G64.T) > 1e-6
