@@ -150,6 +150,22 @@ mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const float* Gn, f
  * factor. 1 <= n <= max_queries + 1 (the vectors one replace carries). */
 mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* Y);
 
+/* mfac_ihvp for callers that cannot allocate device memory or pass a
+ * workspace per call (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same computation and results, with
+ * the call's scratch (pass-1 partial sums, their reduction and the
+ * coefficients) in a fixed 16 MiB device array inside the library instead of
+ * the window's workspace. Allocates nothing; no hipMalloc, hipFree or
+ * allocating library routine. The array exists once per GPU (held until the
+ * process ends; its address is resolved at mfac_window_init) and is shared by
+ * every call on that GPU, so calls that overlap on one GPU (several streams
+ * or host threads) race and must be serialised by the caller; it keeps the
+ * last call's contents, which later calls overwrite before reading.
+ * Limit: (512 + 2) * m * n * 8 bytes (each part rounded up to 256) <= 16 MiB,
+ * i.e. m * n <= 4080; larger returns MFAC_EWORKSPACE before anything is
+ * enqueued. Other arguments and errors as mfac_ihvp. */
+mfac_status mfac_ihvp_noalloc(mfac_window w, int32_t n, const float* X, float* Y);
+
 /* Copy rows [first, first+count) back as count x d row-major fp32 (device
  * pointer). Synchronises the stream. */
 mfac_status mfac_window_get_rows(mfac_window w, int32_t first, int32_t count, float* rows_out);

@@ -40,6 +40,7 @@ SIGNATURES = {
     "mfac_window_replace": (_c.c_int, [_VP, _I32, _VP, _VP, _I32, _VP, _VP]),
     "mfac_window_replace_seq": (_c.c_int, [_VP, _I32, _VP, _VP]),
     "mfac_ihvp": (_c.c_int, [_VP, _I32, _VP, _VP]),
+    "mfac_ihvp_noalloc": (_c.c_int, [_VP, _I32, _VP, _VP]),
     "mfac_window_get_rows": (_c.c_int, [_VP, _I32, _I32, _VP]),
     "mfac_window_info": (_c.c_int, [_VP, _c.POINTER(_I32), _c.POINTER(_I64)]),
     "mfac_window_set_head": (_c.c_int, [_VP, _I32, _I64]),

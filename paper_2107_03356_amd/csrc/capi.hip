@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "../../include/mfac.h"
@@ -40,11 +41,46 @@ bool aligned4(const void* p) { return ((uintptr_t)p & 3u) == 0; }
 int64_t nslab_of(int64_t d) { return ceil_div(d, SLAB); }
 int padded_m(int m) { return (int)round_up(m, NB); }
 
+// ---------------------------------------------------------------- allocation-free IHVP
+// Scratch of mfac_ihvp_noalloc: a file-scope device array, one per GPU the
+// library runs on, held until the process ends. Host code never uses the
+// array's name as an address: it takes the device address from
+// hipGetSymbolAddress, once per device (at window init, with the window's
+// device current), and passes that pointer on.
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(16) << 20;
+__device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_dev[MAX_DEVICES];
+
+// Device address of this device's scratch (resolved on first use per device).
+hipError_t scratch_address(int device, void** out) {
+    *out = nullptr;
+    if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(scratch_mu);
+    if (!scratch_dev[device]) {
+        int cur = -1;
+        hipError_t e = hipGetDevice(&cur);
+        if (e != hipSuccess) return e;
+        if (cur != device && (e = hipSetDevice(device)) != hipSuccess) return e;
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != device) (void)hipSetDevice(cur);
+        if (e != hipSuccess) return e;
+        scratch_dev[device] = ptr;
+    }
+    *out = scratch_dev[device];
+    return hipSuccess;
+}
+
+
 }  // namespace
 
 struct mfac_window_s {
     int64_t d;
     int m, mp, max_q;
+    int device;  // the device of the handle's stream at init
     double lambda;
     int64_t nslab;
     float* G;
@@ -165,7 +201,6 @@ hipError_t mark_end(H* h, int phase) {
     return e;
 }
 
-
 // Sum and release the recorded marks of a handle into ms/count (nph phases).
 template <typename H>
 mfac_status marks_read(H* h, int nph, double* ms_out, int64_t* count_out) {
@@ -278,6 +313,18 @@ MFAC_API mfac_status mfac_window_init(mfac_window* out, int64_t d, int32_t m, do
     w->G = (float*)storage;
     w->st = stream;
     w->period = m > 1024 ? m : 1024;
+    if (hipStreamGetDevice(stream, &w->device) != hipSuccess) {
+        free(w);
+        return MFAC_EHIP;
+    }
+    {
+        // the allocation-free IHVP's scratch on this device, resolved once
+        void* sp = nullptr;
+        if (scratch_address(w->device, &sp) != hipSuccess) {
+            free(w);
+            return MFAC_EHIP;
+        }
+    }
     window_layout<mfac_window_s>(d, m, max_queries, (char*)workspace, w);
 
     mfac_status rc = MFAC_OK;
@@ -460,10 +507,11 @@ MFAC_API mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const flo
     return MFAC_OK;
 }
 
-MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* Y) {
-    if (!w || !X || !Y) return MFAC_EINVAL;
-    if (n < 1 || n > w->max_q + 1) return MFAC_EINVAL;
-    if (!aligned4(X) || !aligned4(Y)) return MFAC_EINVAL;
+namespace {
+
+// Y = F^-1 X for n rows: pass 1 into part, its reduction into p, the
+// coefficients into coef, pass 2 (part, p, coef: scratch of the call).
+mfac_status ihvp_run(mfac_window w, int32_t n, const float* X, float* Y, double* part, double* p, double* coef) {
     const int64_t d = w->d;
     const bool al = aligned16(X) && aligned16(Y) && (n == 1 || d % 4 == 0);
     VecIn vin{};
@@ -477,16 +525,47 @@ MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* 
     }
     Pass1Grid grid{};
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, n, vin, al, w->part, &grid, w->st));
+    HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, n, vin, al, part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_reduce_partials(w->part, grid, w->m, n, w->p, w->st));
-    HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p, n, n, -1, inv_lam, inv_lam, w->coef, w->err, w->st));
+    HIPCHK(launch_reduce_partials(part, grid, w->m, n, p, w->st));
+    HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, p, n, n, -1, inv_lam, inv_lam, coef, w->err, w->st));
     HIPCHK(mark_end(w, 1));
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, n, w->coef, vout, al, w->st));
+    HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, n, coef, vout, al, w->st));
     HIPCHK(mark_end(w, 2));
     return MFAC_OK;
+}
+
+bool ihvp_args_ok(mfac_window w, int32_t n, const float* X, float* Y) {
+    return w && X && Y && n >= 1 && n <= w->max_q + 1 && aligned4(X) && aligned4(Y);
+}
+
+// Scratch layout of one call: pass-1 partials (at most PASS1_MAX_GRID
+// work-groups x m rows x n vectors), the reduced sums p and the coefficients.
+size_t noalloc_need(int m, int n, size_t* off_p, size_t* off_c) {
+    const size_t mn = (size_t)m * n * sizeof(double);
+    const size_t part = align256((size_t)PASS1_MAX_GRID * mn);
+    *off_p = part;
+    *off_c = part + align256(mn);
+    return *off_c + align256(mn);
+}
+
+}  // namespace
+
+MFAC_API mfac_status mfac_ihvp(mfac_window w, int32_t n, const float* X, float* Y) {
+    if (!ihvp_args_ok(w, n, X, Y)) return MFAC_EINVAL;
+    return ihvp_run(w, n, X, Y, w->part, w->p, w->coef);
+}
+
+MFAC_API mfac_status mfac_ihvp_noalloc(mfac_window w, int32_t n, const float* X, float* Y) {
+    if (!ihvp_args_ok(w, n, X, Y)) return MFAC_EINVAL;
+    size_t op, oc;
+    if (noalloc_need(w->m, n, &op, &oc) > NOALLOC_SCRATCH_BYTES) return MFAC_EWORKSPACE;
+    void* base = nullptr;
+    HIPCHK(scratch_address(w->device, &base));
+    char* b = (char*)base;
+    return ihvp_run(w, n, X, Y, (double*)b, (double*)(b + op), (double*)(b + oc));
 }
 
 MFAC_API mfac_status mfac_window_get_rows(mfac_window w, int32_t first, int32_t count, float* rows_out) {

@@ -368,6 +368,7 @@ void check_rejections() {
     CHECK(w == nullptr);
     CHECK(mfac_window_replace(nullptr, -1, (float*)256, nullptr, 0, nullptr, nullptr) == MFAC_EINVAL);
     CHECK(mfac_ihvp(nullptr, 1, (float*)256, (float*)512) == MFAC_EINVAL);
+    CHECK(mfac_ihvp_noalloc(nullptr, 1, (float*)256, (float*)512) == MFAC_EINVAL);
     CHECK(mfac_window_destroy(nullptr) == MFAC_OK);
     CHECK(mfac_static_destroy(nullptr) == MFAC_OK);
     // size queries at the edges of what is accepted (UBSan: no overflow)
@@ -415,6 +416,7 @@ void drive_window(int64_t d, int m, int q) {
         CHECK(mfac_window_replace_seq(w, 5, Gn, Yn) == MFAC_OK);
         CHECK(mfac_ihvp(w, q + 1, X, Y) == MFAC_OK);
         CHECK(mfac_ihvp(w, q + 2, X, Y) == MFAC_EINVAL);
+        CHECK(mfac_ihvp_noalloc(w, 1, X, Y) == ((int64_t)m * 1 <= 4080 ? MFAC_OK : MFAC_EWORKSPACE));
         CHECK(mfac_window_set_rows(w, 0, m, G0) == MFAC_OK);
         CHECK(mfac_window_set_rows(w, 1, m, G0) == MFAC_EINVAL);
         CHECK(mfac_window_rebuild(w) == MFAC_OK);
