@@ -185,9 +185,13 @@ def bench_static(args, wl, dev):
 
     P.load()
     d, m, B = wl.d, wl.m, wl.block
+    paged = wl.page_cols > 0
+    # the fast mode (fp32 matrix cores, exact mask) wherever it applies
+    fast = not args.fp64 and not paged and m <= 4096 and B <= 65536
     # algorithmic flops per run: symmetric Gram m^2 B and triangular W = L^-1 G_b
     # m^2 B per block (2 m^2 d together), Cholesky and triangular inverse m^3/3 each
     flops = 2.0 * m * m * d + 2.0 * (m ** 3 / 3.0) * (d // B)
+    mfma_peak = 157.3 if fast else 78.6   # the dominant kernel's dtype: fp32 or fp64 matrix cores
     t0 = time.perf_counter()
     gs = GradientStream(wl, seed=args.seed, device=dev)
     G0 = torch.empty((m, d), dtype=torch.float32, device=dev)
@@ -196,7 +200,6 @@ def bench_static(args, wl, dev):
         if r % 256 == 255:
             log(f"rows {r + 1}/{m}")
     theta = gs.theta()
-    paged = wl.page_cols > 0
     G = torch.empty((m, d), dtype=torch.float32, pin_memory=True) if paged else torch.empty_like(G0)
     pages = dict(page_cols=wl.page_cols, device=dev) if paged else {}
     keep = d // 2
@@ -209,7 +212,7 @@ def bench_static(args, wl, dev):
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        sb = P.StaticBlocks(G, B, wl.lam, trace=True, **pages)
+        sb = P.StaticBlocks(G, B, wl.lam, trace=True, fp32=fast, **pages)
         diag = sb.inv_diag()
         mask, _ = sb.obs_mask(theta, keep, scores=False)
         e1.record(stream)
@@ -233,8 +236,13 @@ def bench_static(args, wl, dev):
     gram_flops = float(m) * m * d * runs / max(stage_cnt[0], 1)
     gram_tf = gram_flops / (gram_ms * 1e-3) / 1e12
 
-    # queries on the finished precompute (W in place of G): block-wise IHVP
-    # with 1 and 4 vectors, and the OBS correction for the keep-mask's complement
+    # the last run's outputs, for the oracle check below
+    mask_last = mask.cpu().numpy()
+    diag_last = sb.inv_diag(fp64=True).cpu().numpy()
+
+    # queries on the finished precompute (W in place of G, or formed into the
+    # workspace by the first query in the fast mode): block-wise IHVP with 1
+    # and 4 vectors, and the OBS correction for the keep-mask's complement
     queries = {}
     X = torch.empty((4, d), dtype=torch.float32, device=dev)
     for q in range(4):
@@ -242,7 +250,13 @@ def bench_static(args, wl, dev):
     reps = 2 if paged else 10
     for n in (1, 4):
         Y = torch.empty((n, d), dtype=torch.float32, device=dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
         sb.ihvp(X[:n], Y)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if n == 1 and fast:
+            queries["first_query_ms_incl_w"] = e0.elapsed_time(e1)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(reps):
@@ -278,25 +292,35 @@ def bench_static(args, wl, dev):
                 "download_gbs": down / (ms * 1e-3) / 1e9, "peak_gbs_per_direction": HOST_LINK_PEAK_GBS,
                 "frac_upload": up / (ms * 1e-3) / 1e9 / HOST_LINK_PEAK_GBS}
         log(f"host link: {link}")
+    parity = None
     if not args.no_cpu_baseline:
         del G, X, Y, delta
         torch.cuda.empty_cache()
         log("cpu baseline (oracle) ...")
-        cpu = cpu_static_baseline(wl, G0, theta, wl.lam, args.cpu_blocks)
+        if B < d:
+            parity, cpu = oracle_static_check(wl, G0, theta, keep, mask_last, diag_last)
+            log(f"oracle check: {parity}")
+        else:
+            cpu = cpu_static_baseline(wl, G0, theta, wl.lam, args.cpu_blocks)
         log(f"cpu baseline {cpu}")
+    gram_kernel = "k_gram_blocks32" if fast else "k_gram_blocks"
     out = {
         "metric": ("static block-wise precompute + inverse diagonal + top-50% OBD mask, runs/sec (1 GPU"
                    + (", G paged from pinned host memory)" if paged else ")")),
         "value": 1000.0 / ms, "unit": "runs/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
-        "data": "synthetic",
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if fast else "f64", "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep,
-                   "page_cols": wl.page_cols or None},
-        "roofline": {"bound": "mfma", "kernel": "k_gram_blocks", "achieved": gram_tf, "peak": 78.6,
-                     "unit": "TFLOP/s", "frac": gram_tf / 78.6, "traffic": read_static_counters(wl.name, "k_gram_blocks")},
+                   "page_cols": wl.page_cols or None,
+                   "mode": ("fast: Gram and W on fp32 matrix cores, fp64 factor, fp64 band re-decided at the cut"
+                            if fast else "fp64 matrix cores throughout")},
+        "roofline": {"bound": "mfma", "kernel": gram_kernel, "achieved": gram_tf, "peak": mfma_peak,
+                     "unit": "TFLOP/s", "frac": gram_tf / mfma_peak,
+                     "traffic": read_static_counters(wl.name, gram_kernel)},
         "whole_run": {"achieved_tflops": flops / (ms * 1e-3) / 1e12,
-                      "frac": flops / (ms * 1e-3) / 1e12 / 78.6,
+                      "frac": flops / (ms * 1e-3) / 1e12 / mfma_peak,
                       "flops": flops},
+        "parity": parity,
         "stages_ms_per_run": {"gram": stage_ms[0] / runs, "factor_inverse": stage_ms[1] / runs,
                               "w_and_diag": stage_ms[2] / runs, "scores_mask": stage_ms[3] / runs},
         "stage_launches_per_run": {"gram": stage_cnt[0] // runs, "factor_inverse": stage_cnt[1] // runs,
@@ -306,6 +330,9 @@ def bench_static(args, wl, dev):
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+    if parity is not None and parity["mask_mismatches"]:
+        log("PARITY FAILURE: the keep-mask differs from the oracle's")
+        sys.exit(1)
 
 
 def resnet20(num_classes=10):
@@ -494,6 +521,49 @@ def bench_optimizer(args, wl, dev):
     print(json.dumps(out), flush=True)
 
 
+def oracle_static_check(wl, G0, theta, keep, mask_gpu, diag_gpu):
+    """The oracle's inverse diagonal of every block (oracle.static.inv_diag,
+    a pool of threads over blocks, one BLAS thread each), its scores and
+    global keep-mask, compared with the library's last run: the mask bit for
+    bit, the diagonal and scores relative. The oracle's whole run is timed as
+    the CPU baseline."""
+    import concurrent.futures as cf
+
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import mask as omask
+    from oracle import static as ostatic
+
+    d, B = wl.d, wl.block
+    Gh = G0.cpu().numpy()
+    th = theta.cpu().numpy()
+    nthreads = max(1, min(16, os.cpu_count() or 1))
+    dref = np.empty(d)
+
+    def one(b):
+        dref[b * B:(b + 1) * B] = ostatic.inv_diag(Gh, wl.lam, B, blocks=[b])
+
+    t0 = time.perf_counter()
+    with threadpool_limits(1), cf.ThreadPoolExecutor(nthreads) as ex:
+        list(ex.map(one, range(d // B)))
+    sref = omask.scores(th, dref)
+    mref = omask.keep_mask(sref, keep)
+    sec = time.perf_counter() - t0
+    nz = sref > 0
+    sgpu = omask.scores(th, diag_gpu)
+    parity = {"mask_mismatches": int(np.count_nonzero(mref != mask_gpu)), "mask_bits": int(d),
+              "diag_max_rel": float(np.max(np.abs(diag_gpu - dref) / np.abs(dref))),
+              "score_max_rel": float(np.max(np.abs(sgpu[nz] - sref[nz]) / sref[nz])),
+              "oracle": "fp64 Woodbury per block (Cholesky, triangular solve) over all blocks"}
+    _, blas = blas_info()
+    cpu = {"value": 1.0 / sec, "unit": "runs/s", "cores": nthreads, "blas": blas, "kind": "oracle",
+           "sample": (f"the whole run: oracle inverse diagonal of all {d // B} blocks + scores + keep-mask "
+                      f"(numpy fp64; {nthreads} threads over blocks, one BLAS thread each)"),
+           "sec_per_run": sec}
+    return parity, cpu
+
+
 def cpu_static_baseline(wl, G0, theta, lam, nsample):
     """The oracle's block-wise inverse diagonal, scores and keep-mask (fp64) on a
     column sample of the same G: the first `nsample` whole blocks, or for B = d
@@ -560,6 +630,8 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=12, help="optimizer workloads: oracle steps timed")
     ap.add_argument("--cpu-blocks", type=int, default=128,
                     help="static workloads: blocks the oracle baseline is timed on")
+    ap.add_argument("--fp64", action="store_true",
+                    help="static workloads: the fp64 mode (default: the fast fp32 mode where it applies)")
     ap.add_argument("--refactor-period", type=int, default=None,
                     help="coefficient policy: full refactor every N replaces (0 = every replace); default: the library's")
     args = ap.parse_args()

@@ -56,6 +56,7 @@ typedef enum {
     MFAC_EHIP = -3,        /* a HIP runtime call or kernel launch failed              */
     MFAC_ENONFINITE = -4,  /* non-finite data or non-positive pivot seen on device    */
     MFAC_ESTATE = -5,      /* call not valid in the handle's current state            */
+    MFAC_EPRECISION = -6,  /* fast static mode: the keep-mask could not be certified   */
     /* not a status: widens the enum to the full int32 range, so any code a C
        caller passes (e.g. to mfac_status_string) is a valid value of the type */
     MFAC_STATUS_INT32_ = 0x7fffffff
@@ -233,9 +234,11 @@ size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m);
  * also writes over G: V_i = sqrt(q_i / lambda) W_i). The inverse diagonal
  * diag(F_b^-1) = (1 - sum_i W_b[i,:]^2) / lambda is formed in fp64 from the
  * unrounded W and kept in the workspace.
+ * With MFAC_STATIC_FP32 the precompute leaves G intact instead (see the flag).
  * Requirements: 1 <= m <= 8192, 4 <= block, block % 4 == 0,
  * d % block == 0, d <= 2^32 - 256, lambda > 0 finite, G 16-byte aligned,
- * workspace 256-byte aligned, flags a combination of MFAC_STATIC_* bits. */
+ * workspace 256-byte aligned (at least mfac_static_workspace_bytes_flags for
+ * the flags given), flags a combination of MFAC_STATIC_* bits. */
 mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m,
                                    double lambda, float* G, void* workspace,
                                    size_t workspace_bytes, uint32_t flags, hipStream_t stream);
@@ -243,6 +246,23 @@ mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, i
 /* flags of mfac_static_precompute and mfac_static_precompute_paged */
 #define MFAC_STATIC_TRACE 1u /* record HIP events around the precompute's stages and
                                 mfac_obs_mask; read with mfac_static_trace_read */
+/* Fast mode (mfac_static_precompute only; m <= 4096, block <= 65536): the
+ * Gram matrices and W on fp32 matrix cores (fp32 products, sums of up to 512
+ * products in fp32 then fp64; the factor stays fp64). The inverse diagonal then
+ * carries the fp32 rounding (about 1e-8 relative on gradient-like data with a
+ * well-conditioned G_b G_b^T + m*lambda*I). G is left intact: the fp32 L^-1 of
+ * every block is kept in the workspace, and W is formed into the workspace by
+ * the first query that reads it (mfac_static_ihvp, mfac_static_element,
+ * mfac_obs_update). mfac_obs_mask stays exact: coordinates whose fp64 score
+ * lies within 1e-5 relative of the cut get their diagonal recomputed in fp64
+ * (iterative refinement against G, see mfac_obs_mask), so the mask equals the
+ * fp64 mask whenever the fp32 path's score error is below about 1e-5. */
+#define MFAC_STATIC_FP32 2u
+
+/* Workspace bytes for mfac_static_precompute with these flags (the fast mode
+ * needs more: the fp32 L^-1 of every block, m*d floats for W, and the band
+ * list). 0 on invalid sizes or flags. */
+size_t mfac_static_workspace_bytes_flags(int64_t d, int32_t block, int32_t m, uint32_t flags);
 
 /* Host-paged static precompute, for a G larger than the device should hold
  * (Appendix C, swapping gradient blocks between host and GPU memory; here
@@ -287,14 +307,31 @@ mfac_status mfac_static_trace_read(mfac_static s, double* ms_out /* host */, int
  * the identity selection), rounded to fp32. */
 mfac_status mfac_inv_diag(mfac_static s, float* diag_out);
 
-/* Same, in fp64. */
+/* Same, in fp64 (fp64-accurate in the default mode; in the fast mode it has
+ * the fp32 path's error, except coordinates that an mfac_obs_mask call
+ * recomputed in its band). */
 mfac_status mfac_inv_diag64(mfac_static s, double* diag_out);
 
 /* OBD saliency rho_j = theta_j^2 / (2 [F^-1]_jj) in fp64 (Section 4.1) and a
  * global keep-mask over all blocks: keep_mask[j] = 1 for the `keep` largest
  * rho, ties broken by the lower index; 0 <= keep <= d. scores_out may be
  * NULL. theta 4-byte aligned. Uses workspace scratch; output is exact given
- * the fp64 diagonal. */
+ * the fp64 diagonal. In the fast mode (MFAC_STATIC_FP32) the scores come from
+ * the fp32-path diagonal; the keep-th largest score t is selected, every
+ * coordinate with a nonzero score within [t(1 - 1e-5), t(1 + 1e-5)] has
+ * [F^-1]_jj recomputed in fp64 (x = A_b^-1 g_j by iterative refinement: the
+ * residual g_j - A_b x formed from G in fp64, the kept fp32 L^-1 as
+ * preconditioner, until the estimated remaining error is below 1e-13 of x;
+ * then (1 - g_j.x) /
+ * lambda), stored into the diagonal, and the selection runs again. The mask
+ * then equals the fp64 mask: a coordinate outside the band is on the same side
+ * of the fp64 cut as long as the fp32 scores are within 1e-5 / (1 + 1e-5)
+ * relative of the fp64 ones. The refinement measures that error on the band
+ * (the coordinates at the cut); if any exceeds 2.5e-6 (a quarter of the band's
+ * half-width: the fp32 path is then too inaccurate for this G, e.g. blocks
+ * whose Fisher term dwarfs m*lambda), the mask is not certified and the next
+ * mfac_static_status returns MFAC_EPRECISION: use the default (fp64) mode. A
+ * refinement that does not settle within 12 steps latches MFAC_ENONFINITE. */
 mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t keep,
                           double* scores_out, uint8_t* keep_mask_out);
 

@@ -7,6 +7,7 @@ The library is libmfac.so (C ABI in include/mfac.h), built in place by
 from ._binding import (  # noqa: F401
     MFAC_EHIP,
     MFAC_EINVAL,
+    MFAC_EPRECISION,
     MFAC_ENONFINITE,
     MFAC_ESTATE,
     MFAC_EWORKSPACE,

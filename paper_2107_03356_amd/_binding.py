@@ -22,7 +22,9 @@ MFAC_EWORKSPACE = -2
 MFAC_EHIP = -3
 MFAC_ENONFINITE = -4
 MFAC_ESTATE = -5
+MFAC_EPRECISION = -6
 MFAC_STATIC_TRACE = 1
+MFAC_STATIC_FP32 = 2
 
 _c = ctypes
 _VP, _I32, _I64, _SZ, _F32, _F64 = _c.c_void_p, _c.c_int32, _c.c_int64, _c.c_size_t, _c.c_float, _c.c_double
@@ -51,6 +53,7 @@ SIGNATURES = {
     "mfac_window_status": (_c.c_int, [_VP]),
     "mfac_window_destroy": (_c.c_int, [_VP]),
     "mfac_static_workspace_bytes": (_SZ, [_I64, _I32, _I32]),
+    "mfac_static_workspace_bytes_flags": (_SZ, [_I64, _I32, _I32, _c.c_uint32]),
     "mfac_static_precompute": (_c.c_int, [_PVP, _I64, _I32, _I32, _F64, _VP, _VP, _SZ, _c.c_uint32, _VP]),
     "mfac_static_paged_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I64]),
     "mfac_static_precompute_paged": (_c.c_int, [_PVP, _I64, _I32, _I32, _F64, _VP, _I64, _VP, _SZ, _c.c_uint32,
@@ -272,14 +275,16 @@ class Window:
 class StaticBlocks:
     """Static block-wise precompute over a caller's m x d gradient matrix.
 
-    G is overwritten in place by W (W_b = R_b^-1 G_b per block). G is either a
+    G is overwritten in place by W (W_b = R_b^-1 G_b per block), except with
+    ``fp32=True`` (the fast mode: fp32 matrix cores, G left intact, W formed in
+    the workspace by the first query, the keep-mask still exact). G is either a
     device tensor, or (``page_cols`` given) a pinned host tensor
     (``pin_memory=True``) larger than the device should hold: it then passes
     through the device in pages of ``page_cols`` columns (whole blocks when
     block < d), and the queries read W from host memory.
     """
 
-    def __init__(self, G, block, lam, stream=None, trace=False, page_cols=None, device=None):
+    def __init__(self, G, block, lam, stream=None, trace=False, page_cols=None, device=None, fp32=False):
         import torch
         self.torch = torch
         assert G.dtype == torch.float32 and G.is_contiguous() and G.dim() == 2
@@ -287,13 +292,13 @@ class StaticBlocks:
         self.m, self.d = G.shape
         self.block, self.lam = int(block), float(lam)
         lib = load()
-        flags = MFAC_STATIC_TRACE if trace else 0
+        flags = (MFAC_STATIC_TRACE if trace else 0) | (MFAC_STATIC_FP32 if fp32 else 0)
         h = ctypes.c_void_p()
         if page_cols is None:
             self.device = G.device
-            wb = lib.mfac_static_workspace_bytes(self.d, self.block, self.m)
+            wb = lib.mfac_static_workspace_bytes_flags(self.d, self.block, self.m, flags)
             if wb == 0:
-                raise MfacError("mfac_static_workspace_bytes", MFAC_EINVAL)
+                raise MfacError("mfac_static_workspace_bytes_flags", MFAC_EINVAL)
             self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
             self.stream = _stream_handle(torch, self.device, stream)
             st = lib.mfac_static_precompute(ctypes.byref(h), self.d, self.block, self.m, self.lam, _ptr(G),

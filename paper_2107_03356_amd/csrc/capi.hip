@@ -108,6 +108,14 @@ struct mfac_static_s {
     int B, m, mp, nblocks, batch;
     double lambda;
     float* G;
+    // fast mode (MFAC_STATIC_FP32): fp32 MFMA Gram and W, the fp32 L^-1 of every
+    // block kept, G left intact, W formed on the first query into its own
+    // buffer; the keep-mask's band recomputed exactly in fp64
+    bool fast, w_ready;
+    float* W;  // where the queries read W: G (fp64 mode) or the W buffer (fast mode)
+    float* A32;  // fast mode: the batch of fp32 Gram matrices, factored in place
+    float* L32;  // fast mode: fp32 L^-1 of every block (the factor writes it here)
+    unsigned int *band_count, *band_list;
     hipStream_t st;
     int* err;
     double *A, *Linv, *gpart, *diag, *scores, *qpart;
@@ -270,6 +278,7 @@ MFAC_API const char* mfac_status_string(mfac_status s) {
         case MFAC_EHIP: return "HIP runtime or launch failure";
         case MFAC_ENONFINITE: return "non-finite value or non-positive pivot on device";
         case MFAC_ESTATE: return "call not valid in the current state";
+        case MFAC_EPRECISION: return "fast static mode could not certify the keep-mask; use the fp64 mode";
         default: break;
     }
     return "unknown status";
@@ -645,6 +654,21 @@ bool static_sizes_ok(int64_t d, int32_t B, int32_t m) {
            d <= (int64_t(1) << 32) - 256;
 }
 
+// the fast mode's band refinement keeps 3m + 2048 doubles in LDS and reads a
+// whole block per band coordinate and step
+constexpr int FAST_MAX_M = 4096;
+constexpr int FAST_MAX_B = 65536;
+// relative half-width of the band re-decided in fp64 (the fp32 path's score
+// error must stay below tau / (1 + tau); measured near 1e-8 on the pruning
+// workload)
+constexpr double BAND_TAU = 1e-5;
+
+bool static_flags_ok(int64_t d, int32_t B, int32_t m, uint32_t flags) {
+    if (flags & ~(MFAC_STATIC_TRACE | MFAC_STATIC_FP32)) return false;
+    if ((flags & MFAC_STATIC_FP32) && (m > FAST_MAX_M || B > FAST_MAX_B)) return false;
+    return static_sizes_ok(d, B, m);
+}
+
 int static_batch(int64_t d, int B, int m) {
     const int mp = padded_m(m);
     const int64_t nblocks = d / B;
@@ -674,7 +698,7 @@ int64_t static_gram_part(int64_t nblocks, int batch, int mp, int B) {
 }
 
 template <typename S>
-size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
+size_t static_layout(int64_t d, int B, int m, bool fast, char* base, S* s) {
     const int mp = padded_m(m);
     const int batch = static_batch(d, B, m);
     Carve c{base};
@@ -682,13 +706,29 @@ size_t static_layout(int64_t d, int B, int m, char* base, S* s) {
     double* diag = c.take<double>((size_t)d);
     double* scores = c.take<double>((size_t)d);
     char* sel = c.take<char>((size_t)select_scratch_bytes(d));
-    double* A = c.take<double>((size_t)batch * mp * mp);
-    double* Linv = c.take<double>((size_t)batch * mp * mp);
+    // fp64 mode: a batch of fp64 A and L^-1; fast mode: a batch of fp32 A, and
+    // the fp32 L^-1 of every block, W and the band list
+    double* A = fast ? nullptr : c.take<double>((size_t)batch * mp * mp);
+    double* Linv = fast ? nullptr : c.take<double>((size_t)batch * mp * mp);
     double* gpart = c.take<double>((size_t)static_gram_part(d / B, batch, mp, B));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
     double* qcoef = c.take<double>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
+    float *A32 = nullptr, *L32 = nullptr, *W = nullptr;
+    unsigned int *bcount = nullptr, *blist = nullptr;
+    if (fast) {
+        A32 = c.take<float>((size_t)batch * mp * mp);
+        L32 = c.take<float>((size_t)(d / B) * mp * mp);
+        W = c.take<float>((size_t)m * d);
+        bcount = c.take<unsigned int>(64);
+        blist = c.take<unsigned int>((size_t)d);
+    }
     if (s) {
+        s->A32 = A32;
+        s->L32 = L32;
+        s->W = W;
+        s->band_count = bcount;
+        s->band_list = blist;
         s->qpart = qpart;
         s->qcoef = qcoef;
         s->xobs = xobs;
@@ -725,7 +765,12 @@ void static_release(mfac_static_s* s) {
 
 MFAC_API size_t mfac_static_workspace_bytes(int64_t d, int32_t block, int32_t m) {
     if (!static_sizes_ok(d, block, m)) return 0;
-    return static_layout<mfac_static_s>(d, block, m, nullptr, nullptr);
+    return static_layout<mfac_static_s>(d, block, m, false, nullptr, nullptr);
+}
+
+MFAC_API size_t mfac_static_workspace_bytes_flags(int64_t d, int32_t block, int32_t m, uint32_t flags) {
+    if (!static_flags_ok(d, block, m, flags)) return 0;
+    return static_layout<mfac_static_s>(d, block, m, (flags & MFAC_STATIC_FP32) != 0, nullptr, nullptr);
 }
 
 MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, int32_t m, double lambda,
@@ -733,11 +778,11 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
                                             hipStream_t stream) {
     if (!out) return MFAC_EINVAL;
     *out = nullptr;
-    if (!static_sizes_ok(d, block, m)) return MFAC_EINVAL;
-    if (flags & ~MFAC_STATIC_TRACE) return MFAC_EINVAL;
+    if (!static_flags_ok(d, block, m, flags)) return MFAC_EINVAL;
     if (!(lambda > 0.0) || !isfinite(lambda)) return MFAC_EINVAL;
     if (!G || !workspace || !aligned16(G) || ((uintptr_t)workspace & 255u)) return MFAC_EINVAL;
-    if (workspace_bytes < mfac_static_workspace_bytes(d, block, m)) return MFAC_EWORKSPACE;
+    if (workspace_bytes < mfac_static_workspace_bytes_flags(d, block, m, flags)) return MFAC_EWORKSPACE;
+    const bool fast = (flags & MFAC_STATIC_FP32) != 0;
 
     mfac_static s = (mfac_static)calloc(1, sizeof(mfac_static_s));
     if (!s) return MFAC_EINVAL;
@@ -751,7 +796,9 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
     s->st = stream;
     s->trace = (flags & MFAC_STATIC_TRACE) != 0;
     if (s->trace) s->marks = new std::vector<mfac_window_s::Mark>();
-    static_layout<mfac_static_s>(d, block, m, (char*)workspace, s);
+    static_layout<mfac_static_s>(d, block, m, fast, (char*)workspace, s);
+    s->fast = fast;
+    if (!fast) s->W = G;  // W is written over G
 
     const int64_t bstride = (int64_t)s->mp * s->mp;
     const double mu = (double)m * lambda;
@@ -763,14 +810,23 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
     if (launch_fill_zero((float*)s->err, 1, s->st) != hipSuccess) return fail();
     for (int b0 = 0; b0 < s->nblocks; b0 += s->batch) {
         const int nb = (s->nblocks - b0) < s->batch ? (s->nblocks - b0) : s->batch;
+        // fast mode: fp32 Gram, fp32 factor whose L^-1 goes to the kept
+        // per-block store, and the diagonal from the fp32 W (not stored)
+        float* L32b = fast ? s->L32 + (int64_t)b0 * bstride : nullptr;
         if (mark_begin(s) != hipSuccess) return fail();
-        if (launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->gpart, s->st) != hipSuccess) return fail();
+        const hipError_t eg = fast ? launch_gram_blocks32(G, m, d, block, b0, nb, mu, s->A32, s->mp, s->gpart, s->st)
+                                   : launch_gram_blocks(G, m, d, block, b0, nb, mu, s->A, s->mp, s->gpart, s->st);
+        if (eg != hipSuccess) return fail();
         if (mark_end(s, 0) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
-        if (launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st) != hipSuccess) return fail();
+        const hipError_t ef = fast ? launch_factor_invert32(s->A32, L32b, s->mp, nb, bstride, s->err, s->st)
+                                   : launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st);
+        if (ef != hipSuccess) return fail();
         if (mark_end(s, 1) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
-        if (launch_trmm_diag(s->Linv, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, s->st) !=
-            hipSuccess)
-            return fail();
+        const hipError_t et =
+            fast ? launch_trmm32(nullptr, L32b, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, nullptr,
+                                 nullptr, 0, s->st)
+                 : launch_trmm_diag(s->Linv, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, s->st);
+        if (et != hipSuccess) return fail();
         if (mark_end(s, 2) != hipSuccess) return fail();
     }
     *out = s;
@@ -801,31 +857,54 @@ MFAC_API mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t ke
     double* sc = scores_out ? scores_out : s->scores;
     HIPCHK(mark_begin(s));
     HIPCHK(launch_scores(theta, s->diag, s->d, sc, s->err, s->st));
+    if (s->fast)
+        HIPCHK(launch_band_refine(sc, s->d, keep, s->sel, BAND_TAU, s->band_count, s->band_list, s->G, s->m, s->B,
+                                  s->L32, s->mp, (int64_t)s->mp * s->mp, s->lambda, theta, s->diag, sc, s->err,
+                                  s->st));
     HIPCHK(launch_topk_mask(sc, s->d, keep, s->sel, keep_mask_out, s->st));
     HIPCHK(mark_end(s, 3));
     return MFAC_OK;
 }
 
+namespace {
+// Fast mode: W = L^-1 G for every block into the W buffer, once, from the kept
+// fp32 L^-1 (G stays intact for later keep-masks).
+mfac_status ensure_w(mfac_static s) {
+    if (!s->fast || s->w_ready) return MFAC_OK;
+    const int64_t bstride = (int64_t)s->mp * s->mp;
+    HIPCHK(launch_trmm32(nullptr, s->L32, s->mp, bstride, s->G, s->m, s->d, s->B, 0, s->nblocks, s->lambda, nullptr,
+                         s->W, nullptr, 0, s->st));
+    s->w_ready = true;
+    return MFAC_OK;
+}
+}  // namespace
+
 MFAC_API mfac_status mfac_static_ihvp(mfac_static s, int32_t n, const float* X, float* Y) {
     if (!s || !X || !Y || n < 1 || n > 4 || !aligned16(X) || !aligned16(Y)) return MFAC_EINVAL;
     const double inv_lam = 1.0 / s->lambda;
-    HIPCHK(launch_static_ihvp(s->G, s->m, s->d, s->B, n, X, (float)inv_lam, inv_lam, Y, s->qpart, s->qcoef, s->st));
+    const mfac_status rc = ensure_w(s);
+    if (rc != MFAC_OK) return rc;
+    HIPCHK(launch_static_ihvp(s->W, s->m, s->d, s->B, n, X, (float)inv_lam, inv_lam, Y, s->qpart, s->qcoef, s->st));
     return MFAC_OK;
 }
 
 MFAC_API mfac_status mfac_static_element(mfac_static s, int64_t nq, const int64_t* ij, double* out) {
     if (!s || nq < 0 || (nq > 0 && (!ij || !out)) || ((uintptr_t)ij & 7u) || ((uintptr_t)out & 7u))
         return MFAC_EINVAL;
-    HIPCHK(launch_static_element(s->G, s->m, s->d, s->B, nq, ij, s->lambda, out, s->err, s->st));
+    const mfac_status rc = ensure_w(s);
+    if (rc != MFAC_OK) return rc;
+    HIPCHK(launch_static_element(s->W, s->m, s->d, s->B, nq, ij, s->lambda, out, s->err, s->st));
     return MFAC_OK;
 }
 
 MFAC_API mfac_status mfac_obs_update(mfac_static s, const float* theta, const uint8_t* keep_mask, float* delta_out) {
     if (!s || !theta || !keep_mask || !delta_out || !aligned4(theta) || !aligned16(delta_out)) return MFAC_EINVAL;
     const double inv_lam = 1.0 / s->lambda;
+    const mfac_status rc = ensure_w(s);
+    if (rc != MFAC_OK) return rc;
     HIPCHK(launch_obs_x(theta, keep_mask, s->diag, s->d, s->xobs, s->st));
     // delta = -F^-1 x = -x / lambda + W^T (W x) / lambda
-    HIPCHK(launch_static_ihvp(s->G, s->m, s->d, s->B, 1, s->xobs, (float)-inv_lam, -inv_lam, delta_out, s->qpart,
+    HIPCHK(launch_static_ihvp(s->W, s->m, s->d, s->B, 1, s->xobs, (float)-inv_lam, -inv_lam, delta_out, s->qpart,
                               s->qcoef, s->st));
     return MFAC_OK;
 }
@@ -844,7 +923,8 @@ MFAC_API mfac_status mfac_static_status(mfac_static s) {
     if (e != 0) {
         HIPCHK(launch_fill_zero((float*)s->err, 1, s->st));
         HIPCHK(hipStreamSynchronize(s->st));
-        return MFAC_ENONFINITE;
+        // bit 64: the band refinement measured an fp32 error too large for its band
+        return e == 64 ? MFAC_EPRECISION : MFAC_ENONFINITE;
     }
     return MFAC_OK;
 }
@@ -1065,6 +1145,7 @@ MFAC_API mfac_status mfac_static_precompute_paged(mfac_static* out, int64_t d, i
     s->nblocks = (int)(d / block);
     s->lambda = lambda;
     s->G = (float*)at.devicePointer;
+    s->W = s->G;
     s->Ghost = G_host;
     s->paged = true;
     s->st = stream;

@@ -104,36 +104,40 @@ __global__ __launch_bounds__(256) void k_assemble(double* __restrict__ K, int m,
 }
 
 // ------------------------------------------------------------------ potrf
-// One 64-thread wave per batch item: factor diagonal tile t in place (lower)
+__device__ __forceinline__ double rsqrt_of(double x) { return rsqrt(x); }
+__device__ __forceinline__ float rsqrt_of(float x) { return rsqrtf(x); }
+
+// One 64-thread wave per batch item (fp64, or fp32 for the fast static mode): factor diagonal tile t in place (lower)
 // and write its inverse into the diagonal tile of Linv. Lane i keeps row i of
 // the tile in registers; each column step broadcasts the new column through a
 // double-buffered LDS vector (reads of step j and writes of step j+2 are
 // separated by the barriers of step j+1), so the trailing update is a run of
 // independent FMAs on registers.
-__global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, double* __restrict__ Linv,
-                                                   int mp, int64_t bstride, int t, int* __restrict__ err) {
-    __shared__ double col[2][64];
-    __shared__ double T[64][65];
-    __shared__ double rdiag[64];  // 1 / L[j][j]
-    double* Ab = A + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
-    double* Lb = Linv + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
+template <typename R>
+__global__ __launch_bounds__(64) void k_potrf_diag(R* __restrict__ A, R* __restrict__ Linv, int mp, int64_t bstride,
+                                                   int t, int* __restrict__ err) {
+    __shared__ R col[2][64];
+    __shared__ R T[64][65];
+    __shared__ R rdiag[64];  // 1 / L[j][j]
+    R* Ab = A + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
+    R* Lb = Linv + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
     const int i = threadIdx.x;
-    double a[64];
+    R a[64];
 #pragma unroll
     for (int c = 0; c < 64; ++c) a[c] = Ab[(int64_t)i * mp + c];
     int bad = 0;
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
-        double* cb = col[j & 1];
+        R* cb = col[j & 1];
         // the pivot lane publishes 1 / L[j][j] = rsqrt(pivot); the column below
         // it scales by that reciprocal (no division on the per-column chain)
         if (i == j) {
-            double piv = a[j];
-            if (!(piv > 0.0) || !isfinite(piv)) {
+            R piv = a[j];
+            if (!(piv > R(0)) || !isfinite(piv)) {
                 bad = 1;
-                piv = 1.0;
+                piv = R(1);
             }
-            const double r = rsqrt(piv);
+            const R r = rsqrt_of(piv);
             a[j] = piv * r;
             cb[j] = r;
             rdiag[j] = r;
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
         }
         __syncthreads();
         if (i > j) {
-            const double lij = a[j];
+            const R lij = a[j];
 #pragma unroll
             for (int c = j + 1; c < 64; ++c) a[c] -= lij * cb[c];
         }
@@ -154,7 +158,7 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
     // the factor (lower part of the registers) into LDS and back to A
 #pragma unroll
     for (int c = 0; c < 64; ++c) {
-        const double v = (c <= i) ? a[c] : 0.0;
+        const R v = (c <= i) ? a[c] : R(0);
         T[i][c] = v;
         Ab[(int64_t)i * mp + c] = v;
     }
@@ -166,10 +170,10 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
     // address across the wave (LDS broadcast); the dot products use four
     // partial sums so consecutive FMAs do not wait on each other.
     {
-        double x[64];
+        R x[64];
 #pragma unroll
         for (int r = 0; r < 64; ++r) {
-            double s0 = (r == i) ? 1.0 : 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+            R s0 = (r == i) ? R(1) : R(0), s1 = 0, s2 = 0, s3 = 0;
 #pragma unroll
             for (int l = 0; l + 3 < r; l += 4) {
                 s0 -= T[r][l] * x[l];
@@ -191,11 +195,12 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double* __restrict__ A, doubl
     for (int c = 0; c < 64; ++c) Lb[(int64_t)i * mp + c] = T[i][c];
 }
 
-__global__ __launch_bounds__(256) void k_zero_superdiag(double* __restrict__ Linv, int mp, int64_t bstride) {
+template <typename R>
+__global__ __launch_bounds__(256) void k_zero_superdiag(R* __restrict__ Linv, int mp, int64_t bstride) {
     // zero the first superdiagonal of 64 x 64 tiles, (t, t+1); grid (T-1, nbatch)
     const int t = blockIdx.x;
-    double* C = Linv + (int64_t)blockIdx.y * bstride + (int64_t)t * 64 * mp + (t + 1) * 64;
-    for (int e = threadIdx.x; e < 4096; e += 256) C[(int64_t)(e >> 6) * mp + (e & 63)] = 0.0;
+    R* C = Linv + (int64_t)blockIdx.y * bstride + (int64_t)t * 64 * mp + (t + 1) * 64;
+    for (int e = threadIdx.x; e < 4096; e += 256) C[(int64_t)(e >> 6) * mp + (e & 63)] = R(0);
 }
 
 // ------------------------------------------------------------------ explicit inverse
@@ -338,18 +343,23 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
     return hipGetLastError();
 }
 
-hipError_t launch_potrf_tile(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int t, int* err,
-                             hipStream_t st) {
-    hipLaunchKernelGGL(k_potrf_diag, dim3(nbatch), dim3(64), 0, st, A, Linv, mp, bstride, t, err);
+template <typename R>
+hipError_t launch_potrf_tile(R* A, R* Linv, int mp, int nbatch, int64_t bstride, int t, int* err, hipStream_t st) {
+    hipLaunchKernelGGL(k_potrf_diag<R>, dim3(nbatch), dim3(64), 0, st, A, Linv, mp, bstride, t, err);
     return hipGetLastError();
 }
+template hipError_t launch_potrf_tile<double>(double*, double*, int, int, int64_t, int, int*, hipStream_t);
+template hipError_t launch_potrf_tile<float>(float*, float*, int, int, int64_t, int, int*, hipStream_t);
 
-hipError_t launch_zero_superdiag(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st) {
+template <typename R>
+hipError_t launch_zero_superdiag(R* M, int mp, int nbatch, int64_t bstride, hipStream_t st) {
     const int T = mp / 64;
     if (T < 2) return hipSuccess;
-    hipLaunchKernelGGL(k_zero_superdiag, dim3(T - 1, nbatch), dim3(256), 0, st, M, mp, bstride);
+    hipLaunchKernelGGL(k_zero_superdiag<R>, dim3(T - 1, nbatch), dim3(256), 0, st, M, mp, bstride);
     return hipGetLastError();
 }
+template hipError_t launch_zero_superdiag<double>(double*, int, int, int64_t, hipStream_t);
+template hipError_t launch_zero_superdiag<float>(float*, int, int, int64_t, hipStream_t);
 
 hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, int64_t bstride, hipStream_t st) {
     const int T = mp / 64;

@@ -20,15 +20,43 @@
 namespace mfac {
 
 // defined in chol.hip
-hipError_t launch_potrf_tile(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int t, int* err,
-                             hipStream_t st);
-hipError_t launch_zero_superdiag(double* M, int mp, int nbatch, int64_t bstride, hipStream_t st);
+template <typename T>
+hipError_t launch_potrf_tile(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int t, int* err, hipStream_t st);
+template <typename T>
+hipError_t launch_zero_superdiag(T* M, int mp, int nbatch, int64_t bstride, hipStream_t st);
 
 namespace {
 
 constexpr int BM = 128, BN = 128, BK = 16;
-constexpr int PA = BK + 2;   // pitch of [row][k] chunks (doubles)
-constexpr int PBN = BN + 16; // pitch of a [k][n] chunk (doubles): rows k, k+1 on disjoint LDS banks
+
+// Per element type: the MFMA (16x16x4: fp64, or fp32 on twice the rate), its
+// accumulator, the row of an accumulator register, and the LDS pitches:
+// [row][k] chunks (the 16-row x 4-k read of one MFMA operand on distinct
+// banks) and [k][n] chunks (rows k .. k+3 on disjoint banks).
+template <typename T>
+struct Mf;
+template <>
+struct Mf<double> {
+    typedef v4d acc;
+    typedef double2 pair;
+    static constexpr int PA = BK + 2;
+    static constexpr int PBN = BN + 16;
+    static __device__ __forceinline__ acc mfma(double a, double b, acc c) {
+        return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int row(int lane, int r) { return mfma64_row(lane, r); }
+};
+template <>
+struct Mf<float> {
+    typedef v4f acc;
+    typedef float2 pair;
+    static constexpr int PA = BK + 4;
+    static constexpr int PBN = BN + 16;
+    static __device__ __forceinline__ acc mfma(float a, float b, acc c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int row(int lane, int r) { return mfma32_row(lane, r); }
+};
 
 enum : int {
     KHI_ROW = 1,   // A lower triangular: k < (I+1)*BM for output row tile I
@@ -37,10 +65,11 @@ enum : int {
     LOWER_ONLY = 8 // only output tiles with I >= J
 };
 
+template <typename T>
 struct GemmArgs {
-    const double* A;
-    const double* B;
-    double* C;
+    const T* A;
+    const T* B;
+    T* C;
     int ld;
     int64_t bstride;
     int a0r, a0c;  // stored A origin (row, col)
@@ -62,7 +91,8 @@ enum : int {
 };
 
 // Output tiles of one task (I1 < 0: a single tile).
-__device__ __forceinline__ void task_tiles(const GemmArgs& g, int t, int& I0, int& J0, int& I1, int& J1) {
+template <typename T>
+__device__ __forceinline__ void task_tiles(const GemmArgs<T>& g, int t, int& I0, int& J0, int& I1, int& J1) {
     I1 = J1 = -1;
     if (g.mode == TASK_LOWER) {
         int i = (int)((sqrtf(8.0f * (float)t + 1.0f) - 1.0f) * 0.5f);
@@ -100,18 +130,21 @@ __device__ __forceinline__ void task_tiles(const GemmArgs& g, int t, int& I0, in
 // two work-groups per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
 // of 64) load clamped, in-bounds data and are never stored. The elements C
 // writes are disjoint from the ones A and B read (they may share a buffer).
-template <bool TA, bool TB>
-__global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
+template <typename T, bool TA, bool TB>
+__global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
+    using M = Mf<T>;
+    using T2 = typename M::pair;
+    constexpr int PA = M::PA, PBN = M::PBN;
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
-    __shared__ double As[2][TA ? BK : BM][TA ? PBN : PA];
-    __shared__ double Bs[2][TB ? BN : BK][TB ? PA : PBN];
+    __shared__ T As[2][TA ? BK : BM][TA ? PBN : PA];
+    __shared__ T Bs[2][TB ? BN : BK][TB ? PA : PBN];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     const int bt = lid / g.ntask;
     int I0, J0, I1, J1;
     task_tiles(g, lid - bt * g.ntask, I0, J0, I1, J1);
-    const double* __restrict__ A = g.A + (int64_t)bt * g.bstride;
-    const double* __restrict__ B = g.B + (int64_t)bt * g.bstride;
-    double* __restrict__ C = g.C + (int64_t)bt * g.bstride;
+    const T* __restrict__ A = g.A + (int64_t)bt * g.bstride;
+    const T* __restrict__ B = g.B + (int64_t)bt * g.bstride;
+    T* __restrict__ C = g.C + (int64_t)bt * g.bstride;
     const int ld = g.ld;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
@@ -133,28 +166,28 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
         // inside the operand)
         const int am = min(mrow0 + (TA ? tn : sr), g.M - (TA ? 2 : 1));
         const int bn = min(ncol0 + (TB ? sr : tn), g.N - (TB ? 1 : 2));
-        const double* __restrict__ ap =
+        const T* __restrict__ ap =
             TA ? A + (int64_t)g.a0r * ld + g.a0c + am : A + (int64_t)(g.a0r + am) * ld + g.a0c + sk;
-        const double* __restrict__ bp =
+        const T* __restrict__ bp =
             TB ? B + (int64_t)(g.b0r + bn) * ld + g.b0c + sk : B + (int64_t)g.b0r * ld + g.b0c + bn;
-        double2 pa0, pa1, pb0, pb1;
+        T2 pa0, pa1, pb0, pb1;
         auto load_chunk = [&](int k0) {
             if constexpr (TA) {
-                pa0 = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk) * ld);
-                pa1 = *reinterpret_cast<const double2*>(ap + (int64_t)(k0 + tk + 8) * ld);
+                pa0 = *reinterpret_cast<const T2*>(ap + (int64_t)(k0 + tk) * ld);
+                pa1 = *reinterpret_cast<const T2*>(ap + (int64_t)(k0 + tk + 8) * ld);
             } else {
-                pa0 = *reinterpret_cast<const double2*>(ap + k0);
-                pa1 = *reinterpret_cast<const double2*>(ap + k0 + 2);
+                pa0 = *reinterpret_cast<const T2*>(ap + k0);
+                pa1 = *reinterpret_cast<const T2*>(ap + k0 + 2);
             }
             if constexpr (TB) {
-                pb0 = *reinterpret_cast<const double2*>(bp + k0);
-                pb1 = *reinterpret_cast<const double2*>(bp + k0 + 2);
+                pb0 = *reinterpret_cast<const T2*>(bp + k0);
+                pb1 = *reinterpret_cast<const T2*>(bp + k0 + 2);
             } else {
-                pb0 = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk) * ld);
-                pb1 = *reinterpret_cast<const double2*>(bp + (int64_t)(k0 + tk + 8) * ld);
+                pb0 = *reinterpret_cast<const T2*>(bp + (int64_t)(k0 + tk) * ld);
+                pb1 = *reinterpret_cast<const T2*>(bp + (int64_t)(k0 + tk + 8) * ld);
             }
         };
-        auto put = [](double* dst, double2 v) {
+        auto put = [](T* dst, T2 v) {
             dst[0] = v.x;
             dst[1] = v.y;
         };
@@ -175,9 +208,9 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
             }
         };
 
-        // C tile coordinates of accumulator (x, y, r): fp64 MFMA result register r
-        // of lane l is row (l/16) + 4r, column l%16
-        auto crow = [&](int x, int r) { return mrow0 + wr * 32 + x * 16 + kl + 4 * r; };
+        // C tile coordinates of accumulator (x, y, r): the MFMA result's row
+        // of register r of this lane, column lane % 16
+        auto crow = [&](int x, int r) { return mrow0 + wr * 32 + x * 16 + M::row(lane, r); };
         auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
         const int nchunk = (khi - klo) / BK;
         // This wave's own K range: a triangular operand is zero outside it, so
@@ -194,15 +227,15 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
         if (nchunk > 0) load_chunk(klo);
         // beta C enters as the accumulator's start value (scaled by 1/alpha), so
         // its loads issue together with the first chunk's
-        v4d acc[2][4];
-        const double cs = g.beta / g.alpha;
+        typename M::acc acc[2][4];
+        const T cs = (T)(g.beta / g.alpha);
     #pragma unroll
         for (int x = 0; x < 2; ++x)
     #pragma unroll
             for (int y = 0; y < 4; ++y)
     #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    double v = 0.0;
+                    T v = 0;
                     if (g.beta != 0.0 && !idle) {
                         const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
                         v = cs * C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
@@ -220,7 +253,7 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
             if (!idle && k0 + BK > wklo && k0 < wkhi) {
     #pragma unroll
             for (int kk = 0; kk < BK / 4; ++kk) {
-                double av[2], bv[4];
+                T av[2], bv[4];
     #pragma unroll
                 for (int x = 0; x < 2; ++x)
                     av[x] = TA ? As[buf][kk * 4 + kl][wr * 32 + x * 16 + rl] : As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
@@ -231,7 +264,7 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
                 for (int x = 0; x < 2; ++x)
     #pragma unroll
                     for (int y = 0; y < 4; ++y)
-                        acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
+                        acc[x][y] = M::mfma(av[x], bv[y], acc[x][y]);
             }
             }
             if (c + 1 < nchunk) store_chunk(buf ^ 1);
@@ -245,7 +278,7 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
     #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int row = crow(x, r), col = ccol(y);
-                    if (row < g.M && col < g.N) C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col] = g.alpha * acc[x][y][r];
+                    if (row < g.M && col < g.N) C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col] = (T)g.alpha * acc[x][y][r];
                 }
     };
     tile(I0, J0);
@@ -255,10 +288,11 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs g) {
     }
 }
 
-hipError_t gemm(bool ta, bool tb, const double* A, int a0r, int a0c, const double* B, int b0r, int b0c, double* C,
-                int cm0, int cn0, int M, int N, int K, double alpha, double beta, int flags, int mp, int nbatch,
-                int64_t bstride, hipStream_t st) {
-    GemmArgs g;
+template <typename T>
+hipError_t gemm(bool ta, bool tb, const T* A, int a0r, int a0c, const T* B, int b0r, int b0c, T* C, int cm0, int cn0,
+                int M, int N, int K, double alpha, double beta, int flags, int mp, int nbatch, int64_t bstride,
+                hipStream_t st) {
+    GemmArgs<T> g;
     g.A = A;
     g.B = B;
     g.C = C;
@@ -292,17 +326,17 @@ hipError_t gemm(bool ta, bool tb, const double* A, int a0r, int a0c, const doubl
         g.ntask = g.tiles_m * g.tiles_n;
     }
     const int64_t grid = (int64_t)g.ntask * nbatch;
-    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<false, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
-    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<false, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
-    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<true, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
-    if (ta && tb) hipLaunchKernelGGL((k_bgemm<true, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<T, false, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<T, false, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<T, true, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (ta && tb) hipLaunchKernelGGL((k_bgemm<T, true, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
     return hipGetLastError();
 }
 
 // Factor and invert the diagonal block [o, o+n) of every batch item (n a
 // multiple of 64). U = L21^T (h x n2) is kept in the upper block A12.
-hipError_t factor_node(double* A, double* Linv, int o, int n, int mp, int nbatch, int64_t bstride, int* err,
-                       hipStream_t st) {
+template <typename T>
+hipError_t factor_node(T* A, T* Linv, int o, int n, int mp, int nbatch, int64_t bstride, int* err, hipStream_t st) {
     if (n == 64) return launch_potrf_tile(A, Linv, mp, nbatch, bstride, o / 64, err, st);
     const int h = (n / 128) * 64;  // split at a multiple of 64; n2 >= h
     const int n2 = n - h;
@@ -327,8 +361,8 @@ hipError_t factor_node(double* A, double* Linv, int o, int n, int mp, int nbatch
 
 }  // namespace
 
-hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
-                                hipStream_t st) {
+template <typename T>
+hipError_t factor_invert(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int* err, hipStream_t st) {
     // The trimmed K ranges read Linv only in the lower triangle and in the
     // first superdiagonal of 64 x 64 tiles (upper halves of 128-wide diagonal
     // blocks at 64-aligned origins); the leaves write zeros above their own
@@ -336,6 +370,16 @@ hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int
     hipError_t e = launch_zero_superdiag(Linv, mp, nbatch, bstride, st);
     if (e != hipSuccess) return e;
     return factor_node(A, Linv, 0, mp, mp, nbatch, bstride, err, st);
+}
+
+hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                                hipStream_t st) {
+    return factor_invert<double>(A, Linv, mp, nbatch, bstride, err, st);
+}
+
+hipError_t launch_factor_invert32(float* A, float* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                                  hipStream_t st) {
+    return factor_invert<float>(A, Linv, mp, nbatch, bstride, err, st);
 }
 
 }  // namespace mfac

@@ -303,15 +303,16 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
 // column splits of the partial tiles, in split order, plus mu on the diagonal
 // (identity on the padding rows); with accum, the sum is added to A_b instead.
 // Grid (ntiles, nb).
+template <typename OT>
 __global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __restrict__ part, int nsplit, int ntiles,
-                                                            int m, double mu, int accum, double* __restrict__ A,
+                                                            int m, double mu, int accum, OT* __restrict__ A,
                                                             int mp) {
     const int tile = blockIdx.x, bl = blockIdx.y;
     int ti, tj;
     tile_of(tile, ti, tj);
     const double* src = part + (int64_t)bl * nsplit * ntiles * (GT * GT) + (int64_t)tile * (GT * GT);
     const int64_t sstride = (int64_t)ntiles * (GT * GT);
-    double* Ab = A + (int64_t)bl * mp * mp;
+    OT* Ab = A + (int64_t)bl * mp * mp;
     for (int e = threadIdx.x; e < GT * GT; e += 256) {
         const int rr = e / GT, cc = e % GT;
         const int row = ti * GT + rr, col = tj * GT + cc;
@@ -319,11 +320,147 @@ __global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __rest
         double v = 0.0;
         for (int s = 0; s < nsplit; ++s) v += src[s * sstride + e];
         if (accum)
-            v += Ab[(int64_t)row * mp + col];
+            v += (double)Ab[(int64_t)row * mp + col];
         else if (row == col)
             v += (row < m) ? mu : 1.0;
-        Ab[(int64_t)row * mp + col] = v;
+        Ab[(int64_t)row * mp + col] = (OT)v;
     }
+}
+
+// Static blocks on fp32 MFMA (v_mfma_f32_16x16x4f32): the tiling, staging and
+// task layout of k_gram_blocks, with the fp32 operands fed to the matrix
+// cores as they are. Products of 512 columns accumulate in fp32 registers and
+// are then added to fp64 accumulators, so the rounding of a long block stays
+// that of 512-term sums; the tile goes to A (fp64) as in k_gram_blocks.
+constexpr int FLUSH_CHUNKS = 512 / KB;
+
+__global__ __launch_bounds__(512, 2) void k_gram_blocks32(const float* __restrict__ G, int m, int64_t d, int B,
+                                                          int b0, int ntiles, int nsplit, int kcols, double mu,
+                                                          float* __restrict__ A, int mp,
+                                                          double* __restrict__ part) {
+    __shared__ float As[2][GT][PITCH];
+    __shared__ float Bs[2][GT][PITCH];
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int per_block = ntiles * nsplit;
+    const int bl = lid / per_block;
+    const int rem = lid - bl * per_block;
+    const int sp = rem / ntiles;
+    const int tile = rem - sp * ntiles;
+    int ti, tj;
+    tile_of(tile, ti, tj);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
+    const int rl = lane & 15, kl = lane >> 4;
+    const bool diag_tile = ti == tj;
+    const bool upper_wave = diag_tile && wr * 32 + 31 < wc * 64;
+    const int cbeg = sp * kcols;
+    const int ncols = (B - cbeg) < kcols ? (B - cbeg) : kcols;
+    const float* base = G + (int64_t)(b0 + bl) * B + cbeg;
+    const int ra0 = ti * GT, rb0 = tj * GT;
+    const int sr = tid >> 2, sc = (tid & 3) * 8;
+    const bool oka = ra0 + sr < m, okb = rb0 + sr < m;
+    const float* rowa = base + (int64_t)(ra0 + sr) * d;
+    const float* rowb = base + (int64_t)(rb0 + sr) * d;
+    float4 pa0, pa1, pb0, pb1;
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#define MFAC_GB_LOAD(K0_)                                                                              \
+    {                                                                                                  \
+        const int c_ = (K0_) + sc;                                                                     \
+        pa0 = (oka && c_ < ncols) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;                \
+        pa1 = (oka && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;        \
+        if (!diag_tile) {                                                                              \
+            pb0 = (okb && c_ < ncols) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;            \
+            pb1 = (okb && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero;    \
+        }                                                                                              \
+    }
+#define MFAC_GB_STORE(BUF_)                                                                            \
+    {                                                                                                  \
+        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                                     \
+        a_[0] = pa0;                                                                                   \
+        a_[1] = pa1;                                                                                   \
+        if (!diag_tile) {                                                                              \
+            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                                 \
+            b_[0] = pb0;                                                                               \
+            b_[1] = pb1;                                                                               \
+        }                                                                                              \
+    }
+
+    v4f acc[2][4];
+    double accd[2][4][4];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) {
+            acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) accd[x][y][r] = 0.0;
+        }
+    const int nchunk = (ncols + KB - 1) / KB;
+    MFAC_GB_LOAD(0)
+    MFAC_GB_STORE(0)
+    __syncthreads();
+    for (int c = 0; c < nchunk; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < nchunk) MFAC_GB_LOAD((c + 1) * KB)
+        float (*Ab)[PITCH] = As[buf];
+        float (*Bb)[PITCH] = diag_tile ? As[buf] : Bs[buf];
+        if (!upper_wave) {
+#pragma unroll
+            for (int kk = 0; kk < KB / 4; ++kk) {
+                float av[2], bv[4];
+#pragma unroll
+                for (int x = 0; x < 2; ++x) av[x] = Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
+#pragma unroll
+                for (int y = 0; y < 4; ++y) bv[y] = Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < 4; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+            }
+            if ((c + 1) % FLUSH_CHUNKS == 0 || c + 1 == nchunk) {
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < 4; ++y) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) accd[x][y][r] += (double)acc[x][y][r];
+                        acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+                    }
+            }
+        }
+        if (c + 1 < nchunk) MFAC_GB_STORE(buf ^ 1)
+        __syncthreads();
+    }
+#undef MFAC_GB_LOAD
+#undef MFAC_GB_STORE
+    if (upper_wave) return;
+    if (nsplit > 1) {
+        double* out = part + ((int64_t)bl * nsplit + sp) * ntiles * (GT * GT) + (int64_t)tile * (GT * GT);
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    out[(wr * 32 + x * 16 + mfma32_row(lane, r)) * GT + wc * 64 + y * 16 + rl] = accd[x][y][r];
+        return;
+    }
+    float* Ab = A + (int64_t)bl * mp * mp;
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = ra0 + wr * 32 + x * 16 + mfma32_row(lane, r);
+                const int col = rb0 + wc * 64 + y * 16 + rl;
+                if (row < mp && col < mp) {
+                    double v = accd[x][y][r];
+                    if (row == col) v += (row < m) ? mu : 1.0;
+                    Ab[(int64_t)row * mp + col] = (float)v;
+                }
+            }
 }
 
 }  // namespace
@@ -389,6 +526,19 @@ int64_t gram_blocks_part_doubles(int nb, int mp, int B) {
     return ns > 1 ? (int64_t)nb * ns * ntiles * (GT * GT) : 0;
 }
 
+hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0, int nb, double mu, float* A,
+                                int mp, double* part, hipStream_t st) {
+    int ntiles, kcols;
+    const int ns = gram_blocks_splits(nb, mp, B, ntiles, kcols);
+    hipLaunchKernelGGL(k_gram_blocks32, dim3((unsigned)(ntiles * ns * nb)), dim3(512), 0, st, G, m, d, B, b0, ntiles,
+                       ns, kcols, mu, A, mp, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || ns == 1) return e;
+    hipLaunchKernelGGL(k_gram_blocks_reduce<float>, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part, ns,
+                       ntiles, m, mu, 0, A, mp);
+    return hipGetLastError();
+}
+
 hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb, double mu,
                               double* A, int mp, double* part, hipStream_t st, bool accumulate) {
     int ntiles, kcols;
@@ -398,8 +548,8 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
                        ns, kcols, mu, acc, A, mp, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || ns == 1) return e;
-    hipLaunchKernelGGL(k_gram_blocks_reduce, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part, ns,
-                       ntiles, m, mu, acc, A, mp);
+    hipLaunchKernelGGL(k_gram_blocks_reduce<double>, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part,
+                       ns, ntiles, m, mu, acc, A, mp);
     return hipGetLastError();
 }
 

@@ -83,6 +83,10 @@ int64_t gram_blocks_part_doubles(int nb, int mp, int B);
 hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb,
                               double mu, double* A, int mp, double* part, hipStream_t st,
                               bool accumulate = false);
+// The same on fp32 MFMA (fp32 operands, 512-column fp32 sums added in fp64,
+// split partials summed in fp64), stored as fp32 A; no accumulate mode.
+hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0, int nb, double mu, float* A,
+                                int mp, double* part, hipStream_t st);
 
 // ---------------------------------------------------------------- coefficients
 // A (mp x mp) = K (m x m) + mu I, identity padding; optionally first replaces
@@ -97,6 +101,9 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
 // pivot. Recursive blocked algorithm on batched fp64 MFMA GEMMs.
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
                                 hipStream_t st);
+// The same in fp32 (fp32 matrix cores and leaves), for the fast static mode.
+hipError_t launch_factor_invert32(float* A, float* Linv, int mp, int nbatch, int64_t bstride, int* err,
+                                  hipStream_t st);
 // Ainv = Linv^T Linv (the explicit inverse of A = L L^T), full mp x mp.
 hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, int64_t bstride, hipStream_t st);
 // O(m^2) slot replacement: K row/column k <- p and Ainv <- (A with column k
@@ -113,6 +120,14 @@ hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double*
 hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* G, int m,
                             int64_t d, int B, int b0, int nb, double lam, double* diag,
                             hipStream_t st);
+// W_b = Linv_b G_b on fp32 MFMA for blocks [b0, b0+nb): Linv from Linv64
+// (fp64, the factor's output) or Linv32 (fp32), batch stride lstride; G is
+// read only. diag (or nullptr): (1 - colsum(W^2)) / lam in fp64 from the fp32
+// W. Wout (or nullptr): W, row stride d. Lsave (or nullptr): the fp32 L^-1
+// elements the pass reads, per block at stride sstride.
+hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
+                         int64_t d, int B, int b0, int nb, double lam, double* diag, float* Wout, float* Lsave,
+                         int64_t sstride, hipStream_t st);
 hipError_t launch_diag_to_f32(const double* diag, int64_t d, float* out, hipStream_t st);
 hipError_t launch_scores(const float* theta, const double* diag, int64_t d, double* scores,
                          int* err, hipStream_t st);
@@ -125,6 +140,15 @@ struct SelectScratch {
 };
 int64_t select_scratch_bytes(int64_t d);
 SelectScratch select_scratch_carve(void* base, int64_t d);
+// The band step of the fast static mode: selects the keep-th largest score t,
+// lists the coordinates with |s - t| <= tau t (s != 0) and recomputes their
+// diagonal exactly (fp64 iterative refinement against G with the fp32 L^-1
+// as preconditioner), writing diag and scores of those coordinates.
+// list: d entries; count: one word. m <= 4096.
+hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, SelectScratch sc, double tau,
+                              unsigned int* count, unsigned int* list, const float* G, int m, int B,
+                              const float* L32, int mp, int64_t lstride, double lam, const float* theta,
+                              double* diag, double* scores, int* err, hipStream_t st);
 hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, SelectScratch sc,
                             uint8_t* mask, hipStream_t st);
 

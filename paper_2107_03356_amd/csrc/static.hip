@@ -148,6 +148,145 @@ __global__ __launch_bounds__(512, 4) void k_trmm_diag(const double* __restrict__
         diag[(int64_t)b * B + c0 + tid] = (1.0 - ((red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]))) * inv_lam;
 }
 
+// fp32 MFMA variant (v_mfma_f32_16x16x4f32) for the fast static mode: the
+// same walk as k_trmm_diag, 32-deep k-chunks of fp32 operands in LDS ([row][k]
+// for L^-1 with a 36-float pitch, [k][column] for G with a 144-float pitch:
+// the 16-row x 4-k and 4-k x 16-column read patterns of one MFMA operand hit
+// distinct banks). L^-1 is read in fp64 (from the factor; LT = double) and
+// rounded when staged, or in fp32 (LT = float). With Lsave, the work-groups
+// of slice 0 also store every L^-1 element they stage, rounded to fp32, to
+// Lsave (which then holds the lower triangle and the zero upper parts of the
+// diagonal 128-blocks: all that a later pass reads). G is only read. W is
+// stored (fp32, row stride d) when Wout is set; the column sums of squares of
+// the fp32 W values are summed in fp64 and give the diagonal when diag is set.
+constexpr int TK32 = 32;
+constexpr int PA32 = TK32 + 4;   // [row][k] pitch (floats)
+constexpr int PB32 = TN + 16;    // [k][column] pitch (floats)
+
+template <typename LT>
+__global__ __launch_bounds__(512, 2) void k_trmm32(const LT* __restrict__ Linv, int mp, int64_t lstride,
+                                                   const float* __restrict__ G, int m, int64_t d, int B, int b0,
+                                                   int nslice, double inv_lam, double* __restrict__ diag,
+                                                   float* __restrict__ Wout, float* __restrict__ Lsave,
+                                                   int64_t sstride) {
+    __shared__ float As[2][TM][PA32];
+    __shared__ float Bs[2][TK32][PB32];
+    __shared__ double red[4][TN];
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int bl = lid / nslice, sl = lid - (lid / nslice) * nslice;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
+    const int rl = lane & 15, kl = lane >> 4;
+    const int b = b0 + bl;
+    const int c0 = sl * TN;
+    const int ncol = (B - c0) < TN ? (B - c0) : TN;
+    const LT* __restrict__ Lb = Linv + (int64_t)bl * lstride;
+    float* __restrict__ Ls = (Lsave && sl == 0) ? Lsave + (int64_t)bl * sstride : nullptr;
+    const float* __restrict__ Gb = G + (int64_t)b * B + c0;
+    const int T = (mp + TM - 1) / TM;
+
+    // staging of one k-chunk: L^-1 rows [r0, r0+128) x k [k0, k0+32), 8 per
+    // thread (row tid/4, k (tid%4)*8 .. +7); G rows [k0, k0+32) x 128 columns,
+    // 8 per thread (row tid/16, columns (tid%16)*8 .. +7)
+    const int ar = tid >> 2, ac = (tid & 3) * 8;
+    const int br = tid >> 4, bc = (tid & 15) * 8;
+    // each float4 clamped on its own (ncol is a multiple of 4): the quads
+    // inside the slice load their own columns, the others in-bounds data that
+    // lands in columns nothing reads
+    const int bc0 = min(bc, ncol - 4), bc1 = min(bc + 4, ncol - 4);
+    float4 ra0, ra1, rb0, rb1;
+    auto load = [&](int r0, int k0) {
+        const int64_t arow = (int64_t)min(r0 + ar, mp - 1) * mp + k0 + ac;
+        if constexpr (sizeof(LT) == 8) {
+            const double2* p = reinterpret_cast<const double2*>(Lb + arow);
+            const double2 x0 = p[0], x1 = p[1], x2 = p[2], x3 = p[3];
+            ra0 = make_float4((float)x0.x, (float)x0.y, (float)x1.x, (float)x1.y);
+            ra1 = make_float4((float)x2.x, (float)x2.y, (float)x3.x, (float)x3.y);
+        } else {
+            const float4* p = reinterpret_cast<const float4*>(Lb + arow);
+            ra0 = p[0];
+            ra1 = p[1];
+        }
+        if (Ls && r0 + ar < mp) {
+            float4* q = reinterpret_cast<float4*>(Ls + arow);
+            q[0] = ra0;
+            q[1] = ra1;
+        }
+        const float* gp = Gb + (int64_t)min(k0 + br, m - 1) * d;
+        rb0 = *reinterpret_cast<const float4*>(gp + bc0);
+        rb1 = *reinterpret_cast<const float4*>(gp + bc1);
+    };
+    auto store = [&](int buf) {
+        float4* a = reinterpret_cast<float4*>(&As[buf][ar][ac]);
+        a[0] = ra0;
+        a[1] = ra1;
+        float4* q = reinterpret_cast<float4*>(&Bs[buf][br][bc]);
+        q[0] = rb0;
+        q[1] = rb1;
+    };
+
+    double sq[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int r = T - 1; r >= 0; --r) {
+        v4f acc[2][4];
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+        const int khi = min((r + 1) * TM, mp);
+        const int nchunk = khi / TK32;
+        load(r * TM, 0);
+        store(0);
+        __syncthreads();
+        for (int c = 0; c < nchunk; ++c) {
+            const int buf = c & 1;
+            if (c + 1 < nchunk) load(r * TM, (c + 1) * TK32);
+#pragma unroll
+            for (int kk = 0; kk < TK32 / 4; ++kk) {
+                float av[2], bv[4];
+#pragma unroll
+                for (int x = 0; x < 2; ++x) av[x] = As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
+#pragma unroll
+                for (int y = 0; y < 4; ++y) bv[y] = Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < 4; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+            }
+            if (c + 1 < nchunk) store(buf ^ 1);
+            __syncthreads();
+        }
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int row = r * TM + wr * 32 + x * 16 + mfma32_row(lane, q);
+                    const int col = wc * 64 + y * 16 + rl;
+                    const float w = acc[x][y][q];
+                    if (row < m) {
+                        sq[y] += (double)w * (double)w;
+                        if (Wout && col < ncol) Wout[(int64_t)row * d + (int64_t)b * B + c0 + col] = w;
+                    }
+                }
+    }
+    if (!diag) return;
+    // column sums of squares: over the lanes of one column (+16, +32), then over the four wr
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+        sq[y] += __shfl_xor(sq[y], 16, 64);
+        sq[y] += __shfl_xor(sq[y], 32, 64);
+    }
+    if (kl == 0) {
+#pragma unroll
+        for (int y = 0; y < 4; ++y) red[wr][wc * 64 + y * 16 + rl] = sq[y];
+    }
+    __syncthreads();
+    if (tid < ncol)
+        diag[(int64_t)b * B + c0 + tid] = (1.0 - ((red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]))) * inv_lam;
+}
+
 __global__ void k_diag_to_f32(const double* __restrict__ dg, int64_t d, float* __restrict__ out) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i < d) out[i] = (float)dg[i];
@@ -305,6 +444,223 @@ __global__ __launch_bounds__(256) void k_mask(const double* __restrict__ s, int6
     }
 }
 
+// ------------------------------------------------------------------ band of the fast mode
+// The fast mode's diagonal carries the fp32 path's rounding. Its scores are
+// exact enough to decide every coordinate whose score lies outside
+// [t(1 - tau), t(1 + tau)], t the keep-th largest score, as long as the
+// relative score error stays below tau / (1 + tau): such a coordinate is on
+// the same side of the fp64 cut. The coordinates inside that band get their
+// diagonal recomputed exactly in fp64 (k_band_refine), then the selection
+// runs again.
+__global__ __launch_bounds__(256) void k_band_collect(const double* __restrict__ s, int64_t d,
+                                                      const unsigned long long* __restrict__ state, double tau,
+                                                      unsigned int* __restrict__ count, unsigned int* __restrict__ list) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= d) return;
+    const double t = __longlong_as_double((long long)state[0]);
+    const double v = s[i];
+    // zero scores (theta_j = 0) are exact in either precision
+    if (v != 0.0 && fabs(v - t) <= tau * t) {
+        const unsigned int k = atomicAdd(count, 1u);
+        list[k] = (unsigned int)i;
+    }
+}
+
+__device__ __forceinline__ double wave_sum_dbl(double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+constexpr int BAND_COLS = 2048;  // block columns per chunk of the matrix-free product
+constexpr int BAND_MAXIT = 12;
+constexpr int BAND_THREADS = 1024;
+
+// 1024-thread block reductions (every thread gets the result); sh: 16 doubles.
+__device__ __forceinline__ double block_sum16(double x, double* sh) {
+    x = wave_sum_dbl(x);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
+    __syncthreads();
+    double r = 0.0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) r += sh[w];
+    return r;
+}
+
+__device__ __forceinline__ double block_max16(double x, double* sh) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o, 64));
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
+    __syncthreads();
+    double r = 0.0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) r = fmax(r, sh[w]);
+    return r;
+}
+
+// The exact diagonal entry of one band coordinate j (block b, column g = G_b[:, j]):
+// x = A^-1 g for A = G_b G_b^T + m*lambda*I by iterative refinement in fp64,
+// x <- x + M (g - A x), where A x is applied matrix-free from the fp32 G
+// (exact products, fp64 sums) and M = L^-T L^-1 is the fp32 copy of the
+// block's inverse factor (the factor of the fp32-path Gram, a close
+// preconditioner: each step multiplies the error by the contraction rho, of
+// the order of that factor's relative error). It stops once the estimated
+// remaining error, rho |w| with rho = |w_k| / |w_(k-1)| (w the last update),
+// is below 1e-15 |x|; err |= 32 if that takes more than BAND_MAXIT steps.
+// Then [F_b^-1]_jj = (1 - g.x) / lambda and its score. One work-group of 16
+// waves per band coordinate, persistent over the band list; every sum has a
+// fixed order, so the results do not depend on the schedule. LDS: x, r, z (m
+// doubles each) and a chunk of G_b^T x.
+__global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __restrict__ G, int m, int64_t d, int B,
+                                                              const float* __restrict__ L32, int mp, int64_t lstride,
+                                                              const unsigned int* __restrict__ count,
+                                                              const unsigned int* __restrict__ list, double lam,
+                                                              double tau, const float* __restrict__ theta,
+                                                              double* __restrict__ diag, double* __restrict__ scores,
+                                                              int* __restrict__ err) {
+    extern __shared__ double sh[];
+    const int mq = (m + 3) & ~3;  // vectors padded to whole quads (r's padding stays 0)
+    double* x = sh;
+    double* r = x + mq;
+    double* z = r + mq;
+    double* u = z + mq;
+    __shared__ double red[16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const unsigned int n = *count;
+    const double mu = (double)m * lam;
+    for (unsigned int c = blockIdx.x; c < n; c += gridDim.x) {
+        const int64_t j = list[c];
+        const int64_t b = j / B;
+        const int64_t jj = j - b * B;
+        const float* __restrict__ Gb = G + b * B;
+        const float* __restrict__ L = L32 + b * lstride;
+        for (int i = tid; i < m; i += BAND_THREADS) x[i] = 0.0;
+        double wprev = 0.0;
+        bool conv = false;
+        for (int it = 0; it < BAND_MAXIT && !conv; ++it) {
+            __syncthreads();
+            for (int i = tid; i < mq; i += BAND_THREADS) r[i] = 0.0;
+            __syncthreads();
+            // r = G_b (G_b^T x), column chunk by column chunk (x = 0 at the first step)
+            for (int c0 = 0; it > 0 && c0 < B; c0 += BAND_COLS) {
+                const int nc = min(BAND_COLS, B - c0);
+                // u = G_b[:, chunk]^T x: wave w owns columns [128w, 128w + 128)
+                // of the chunk, two per lane; eight rows of loads in flight
+                {
+                    const int col = wave * 128 + lane * 2;
+                    const bool ok = col < nc;  // nc is a multiple of 4: the pair is whole
+                    const float* gp = Gb + c0 + (ok ? col : 0);
+                    double a0 = 0.0, a1 = 0.0;
+                    int i = 0;
+                    for (; i + 8 <= m; i += 8) {
+                        float2 q[8];
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) q[t] = *reinterpret_cast<const float2*>(gp + (int64_t)(i + t) * d);
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) {
+                            a0 += (double)q[t].x * x[i + t];
+                            a1 += (double)q[t].y * x[i + t];
+                        }
+                    }
+                    for (; i < m; ++i) {
+                        const float2 q = *reinterpret_cast<const float2*>(gp + (int64_t)i * d);
+                        a0 += (double)q.x * x[i];
+                        a1 += (double)q.y * x[i];
+                    }
+                    if (ok) {
+                        u[col] = a0;
+                        u[col + 1] = a1;
+                    }
+                }
+                __syncthreads();
+                // r_i += G_b[i, chunk] . u: wave per row, float4 per lane
+                for (int i = wave; i < m; i += 16) {
+                    const float* gp = Gb + (int64_t)i * d + c0;
+                    double a = 0.0;
+                    for (int cc = lane * 4; cc < nc; cc += 256) {
+                        const float4 q = *reinterpret_cast<const float4*>(gp + cc);
+                        a += (double)q.x * u[cc] + (double)q.y * u[cc + 1] + (double)q.z * u[cc + 2] +
+                             (double)q.w * u[cc + 3];
+                    }
+                    a = wave_sum_dbl(a);
+                    if (lane == 0) r[i] += a;
+                }
+                __syncthreads();
+            }
+            // residual of the block system
+            for (int i = tid; i < m; i += BAND_THREADS) r[i] = (double)Gb[(int64_t)i * d + jj] - r[i] - mu * x[i];
+            __syncthreads();
+            // z = L^-1 r: wave per row i, entries k <= i (the stored row is zero
+            // from i + 1 to the end of its diagonal 128-block, so whole quads are read)
+            for (int i = wave; i < m; i += 16) {
+                const float* lp = L + (int64_t)i * mp;
+                const int kend = (i + 4) & ~3;
+                double a = 0.0;
+                for (int k = lane * 4; k < kend; k += 256) {
+                    const float4 q = *reinterpret_cast<const float4*>(lp + k);
+                    a += (double)q.x * r[k] + (double)q.y * r[k + 1] + (double)q.z * r[k + 2] +
+                         (double)q.w * r[k + 3];
+                }
+                a = wave_sum_dbl(a);
+                if (lane == 0) z[i] = a;
+            }
+            __syncthreads();
+            // x += L^-T z: thread k sums column k over rows i >= k, eight rows
+            // of loads in flight (coalesced across the wave)
+            double wmax = 0.0, xmax = 0.0;
+            for (int k = tid; k < m; k += BAND_THREADS) {
+                const float* lp = L + k;
+                double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+                int i = k;
+                for (; i + 8 <= m; i += 8) {
+                    float q[8];
+#pragma unroll
+                    for (int t = 0; t < 8; ++t) q[t] = lp[(int64_t)(i + t) * mp];
+#pragma unroll
+                    for (int t = 0; t < 8; ++t) a[t] += (double)q[t] * z[i + t];
+                }
+                for (; i < m; ++i) a[0] += (double)lp[(int64_t)i * mp] * z[i];
+                const double w = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+                const double xn = x[k] + w;
+                x[k] = xn;
+                wmax = fmax(wmax, fabs(w));
+                xmax = fmax(xmax, fabs(xn));
+            }
+            wmax = block_max16(wmax, red);
+            xmax = block_max16(xmax, red);
+            // estimated remaining error: the next update, rho |w| with the
+            // contraction rho measured on the last two updates; 1e-13 of x is
+            // the level at which two fp64 evaluations (this one, a Cholesky
+            // solve) differ anyway
+            conv = it > 0 && wmax * (wmax / wprev) <= 1e-13 * xmax;
+            wprev = wmax;
+        }
+        if (!conv && tid == 0) atomicOr(err, 32);
+        double a = 0.0;
+        for (int i = tid; i < m; i += BAND_THREADS) a += (double)Gb[(int64_t)i * d + jj] * x[i];
+        const double S = block_sum16(a, red);
+        if (tid == 0) {
+            const double dg = (1.0 - S) / lam;
+            diag[j] = dg;
+            const double th = (double)theta[j];
+            const double s_new = th * th / (2.0 * dg);
+            // the fp32 path's error, measured at the cut: the band's width is
+            // only safe while it stays well below tau
+            if (!(fabs(scores[j] - s_new) <= 0.25 * tau * s_new)) atomicOr(err, 64);
+            scores[j] = s_new;
+            if (!(dg > 0.0) || !isfinite(dg)) atomicOr(err, 8);
+        }
+        __syncthreads();
+    }
+}
+
+__global__ void k_fill_u32(unsigned int* __restrict__ p, int n, unsigned int v) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
 __global__ void k_fill_u8(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i < n) p[i] = v;
@@ -317,6 +673,19 @@ hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* 
     const int nslice = (int)ceil_div(B, TN);
     hipLaunchKernelGGL(k_trmm_diag, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv, mp, bstride, G, m, d, B,
                        b0, nslice, 1.0 / lam, diag);
+    return hipGetLastError();
+}
+
+hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
+                         int64_t d, int B, int b0, int nb, double lam, double* diag, float* Wout, float* Lsave,
+                         int64_t sstride, hipStream_t st) {
+    const int nslice = (int)ceil_div(B, TN);
+    if (Linv64)
+        hipLaunchKernelGGL(k_trmm32<double>, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv64, mp, lstride, G,
+                           m, d, B, b0, nslice, 1.0 / lam, diag, Wout, Lsave, sstride);
+    else
+        hipLaunchKernelGGL(k_trmm32<float>, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv32, mp, lstride, G,
+                           m, d, B, b0, nslice, 1.0 / lam, diag, Wout, Lsave, sstride);
     return hipGetLastError();
 }
 
@@ -346,14 +715,9 @@ SelectScratch select_scratch_carve(void* base, int64_t d) {
     return s;
 }
 
-hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, SelectScratch sc, uint8_t* mask,
-                            hipStream_t st) {
-    if (d <= 0) return hipSuccess;
-    if (keep <= 0 || keep >= d) {
-        hipLaunchKernelGGL(k_fill_u8, dim3((unsigned)ceil_div(d, 256)), dim3(256), 0, st, mask, d,
-                           (uint8_t)(keep <= 0 ? 0 : 1));
-        return hipGetLastError();
-    }
+namespace {
+// The keep-th largest key into sc.state (8 radix passes); 0 < keep < d.
+hipError_t select_kth(const double* scores, int64_t d, int64_t keep, SelectScratch sc, hipStream_t st) {
     hipLaunchKernelGGL(k_select_init, dim3(1), dim3(256), 0, st, sc.state, sc.hist, keep);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -367,6 +731,43 @@ hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, Selec
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, SelectScratch sc, double tau,
+                              unsigned int* count, unsigned int* list, const float* G, int m, int B,
+                              const float* L32, int mp, int64_t lstride, double lam, const float* theta,
+                              double* diag, double* scores, int* err, hipStream_t st) {
+    if (d <= 0 || keep <= 0 || keep >= d) return hipSuccess;  // the mask needs no cut
+    hipError_t e = select_kth(scores_in, d, keep, sc, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(256), 0, st, count, 1, 0u);
+    hipLaunchKernelGGL(k_band_collect, dim3((unsigned)ceil_div(d, 256)), dim3(256), 0, st, scores_in, d, sc.state,
+                       tau, count, list);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t lds = (size_t)(3 * ((m + 3) & ~3) + BAND_COLS) * sizeof(double);
+    if (lds > 65536) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_band_refine),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_band_refine, dim3(256), dim3(BAND_THREADS), lds, st, G, m, d, B, L32, mp, lstride, count,
+                       list, lam, tau, theta, diag, scores, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, SelectScratch sc, uint8_t* mask,
+                            hipStream_t st) {
+    if (d <= 0) return hipSuccess;
+    if (keep <= 0 || keep >= d) {
+        hipLaunchKernelGGL(k_fill_u8, dim3((unsigned)ceil_div(d, 256)), dim3(256), 0, st, mask, d,
+                           (uint8_t)(keep <= 0 ? 0 : 1));
+        return hipGetLastError();
+    }
+    hipError_t e = select_kth(scores, d, keep, sc, st);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_tie_count, dim3(sc.nchunk), dim3(256), 0, st, scores, d, sc.state, sc.chunk_cnt);
     hipLaunchKernelGGL(k_tie_scan, dim3(1), dim3(256), 0, st, sc.chunk_cnt, sc.nchunk);
     hipLaunchKernelGGL(k_mask, dim3(sc.nchunk), dim3(256), 0, st, scores, d, sc.state, sc.chunk_cnt, mask);

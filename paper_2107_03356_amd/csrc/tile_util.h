@@ -1,4 +1,4 @@
-// Device helpers shared by the fp64 MFMA tile kernels (gram.hip, factor.hip,
+// Device helpers shared by the MFMA tile kernels (gram.hip, factor.hip,
 // static.hip).
 #pragma once
 
@@ -8,6 +8,13 @@ namespace mfac {
 namespace {
 
 typedef double v4d __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Row, within a 16 x 16 MFMA output tile, of accumulator register r of lane l
+// (the column is l % 16 for both). fp64 16x16x4: rows l/16 + 4r; fp32
+// 16x16x4: rows 4(l/16) + r (four consecutive rows per lane).
+__device__ __forceinline__ int mfma64_row(int lane, int r) { return (lane >> 4) + 4 * r; }
+__device__ __forceinline__ int mfma32_row(int lane, int r) { return 4 * (lane >> 4) + r; }
 
 // Work-groups are dispatched round-robin over the 8 XCDs (each with its own
 // L2). Remap so that consecutive logical indices share an XCD: the tiles of

@@ -249,6 +249,42 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
     if (gram_blocks_part_doubles(nb, mp, B)) IN(part, gram_blocks_part_doubles(nb, mp, B) * 8);
     return launched();
 }
+hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0, int nb, double, float* A, int mp,
+                                double* part, hipStream_t) {
+    IN(G, ((int64_t)(m - 1) * d + (int64_t)(b0 + nb) * B) * 4);
+    IN(A, (int64_t)nb * mp * mp * 4);
+    if (gram_blocks_part_doubles(nb, mp, B)) IN(part, gram_blocks_part_doubles(nb, mp, B) * 8);
+    return launched();
+}
+hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
+                         int64_t d, int B, int b0, int nb, double, double* diag, float* Wout, float* Lsave,
+                         int64_t sstride, hipStream_t) {
+    CHECK((Linv64 != nullptr) != (Linv32 != nullptr));
+    if (Linv64) IN(Linv64, ((int64_t)(nb - 1) * lstride + (int64_t)mp * mp) * 8);
+    if (Linv32) IN(Linv32, ((int64_t)(nb - 1) * lstride + (int64_t)mp * mp) * 4);
+    IN(G, ((int64_t)(m - 1) * d + (int64_t)(b0 + nb) * B) * 4);
+    if (diag) IN(diag + (int64_t)b0 * B, (int64_t)nb * B * 8);
+    if (Wout) IN(Wout, ((int64_t)(m - 1) * d + (int64_t)(b0 + nb) * B) * 4);
+    if (Lsave) IN(Lsave, ((int64_t)(nb - 1) * sstride + (int64_t)mp * mp) * 4);
+    return launched();
+}
+hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, SelectScratch sc, double tau,
+                              unsigned int* count, unsigned int* list, const float* G, int m, int B, const float* L32,
+                              int mp, int64_t lstride, double, const float* theta, double* diag, double* scores,
+                              int* err, hipStream_t) {
+    IN(scores_in, d * 8);
+    IN(scores, d * 8);
+    IN(diag, d * 8);
+    IN(theta, d * 4);
+    IN(count, 4);
+    IN(list, d * 4);
+    IN(G, (int64_t)m * d * 4);
+    IN(L32, ((d / B - 1) * lstride + (int64_t)mp * mp) * 4);
+    IN(sc.hist, 1024);
+    IN(err, 4);
+    CHECK(tau > 0.0 && tau < 1e-3 && keep >= 0 && keep <= d && m <= 4096 && B <= 65536);
+    return launched();
+}
 hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k, double, double* A, int mp, int* err,
                            hipStream_t) {
     IN(K, (int64_t)m * m * 8);
@@ -260,6 +296,13 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err, hipStream_t) {
     IN(A, ((int64_t)(nbatch - 1) * bstride + (int64_t)mp * mp) * 8);
     IN(Linv, ((int64_t)(nbatch - 1) * bstride + (int64_t)mp * mp) * 8);
+    IN(err, 4);
+    CHECK(mp % NB == 0);
+    return launched();
+}
+hipError_t launch_factor_invert32(float* A, float* Linv, int mp, int nbatch, int64_t bstride, int* err, hipStream_t) {
+    IN(A, ((int64_t)(nbatch - 1) * bstride + (int64_t)mp * mp) * 4);
+    IN(Linv, ((int64_t)(nbatch - 1) * bstride + (int64_t)mp * mp) * 4);
     IN(err, 4);
     CHECK(mp % NB == 0);
     return launched();
@@ -466,10 +509,15 @@ void drive_window(int64_t d, int m, int q) {
     CHECK(mfac_window_destroy(w0) == MFAC_OK);
 }
 
-void drive_static(int64_t d, int B, int m, bool paged) {
+void drive_static(int64_t d, int B, int m, bool paged, bool fast = false) {
     fake_reset();
+    mfac_static s0_unused = nullptr;
     const int64_t page = paged ? (B < d ? 2 * (int64_t)B : (d / 3 + 3) / 4 * 4) : 0;
-    const size_t wb = paged ? mfac_static_paged_workspace_bytes(d, B, m, page) : mfac_static_workspace_bytes(d, B, m);
+    const uint32_t fl = fast ? MFAC_STATIC_FP32 : 0u;
+    const size_t wb = paged ? mfac_static_paged_workspace_bytes(d, B, m, page)
+                            : mfac_static_workspace_bytes_flags(d, B, m, fl);
+    if (!paged) CHECK(mfac_static_workspace_bytes_flags(d, B, m, 0) == mfac_static_workspace_bytes(d, B, m));
+    if (fast) CHECK(wb > (size_t)m * d * 4 + (size_t)(d / B) * m * m * 4);  // W and the per-block L^-1
     CHECK(wb > 0);
     void* ws = fake_alloc(wb, "workspace");
     float* G = (float*)fake_alloc((size_t)m * d * 4, paged ? "pinned" : "G");
@@ -484,8 +532,11 @@ void drive_static(int64_t d, int B, int m, bool paged) {
     double* out = (double*)fake_alloc(64 * 8, "out");
     auto make = [&](mfac_static* s, uint32_t flags) {
         return paged ? mfac_static_precompute_paged(s, d, B, m, 1e-4, G, page, ws, wb, flags, ST)
-                     : mfac_static_precompute(s, d, B, m, 1e-4, G, ws, wb, flags, ST);
+                     : mfac_static_precompute(s, d, B, m, 1e-4, G, ws, wb, flags | fl, ST);
     };
+    if (paged) CHECK(mfac_static_precompute_paged(&s0_unused, d, B, m, 1e-4, G, page, ws, wb, MFAC_STATIC_FP32, ST) ==
+                     MFAC_EINVAL);
+    if (fast) CHECK(mfac_static_precompute(&s0_unused, d, B, m, 1e-4, G, ws, wb - 1, fl, ST) == MFAC_EWORKSPACE);
     mfac_static s = nullptr;
     for (uint32_t flags : {0u, (uint32_t)MFAC_STATIC_TRACE}) {
         const long before = launches;
@@ -534,6 +585,17 @@ int main() {
     drive_static(3000, 100, 300, false);     // m > B
     drive_static(8192, 1024, 64, true);      // paged, whole blocks per page
     drive_static(12000, 12000, 64, true);    // paged, one block over all pages
+    drive_static(4096, 256, 64, false, true);     // fast mode
+    drive_static(3000, 100, 300, false, true);    // fast mode, m > B
+    drive_static(65536, 65536, 128, false, true); // fast mode, the widest block it accepts
+    {
+        mfac_static s = nullptr;
+        CHECK(mfac_static_workspace_bytes_flags(4096, 256, 4097, MFAC_STATIC_FP32) == 0);     // m past the fast limit
+        CHECK(mfac_static_workspace_bytes_flags(131072, 131072, 64, MFAC_STATIC_FP32) == 0);  // block past it
+        CHECK(mfac_static_workspace_bytes_flags(4096, 256, 64, 4u) == 0);                     // unknown flag
+        CHECK(mfac_static_precompute(&s, 4096, 256, 4097, 1e-4, (float*)256, (void*)512, size_t(1) << 40,
+                                     MFAC_STATIC_FP32, ST) == MFAC_EINVAL);
+    }
     CHECK(streams_live == 0);
     CHECK(events_live == 0);
     if (failures) {
