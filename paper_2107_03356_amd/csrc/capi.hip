@@ -181,9 +181,10 @@ bool window_sizes_ok(int64_t d, int32_t m, int32_t max_q) {
 
 // Tracing: mark_begin before a phase's first launch, mark_end after its last.
 // A phase whose launch failed leaves its begin event open: the next
-// mark_begin (or marks_free) releases it.
+// mark_begin (or marks_free) releases it. The marks of a phase are recorded
+// on the stream it runs on (the handle's, unless given).
 template <typename H>
-hipError_t mark_begin(H* h) {
+hipError_t mark_begin(H* h, hipStream_t st) {
     if (!h->trace) return hipSuccess;
     if (h->open_ev) {
         (void)hipEventDestroy(h->open_ev);
@@ -194,19 +195,29 @@ hipError_t mark_begin(H* h) {
         h->open_ev = nullptr;
         return e;
     }
-    return hipEventRecord(h->open_ev, h->st);
+    return hipEventRecord(h->open_ev, st);
 }
 
 template <typename H>
-hipError_t mark_end(H* h, int phase) {
+hipError_t mark_end(H* h, int phase, hipStream_t st) {
     if (!h->trace) return hipSuccess;
     hipEvent_t b;
     hipError_t e = hipEventCreate(&b);
     if (e != hipSuccess) return e;
-    e = hipEventRecord(b, h->st);
+    e = hipEventRecord(b, st);
     h->marks->push_back({phase, h->open_ev, b});
     h->open_ev = nullptr;
     return e;
+}
+
+template <typename H>
+hipError_t mark_begin(H* h) {
+    return mark_begin(h, h->st);
+}
+
+template <typename H>
+hipError_t mark_end(H* h, int phase) {
+    return mark_end(h, phase, h->st);
 }
 
 // Sum and release the recorded marks of a handle into ms/count (nph phases).
@@ -690,10 +701,12 @@ int static_batch(int64_t d, int B, int m) {
 }
 
 // partial-tile storage of the split block Gram, for the largest need among the
-// batch sizes used (full batches and the last one)
-int64_t static_gram_part(int64_t nblocks, int batch, int mp, int B) {
+// batch sizes used (full batches and the last one); the fast mode's fp32
+// kernel has its own tiles and splits
+int64_t static_gram_part(int64_t nblocks, int batch, int mp, int B, bool fast) {
     const int last = (int)(nblocks - (ceil_div(nblocks, batch) - 1) * batch);
-    const int64_t a = gram_blocks_part_doubles(batch, mp, B), b = gram_blocks_part_doubles(last, mp, B);
+    auto need = [&](int nb) { return fast ? gram_blocks32_part_doubles(nb, mp, B) : gram_blocks_part_doubles(nb, mp, B); };
+    const int64_t a = need(batch), b = need(last);
     return a > b ? a : b;
 }
 
@@ -710,7 +723,7 @@ size_t static_layout(int64_t d, int B, int m, bool fast, char* base, S* s) {
     // the fp32 L^-1 of every block, W and the band list
     double* A = fast ? nullptr : c.take<double>((size_t)batch * mp * mp);
     double* Linv = fast ? nullptr : c.take<double>((size_t)batch * mp * mp);
-    double* gpart = c.take<double>((size_t)static_gram_part(d / B, batch, mp, B));
+    double* gpart = c.take<double>((size_t)static_gram_part(d / B, batch, mp, B, fast));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
     double* qcoef = c.take<double>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);

@@ -18,6 +18,8 @@
 // the full-d precompute of Section 3.1) the block's columns are also split
 // over work-groups and the fp64 partial tiles are summed in split order by
 // k_gram_blocks_reduce.
+// The fast static mode's k_gram_blocks32 runs the block Gram on fp32 MFMA in
+// 256 x 256 tiles (see there).
 #include "internal.h"
 #include "tile_util.h"
 
@@ -300,22 +302,22 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
 }
 
 // A_b (lower triangle of every tile the factorization reads) = sum over the
-// column splits of the partial tiles, in split order, plus mu on the diagonal
+// column splits of the partial tiles (TS x TS), in split order, plus mu on the diagonal
 // (identity on the padding rows); with accum, the sum is added to A_b instead.
 // Grid (ntiles, nb).
-template <typename OT>
+template <typename OT, int TS>
 __global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __restrict__ part, int nsplit, int ntiles,
                                                             int m, double mu, int accum, OT* __restrict__ A,
                                                             int mp) {
     const int tile = blockIdx.x, bl = blockIdx.y;
     int ti, tj;
     tile_of(tile, ti, tj);
-    const double* src = part + (int64_t)bl * nsplit * ntiles * (GT * GT) + (int64_t)tile * (GT * GT);
-    const int64_t sstride = (int64_t)ntiles * (GT * GT);
+    const double* src = part + (int64_t)bl * nsplit * ntiles * (TS * TS) + (int64_t)tile * (TS * TS);
+    const int64_t sstride = (int64_t)ntiles * (TS * TS);
     OT* Ab = A + (int64_t)bl * mp * mp;
-    for (int e = threadIdx.x; e < GT * GT; e += 256) {
-        const int rr = e / GT, cc = e % GT;
-        const int row = ti * GT + rr, col = tj * GT + cc;
+    for (int e = threadIdx.x; e < TS * TS; e += 256) {
+        const int rr = e / TS, cc = e % TS;
+        const int row = ti * TS + rr, col = tj * TS + cc;
         if (row >= mp || col >= mp || (ti == tj && rr < cc)) continue;
         double v = 0.0;
         for (int s = 0; s < nsplit; ++s) v += src[s * sstride + e];
@@ -327,19 +329,27 @@ __global__ __launch_bounds__(256) void k_gram_blocks_reduce(const double* __rest
     }
 }
 
-// Static blocks on fp32 MFMA (v_mfma_f32_16x16x4f32): the tiling, staging and
-// task layout of k_gram_blocks, with the fp32 operands fed to the matrix
-// cores as they are. Products of 512 columns accumulate in fp32 registers and
-// are then added to fp64 accumulators, so the rounding of a long block stays
-// that of 512-term sums; the tile goes to A (fp64) as in k_gram_blocks.
-constexpr int FLUSH_CHUNKS = 512 / KB;
+// Static blocks on fp32 MFMA (v_mfma_f32_16x16x4f32), for the fast mode. At
+// twice the fp64 rate the 128 x 128 tiles of k_gram_blocks are bound by
+// their operand traffic out of L2, so this kernel takes 256 x 256 lower
+// tiles: one work-group of 16 waves per tile and column split, each wave
+// owning 64 x 64 as 4 x 4 MFMA tiles (two MFMAs per LDS read instead of
+// 1.33, half the operand bytes per flop), 32-column chunks double-buffered
+// in LDS (256 rows x 36 floats per operand: the 16-row x 4-k read of one
+// MFMA operand on distinct banks), the next chunk's loads in flight during
+// the MFMAs. Products accumulate in fp32 over at most SPLIT32 columns; wider
+// blocks are split and the splits summed in fp64 (k_gram_blocks_reduce).
+// In diagonal tiles the waves wholly above the diagonal only stage operands.
+constexpr int GT32 = 256;
+constexpr int KB32 = 32;
+constexpr int PITCH32 = KB32 + 4;
+constexpr int SPLIT32 = 2048;
 
-__global__ __launch_bounds__(512, 2) void k_gram_blocks32(const float* __restrict__ G, int m, int64_t d, int B,
-                                                          int b0, int ntiles, int nsplit, int kcols, double mu,
-                                                          float* __restrict__ A, int mp,
-                                                          double* __restrict__ part) {
-    __shared__ float As[2][GT][PITCH];
-    __shared__ float Bs[2][GT][PITCH];
+__global__ __launch_bounds__(1024) void k_gram_blocks32(const float* __restrict__ G, int m, int64_t d, int B, int b0,
+                                                        int ntiles, int nsplit, int kcols, double mu,
+                                                        float* __restrict__ A, int mp, double* __restrict__ part) {
+    __shared__ float As[2][GT32][PITCH32];
+    __shared__ float Bs[2][GT32][PITCH32];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     const int per_block = ntiles * nsplit;
     const int bl = lid / per_block;
@@ -349,114 +359,100 @@ __global__ __launch_bounds__(512, 2) void k_gram_blocks32(const float* __restric
     int ti, tj;
     tile_of(tile, ti, tj);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
+    const int wr = wave >> 2, wc = wave & 3;  // rows wr*64, columns wc*64
     const int rl = lane & 15, kl = lane >> 4;
     const bool diag_tile = ti == tj;
-    const bool upper_wave = diag_tile && wr * 32 + 31 < wc * 64;
+    const bool upper_wave = diag_tile && wr < wc;
     const int cbeg = sp * kcols;
     const int ncols = (B - cbeg) < kcols ? (B - cbeg) : kcols;
     const float* base = G + (int64_t)(b0 + bl) * B + cbeg;
-    const int ra0 = ti * GT, rb0 = tj * GT;
+    const int ra0 = ti * GT32, rb0 = tj * GT32;
+    // staging: 256 rows x 32 columns per operand, 8 floats per thread and operand
     const int sr = tid >> 2, sc = (tid & 3) * 8;
     const bool oka = ra0 + sr < m, okb = rb0 + sr < m;
     const float* rowa = base + (int64_t)(ra0 + sr) * d;
     const float* rowb = base + (int64_t)(rb0 + sr) * d;
     float4 pa0, pa1, pb0, pb1;
     const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#define MFAC_GB_LOAD(K0_)                                                                              \
-    {                                                                                                  \
-        const int c_ = (K0_) + sc;                                                                     \
-        pa0 = (oka && c_ < ncols) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;                \
-        pa1 = (oka && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;        \
-        if (!diag_tile) {                                                                              \
-            pb0 = (okb && c_ < ncols) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;            \
-            pb1 = (okb && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero;    \
-        }                                                                                              \
+#define MFAC_G32_LOAD(K0_)                                                                          \
+    {                                                                                               \
+        const int c_ = (K0_) + sc;                                                                  \
+        pa0 = (oka && c_ < ncols) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;             \
+        pa1 = (oka && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;     \
+        if (!diag_tile) {                                                                           \
+            pb0 = (okb && c_ < ncols) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;         \
+            pb1 = (okb && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero; \
+        }                                                                                           \
     }
-#define MFAC_GB_STORE(BUF_)                                                                            \
-    {                                                                                                  \
-        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                                     \
-        a_[0] = pa0;                                                                                   \
-        a_[1] = pa1;                                                                                   \
-        if (!diag_tile) {                                                                              \
-            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                                 \
-            b_[0] = pb0;                                                                               \
-            b_[1] = pb1;                                                                               \
-        }                                                                                              \
+#define MFAC_G32_STORE(BUF_)                                                                        \
+    {                                                                                               \
+        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                                  \
+        a_[0] = pa0;                                                                                \
+        a_[1] = pa1;                                                                                \
+        if (!diag_tile) {                                                                           \
+            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                              \
+            b_[0] = pb0;                                                                            \
+            b_[1] = pb1;                                                                            \
+        }                                                                                           \
     }
 
-    v4f acc[2][4];
-    double accd[2][4][4];
+    v4f acc[4][4];
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int y = 0; y < 4; ++y) {
-            acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int r = 0; r < 4; ++r) accd[x][y][r] = 0.0;
-        }
-    const int nchunk = (ncols + KB - 1) / KB;
-    MFAC_GB_LOAD(0)
-    MFAC_GB_STORE(0)
+        for (int y = 0; y < 4; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+    const int nchunk = (ncols + KB32 - 1) / KB32;
+    MFAC_G32_LOAD(0)
+    MFAC_G32_STORE(0)
     __syncthreads();
     for (int c = 0; c < nchunk; ++c) {
         const int buf = c & 1;
-        if (c + 1 < nchunk) MFAC_GB_LOAD((c + 1) * KB)
-        float (*Ab)[PITCH] = As[buf];
-        float (*Bb)[PITCH] = diag_tile ? As[buf] : Bs[buf];
+        if (c + 1 < nchunk) MFAC_G32_LOAD((c + 1) * KB32)
+        float (*Ab)[PITCH32] = As[buf];
+        float (*Bb)[PITCH32] = diag_tile ? As[buf] : Bs[buf];
         if (!upper_wave) {
 #pragma unroll
-            for (int kk = 0; kk < KB / 4; ++kk) {
-                float av[2], bv[4];
+            for (int kk = 0; kk < KB32 / 4; ++kk) {
+                float av[4], bv[4];
 #pragma unroll
-                for (int x = 0; x < 2; ++x) av[x] = Ab[wr * 32 + x * 16 + rl][kk * 4 + kl];
+                for (int x = 0; x < 4; ++x) av[x] = Ab[wr * 64 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
                 for (int y = 0; y < 4; ++y) bv[y] = Bb[wc * 64 + y * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                for (int x = 0; x < 2; ++x)
+                for (int x = 0; x < 4; ++x)
 #pragma unroll
                     for (int y = 0; y < 4; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
-            if ((c + 1) % FLUSH_CHUNKS == 0 || c + 1 == nchunk) {
-#pragma unroll
-                for (int x = 0; x < 2; ++x)
-#pragma unroll
-                    for (int y = 0; y < 4; ++y) {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) accd[x][y][r] += (double)acc[x][y][r];
-                        acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
-                    }
-            }
         }
-        if (c + 1 < nchunk) MFAC_GB_STORE(buf ^ 1)
+        if (c + 1 < nchunk) MFAC_G32_STORE(buf ^ 1)
         __syncthreads();
     }
-#undef MFAC_GB_LOAD
-#undef MFAC_GB_STORE
+#undef MFAC_G32_LOAD
+#undef MFAC_G32_STORE
     if (upper_wave) return;
     if (nsplit > 1) {
-        double* out = part + ((int64_t)bl * nsplit + sp) * ntiles * (GT * GT) + (int64_t)tile * (GT * GT);
+        double* out = part + ((int64_t)bl * nsplit + sp) * ntiles * (GT32 * GT32) + (int64_t)tile * (GT32 * GT32);
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
+        for (int x = 0; x < 4; ++x)
 #pragma unroll
             for (int y = 0; y < 4; ++y)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    out[(wr * 32 + x * 16 + mfma32_row(lane, r)) * GT + wc * 64 + y * 16 + rl] = accd[x][y][r];
+                    out[(wr * 64 + x * 16 + mfma32_row(lane, r)) * GT32 + wc * 64 + y * 16 + rl] = acc[x][y][r];
         return;
     }
     float* Ab = A + (int64_t)bl * mp * mp;
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 4; ++x)
 #pragma unroll
         for (int y = 0; y < 4; ++y)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int row = ra0 + wr * 32 + x * 16 + mfma32_row(lane, r);
+                const int row = ra0 + wr * 64 + x * 16 + mfma32_row(lane, r);
                 const int col = rb0 + wc * 64 + y * 16 + rl;
                 if (row < mp && col < mp) {
-                    double v = accd[x][y][r];
+                    double v = (double)acc[x][y][r];
                     if (row == col) v += (row < m) ? mu : 1.0;
                     Ab[(int64_t)row * mp + col] = (float)v;
                 }
@@ -518,7 +514,31 @@ int gram_blocks_splits(int nb, int mp, int B, int& ntiles, int& kcols) {
     kcols = (int)round_up(ceil_div(B, ns), KB);
     return (int)ceil_div(B, kcols);
 }
+
+// Column splits of the fp32 kernel: at most SPLIT32 columns each (fp32 sums
+// stay short), and more when a batch has fewer tiles than CUs (splits of at
+// least SPLIT32 columns, up to ~1024 work-groups).
+int gram32_splits(int nb, int mp, int B, int& ntiles, int& kcols) {
+    const int T = (int)ceil_div(mp, GT32);
+    ntiles = T * (T + 1) / 2;
+    const int64_t wgs = (int64_t)nb * ntiles;
+    int64_t ns = ceil_div(B, SPLIT32);
+    if (wgs < 256) {
+        int64_t fill = 1024 / wgs;
+        if (fill > B / SPLIT32) fill = B / SPLIT32;
+        if (fill > ns) ns = fill;
+    }
+    if (ns < 1) ns = 1;
+    kcols = (int)round_up(ceil_div(B, ns), KB32);
+    return (int)ceil_div(B, kcols);
+}
 }  // namespace
+
+int64_t gram_blocks32_part_doubles(int nb, int mp, int B) {
+    int ntiles, kcols;
+    const int ns = gram32_splits(nb, mp, B, ntiles, kcols);
+    return ns > 1 ? (int64_t)nb * ns * ntiles * (GT32 * GT32) : 0;
+}
 
 int64_t gram_blocks_part_doubles(int nb, int mp, int B) {
     int ntiles, kcols;
@@ -529,13 +549,13 @@ int64_t gram_blocks_part_doubles(int nb, int mp, int B) {
 hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0, int nb, double mu, float* A,
                                 int mp, double* part, hipStream_t st) {
     int ntiles, kcols;
-    const int ns = gram_blocks_splits(nb, mp, B, ntiles, kcols);
-    hipLaunchKernelGGL(k_gram_blocks32, dim3((unsigned)(ntiles * ns * nb)), dim3(512), 0, st, G, m, d, B, b0, ntiles,
+    const int ns = gram32_splits(nb, mp, B, ntiles, kcols);
+    hipLaunchKernelGGL(k_gram_blocks32, dim3((unsigned)(ntiles * ns * nb)), dim3(1024), 0, st, G, m, d, B, b0, ntiles,
                        ns, kcols, mu, A, mp, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || ns == 1) return e;
-    hipLaunchKernelGGL(k_gram_blocks_reduce<float>, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part, ns,
-                       ntiles, m, mu, 0, A, mp);
+    hipLaunchKernelGGL((k_gram_blocks_reduce<float, GT32>), dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st,
+                       part, ns, ntiles, m, mu, 0, A, mp);
     return hipGetLastError();
 }
 
@@ -548,8 +568,8 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
                        ns, kcols, mu, acc, A, mp, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || ns == 1) return e;
-    hipLaunchKernelGGL(k_gram_blocks_reduce<double>, dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st, part,
-                       ns, ntiles, m, mu, acc, A, mp);
+    hipLaunchKernelGGL((k_gram_blocks_reduce<double, GT>), dim3((unsigned)ntiles, (unsigned)nb), dim3(256), 0, st,
+                       part, ns, ntiles, m, mu, acc, A, mp);
     return hipGetLastError();
 }
 

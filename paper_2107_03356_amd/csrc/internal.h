@@ -83,8 +83,10 @@ int64_t gram_blocks_part_doubles(int nb, int mp, int B);
 hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, int nb,
                               double mu, double* A, int mp, double* part, hipStream_t st,
                               bool accumulate = false);
-// The same on fp32 MFMA (fp32 operands, 512-column fp32 sums added in fp64,
-// split partials summed in fp64), stored as fp32 A; no accumulate mode.
+// The same on fp32 MFMA in 256 x 256 tiles (fp32 sums over at most 2048
+// columns, longer blocks split and the splits summed in fp64), stored as fp32
+// A; no accumulate mode. part: gram_blocks32_part_doubles(nb, mp, B).
+int64_t gram_blocks32_part_doubles(int nb, int mp, int B);
 hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0, int nb, double mu, float* A,
                                 int mp, double* part, hipStream_t st);
 

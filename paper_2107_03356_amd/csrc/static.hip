@@ -472,23 +472,24 @@ __device__ __forceinline__ double wave_sum_dbl(double x) {
     return x;
 }
 
-constexpr int BAND_COLS = 2048;  // block columns per chunk of the matrix-free product
+constexpr int BAND_THREADS = 512;
+constexpr int BAND_WAVES = BAND_THREADS / 64;
+constexpr int BAND_COLS = BAND_WAVES * 128;  // block columns per chunk of the matrix-free product
 constexpr int BAND_MAXIT = 12;
-constexpr int BAND_THREADS = 1024;
 
-// 1024-thread block reductions (every thread gets the result); sh: 16 doubles.
-__device__ __forceinline__ double block_sum16(double x, double* sh) {
+// Work-group reductions (every thread gets the result); sh: BAND_WAVES doubles.
+__device__ __forceinline__ double block_sum_band(double x, double* sh) {
     x = wave_sum_dbl(x);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
     __syncthreads();
     double r = 0.0;
 #pragma unroll
-    for (int w = 0; w < 16; ++w) r += sh[w];
+    for (int w = 0; w < BAND_WAVES; ++w) r += sh[w];
     return r;
 }
 
-__device__ __forceinline__ double block_max16(double x, double* sh) {
+__device__ __forceinline__ double block_max_band(double x, double* sh) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o, 64));
     __syncthreads();
@@ -496,7 +497,7 @@ __device__ __forceinline__ double block_max16(double x, double* sh) {
     __syncthreads();
     double r = 0.0;
 #pragma unroll
-    for (int w = 0; w < 16; ++w) r = fmax(r, sh[w]);
+    for (int w = 0; w < BAND_WAVES; ++w) r = fmax(r, sh[w]);
     return r;
 }
 
@@ -526,7 +527,7 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
     double* r = x + mq;
     double* z = r + mq;
     double* u = z + mq;
-    __shared__ double red[16];
+    __shared__ double red[BAND_WAVES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const unsigned int n = *count;
     const double mu = (double)m * lam;
@@ -547,19 +548,20 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
             for (int c0 = 0; it > 0 && c0 < B; c0 += BAND_COLS) {
                 const int nc = min(BAND_COLS, B - c0);
                 // u = G_b[:, chunk]^T x: wave w owns columns [128w, 128w + 128)
-                // of the chunk, two per lane; eight rows of loads in flight
+                // of the chunk, two per lane; sixteen rows of loads in flight
+                // (rows are d floats apart: each load is its own translation)
                 {
                     const int col = wave * 128 + lane * 2;
                     const bool ok = col < nc;  // nc is a multiple of 4: the pair is whole
                     const float* gp = Gb + c0 + (ok ? col : 0);
                     double a0 = 0.0, a1 = 0.0;
                     int i = 0;
-                    for (; i + 8 <= m; i += 8) {
-                        float2 q[8];
+                    for (; i + 16 <= m; i += 16) {
+                        float2 q[16];
 #pragma unroll
-                        for (int t = 0; t < 8; ++t) q[t] = *reinterpret_cast<const float2*>(gp + (int64_t)(i + t) * d);
+                        for (int t = 0; t < 16; ++t) q[t] = *reinterpret_cast<const float2*>(gp + (int64_t)(i + t) * d);
 #pragma unroll
-                        for (int t = 0; t < 8; ++t) {
+                        for (int t = 0; t < 16; ++t) {
                             a0 += (double)q[t].x * x[i + t];
                             a1 += (double)q[t].y * x[i + t];
                         }
@@ -575,17 +577,27 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
                     }
                 }
                 __syncthreads();
-                // r_i += G_b[i, chunk] . u: wave per row, float4 per lane
-                for (int i = wave; i < m; i += 16) {
-                    const float* gp = Gb + (int64_t)i * d + c0;
-                    double a = 0.0;
+                // r_i += G_b[i, chunk] . u: four rows per wave at a time (their
+                // loads in flight together), float4 per lane
+                for (int i0 = wave * 4; i0 < m; i0 += BAND_WAVES * 4) {
+                    double a[4] = {0.0, 0.0, 0.0, 0.0};
                     for (int cc = lane * 4; cc < nc; cc += 256) {
-                        const float4 q = *reinterpret_cast<const float4*>(gp + cc);
-                        a += (double)q.x * u[cc] + (double)q.y * u[cc + 1] + (double)q.z * u[cc + 2] +
-                             (double)q.w * u[cc + 3];
+                        float4 q[4];
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            q[t] = (i0 + t < m) ? *reinterpret_cast<const float4*>(Gb + (int64_t)(i0 + t) * d + c0 + cc)
+                                                : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            a[t] += (double)q[t].x * u[cc] + (double)q[t].y * u[cc + 1] +
+                                    (double)q[t].z * u[cc + 2] + (double)q[t].w * u[cc + 3];
                     }
-                    a = wave_sum_dbl(a);
-                    if (lane == 0) r[i] += a;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) a[t] = wave_sum_dbl(a[t]);
+                    if (lane == 0)
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            if (i0 + t < m) r[i0 + t] += a[t];
                 }
                 __syncthreads();
             }
@@ -594,32 +606,43 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
             __syncthreads();
             // z = L^-1 r: wave per row i, entries k <= i (the stored row is zero
             // from i + 1 to the end of its diagonal 128-block, so whole quads are read)
-            for (int i = wave; i < m; i += 16) {
-                const float* lp = L + (int64_t)i * mp;
-                const int kend = (i + 4) & ~3;
-                double a = 0.0;
+            for (int i0 = wave * 4; i0 < m; i0 += BAND_WAVES * 4) {
+                // four rows at a time; row i reads its quads below (i + 4) & ~3
+                double a[4] = {0.0, 0.0, 0.0, 0.0};
+                const int kend = (min(i0 + 3, m - 1) + 4) & ~3;
                 for (int k = lane * 4; k < kend; k += 256) {
-                    const float4 q = *reinterpret_cast<const float4*>(lp + k);
-                    a += (double)q.x * r[k] + (double)q.y * r[k + 1] + (double)q.z * r[k + 2] +
-                         (double)q.w * r[k + 3];
+                    float4 q[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        q[t] = (i0 + t < m && k < ((i0 + t + 4) & ~3))
+                                   ? *reinterpret_cast<const float4*>(L + (int64_t)(i0 + t) * mp + k)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        a[t] += (double)q[t].x * r[k] + (double)q[t].y * r[k + 1] + (double)q[t].z * r[k + 2] +
+                                (double)q[t].w * r[k + 3];
                 }
-                a = wave_sum_dbl(a);
-                if (lane == 0) z[i] = a;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) a[t] = wave_sum_dbl(a[t]);
+                if (lane == 0)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (i0 + t < m) z[i0 + t] = a[t];
             }
             __syncthreads();
-            // x += L^-T z: thread k sums column k over rows i >= k, eight rows
-            // of loads in flight (coalesced across the wave)
+            // x += L^-T z: thread k sums column k over rows i >= k, sixteen
+            // rows of loads in flight (coalesced across the wave)
             double wmax = 0.0, xmax = 0.0;
             for (int k = tid; k < m; k += BAND_THREADS) {
                 const float* lp = L + k;
                 double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
                 int i = k;
-                for (; i + 8 <= m; i += 8) {
-                    float q[8];
+                for (; i + 16 <= m; i += 16) {
+                    float q[16];
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) q[t] = lp[(int64_t)(i + t) * mp];
+                    for (int t = 0; t < 16; ++t) q[t] = lp[(int64_t)(i + t) * mp];
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) a[t] += (double)q[t] * z[i + t];
+                    for (int t = 0; t < 16; ++t) a[t & 7] += (double)q[t] * z[i + t];
                 }
                 for (; i < m; ++i) a[0] += (double)lp[(int64_t)i * mp] * z[i];
                 const double w = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
@@ -628,8 +651,8 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
                 wmax = fmax(wmax, fabs(w));
                 xmax = fmax(xmax, fabs(xn));
             }
-            wmax = block_max16(wmax, red);
-            xmax = block_max16(xmax, red);
+            wmax = block_max_band(wmax, red);
+            xmax = block_max_band(xmax, red);
             // estimated remaining error: the next update, rho |w| with the
             // contraction rho measured on the last two updates; 1e-13 of x is
             // the level at which two fp64 evaluations (this one, a Cholesky
@@ -640,7 +663,7 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
         if (!conv && tid == 0) atomicOr(err, 32);
         double a = 0.0;
         for (int i = tid; i < m; i += BAND_THREADS) a += (double)Gb[(int64_t)i * d + jj] * x[i];
-        const double S = block_sum16(a, red);
+        const double S = block_sum_band(a, red);
         if (tid == 0) {
             const double dg = (1.0 - S) / lam;
             diag[j] = dg;

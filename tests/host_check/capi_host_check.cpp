@@ -249,11 +249,12 @@ hipError_t launch_gram_blocks(const float* G, int m, int64_t d, int B, int b0, i
     if (gram_blocks_part_doubles(nb, mp, B)) IN(part, gram_blocks_part_doubles(nb, mp, B) * 8);
     return launched();
 }
+int64_t gram_blocks32_part_doubles(int nb, int mp, int B) { return B > 2048 ? (int64_t)nb * mp * mp * 3 : 0; }
 hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0, int nb, double, float* A, int mp,
                                 double* part, hipStream_t) {
     IN(G, ((int64_t)(m - 1) * d + (int64_t)(b0 + nb) * B) * 4);
     IN(A, (int64_t)nb * mp * mp * 4);
-    if (gram_blocks_part_doubles(nb, mp, B)) IN(part, gram_blocks_part_doubles(nb, mp, B) * 8);
+    if (gram_blocks32_part_doubles(nb, mp, B)) IN(part, gram_blocks32_part_doubles(nb, mp, B) * 8);
     return launched();
 }
 hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
