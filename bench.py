@@ -312,7 +312,7 @@ def bench_static(args, wl, dev):
         "dtype": "f32" if fast else "f64", "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "m": m, "block": B, "lambda": wl.lam, "keep": keep,
                    "page_cols": wl.page_cols or None,
-                   "mode": ("fast: Gram and W on fp32 matrix cores, fp64 factor, fp64 band re-decided at the cut"
+                   "mode": ("fast: Gram, factor and W on fp32 matrix cores, fp64 band re-decided at the cut"
                             if fast else "fp64 matrix cores throughout")},
         "roofline": {"bound": "mfma", "kernel": gram_kernel, "achieved": gram_tf, "peak": mfma_peak,
                      "unit": "TFLOP/s", "frac": gram_tf / mfma_peak,

@@ -7,8 +7,8 @@
 // coefficients of Theorem 1 are then c = lambda^-1 A^-1 G x. The library
 // keeps the explicit inverse A^-1 (the paper's remark that a modified
 // Cholesky kernel would beat its LU): factor.hip computes L and L^-1 with a
-// recursive blocked algorithm whose 64 x 64 leaves this file factors and
-// inverts in registers (k_potrf_diag); k_lauum forms A^-1 = L^-T L^-1; the
+// recursive blocked algorithm whose diagonal nodes of 64 or 128 this file
+// factors and inverts in LDS (k_factor_node); k_lauum forms A^-1 = L^-T L^-1; the
 // O(m^2) slot replacement updates A^-1 in place between refactors; and the
 // coefficient kernel applies it. A is padded to a multiple of 64 with an
 // identity block so no kernel needs edge handling.
@@ -18,11 +18,11 @@
 // tiles, operands from LDS. They are written as C[r][c] = sum_k a[r][k] *
 // b[c][k]; a tile that enters as b[k][c] is transposed while it is staged.
 #include "internal.h"
+#include "tile_util.h"
 
 namespace mfac {
 namespace {
 
-typedef double v4d __attribute__((ext_vector_type(4)));
 constexpr int P = 68;  // LDS pitch of a 64 x 64 fp64 tile
 
 __device__ __forceinline__ void stage_tile_t(double (*S)[P], const double* __restrict__ src, int64_t ld) {
@@ -103,96 +103,233 @@ __global__ __launch_bounds__(256) void k_assemble(double* __restrict__ K, int m,
     A[e] = v;
 }
 
-// ------------------------------------------------------------------ potrf
+// ------------------------------------------------------------------ diagonal nodes
 __device__ __forceinline__ double rsqrt_of(double x) { return rsqrt(x); }
 __device__ __forceinline__ float rsqrt_of(float x) { return rsqrtf(x); }
 
-// One 64-thread wave per batch item (fp64, or fp32 for the fast static mode): factor diagonal tile t in place (lower)
-// and write its inverse into the diagonal tile of Linv. Lane i keeps row i of
-// the tile in registers; each column step broadcasts the new column through a
-// double-buffered LDS vector (reads of step j and writes of step j+2 are
-// separated by the barriers of step j+1), so the trailing update is a run of
-// independent FMAs on registers.
+// v of lane src (src the same in every lane)
+__device__ __forceinline__ float lane_value(float v, int src) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src));
+}
+__device__ __forceinline__ double lane_value(double v, int src) {
+    const long long b = __double_as_longlong(v);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, src);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), src);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+// Orders LDS traffic between the lanes of one wave: a wave's LDS operations
+// complete in issue order, so this only has to keep the compiler from moving
+// them across the point.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 16x16x4 MFMA per element type: accumulator and the row of register r
 template <typename R>
-__global__ __launch_bounds__(64) void k_potrf_diag(R* __restrict__ A, R* __restrict__ Linv, int mp, int64_t bstride,
-                                                   int t, int* __restrict__ err) {
-    __shared__ R col[2][64];
-    __shared__ R T[64][65];
-    __shared__ R rdiag[64];  // 1 / L[j][j]
-    R* Ab = A + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
-    R* Lb = Linv + (int64_t)blockIdx.x * bstride + (int64_t)t * 64 * mp + t * 64;
-    const int i = threadIdx.x;
-    R a[64];
-#pragma unroll
-    for (int c = 0; c < 64; ++c) a[c] = Ab[(int64_t)i * mp + c];
-    int bad = 0;
-#pragma unroll
-    for (int j = 0; j < 64; ++j) {
-        R* cb = col[j & 1];
-        // the pivot lane publishes 1 / L[j][j] = rsqrt(pivot); the column below
-        // it scales by that reciprocal (no division on the per-column chain)
-        if (i == j) {
-            R piv = a[j];
-            if (!(piv > R(0)) || !isfinite(piv)) {
-                bad = 1;
-                piv = R(1);
-            }
-            const R r = rsqrt_of(piv);
-            a[j] = piv * r;
-            cb[j] = r;
-            rdiag[j] = r;
-        }
-        __syncthreads();
-        if (i > j) {
-            a[j] = a[j] * cb[j];
-            cb[i] = a[j];
-        }
-        __syncthreads();
-        if (i > j) {
-            const R lij = a[j];
-#pragma unroll
-            for (int c = j + 1; c < 64; ++c) a[c] -= lij * cb[c];
-        }
+struct NodeMfma;
+template <>
+struct NodeMfma<double> {
+    typedef v4d acc;
+    static __device__ __forceinline__ acc mfma(double a, double b, acc c) {
+        return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
     }
-    if (bad) atomicOr(err, 2);
-    // the factor (lower part of the registers) into LDS and back to A
-#pragma unroll
-    for (int c = 0; c < 64; ++c) {
-        const R v = (c <= i) ? a[c] : R(0);
-        T[i][c] = v;
-        Ab[(int64_t)i * mp + c] = v;
+    static __device__ __forceinline__ int row(int lane, int r) { return mfma64_row(lane, r); }
+};
+template <>
+struct NodeMfma<float> {
+    typedef v4f acc;
+    static __device__ __forceinline__ acc mfma(float a, float b, acc c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
     }
-    __syncthreads();
-    // Column i of the inverse of the lower factor by forward substitution,
-    // kept in registers: x_r = (delta_ri - sum_{l<r} T[r][l] x_l) / T[r][r]
-    // (as a product with the stored reciprocal).
-    // Rows above i come out as exact zeros. Reads of T[r][l] are the same
-    // address across the wave (LDS broadcast); the dot products use four
-    // partial sums so consecutive FMAs do not wait on each other.
+    static __device__ __forceinline__ int row(int lane, int r) { return mfma32_row(lane, r); }
+};
+
+constexpr int NPX = 132;  // LDS pitch of the node (rows of 16-row MFMA reads on distinct banks)
+constexpr int NSP = 20;   // LDS pitch of the 16-column product scratch
+
+// Factor and invert the diagonal node [o, o+n) (n = 64 or 128) of every batch
+// item in one launch: one work-group of four waves per item, the node's lower
+// 64 x 64 tiles resident in LDS (fp64: 153 KB). Blocked in 16 x 16 tiles so
+// that every loop is short and the code stays small:
+//   Cholesky, 16-column panels left to right: wave 0 factors the panel's
+//     diagonal block and inverts it in the same column sweep (a lane per row
+//     of L and per column of the inverse D); the rows below are A D^T, and
+//     the four waves apply the panel's rank-16 update to the lower tiles to
+//     its right, both on MFMA;
+//   inverse of the factor in place, block columns right to left:
+//     Linv[below j][j] = -Linv[below j][below j] L[below j][j] D_j,
+//     where the first factor is already the inverse (two MFMA products).
+// Writes the node's lower tiles of Linv, zeros above the diagonal of its
+// diagonal 64 x 64 tiles; A is only read. Only lower-triangle values of A
+// enter the result. err |= 2 on a non-positive or non-finite pivot (which
+// then continues as 1).
+template <typename R>
+__global__ __launch_bounds__(256) void k_factor_node(const R* __restrict__ A, R* __restrict__ Linv, int mp,
+                                                     int64_t bstride, int o, int n, int* __restrict__ err) {
+    __shared__ R X[128][NPX];
+    __shared__ R S[112][NSP];
+    __shared__ __align__(16) R colv[2][16];  // the current column of L (double-buffered)
+    typedef NodeMfma<R> M;
+    typedef typename M::acc acc_t;
+    const R* Ab = A + (int64_t)blockIdx.x * bstride;
+    R* Lb = Linv + (int64_t)blockIdx.x * bstride;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rl = lane & 15, kl = lane >> 4;
+    const int np = n >> 4;
+    // the lower 64 x 64 tiles (00, 10, 11; 00 alone when n = 64): thread t
+    // moves row t/4, columns 16 (t%4) .. +15 of each, all loads in flight
+    // before the first LDS store
+    constexpr int VE = 16 / sizeof(R);  // elements per 16-byte access
+    typedef R vec_t __attribute__((ext_vector_type(VE)));
+    const int lr = tid >> 2, lc = (tid & 3) * 16;
+    const int ntile = n == 128 ? 3 : 1;
     {
-        R x[64];
+        vec_t buf[3][16 / VE];
 #pragma unroll
-        for (int r = 0; r < 64; ++r) {
-            R s0 = (r == i) ? R(1) : R(0), s1 = 0, s2 = 0, s3 = 0;
+        for (int tl = 0; tl < 3; ++tl) {
+            if (tl < ntile) {
+                const int tr = tl == 0 ? 0 : 64, tc = tl == 2 ? 64 : 0;
+                const vec_t* src = reinterpret_cast<const vec_t*>(Ab + (int64_t)(o + tr + lr) * mp + o + tc + lc);
 #pragma unroll
-            for (int l = 0; l + 3 < r; l += 4) {
-                s0 -= T[r][l] * x[l];
-                s1 -= T[r][l + 1] * x[l + 1];
-                s2 -= T[r][l + 2] * x[l + 2];
-                s3 -= T[r][l + 3] * x[l + 3];
+                for (int v = 0; v < 16 / VE; ++v) buf[tl][v] = src[v];
             }
-#pragma unroll
-            for (int l = r & ~3; l < r; ++l) s0 -= T[r][l] * x[l];
-            x[r] = ((s0 + s1) + (s2 + s3)) * rdiag[r];
         }
-        __syncthreads();
-        // transpose through LDS so each lane writes a row of the inverse
 #pragma unroll
-        for (int r = 0; r < 64; ++r) T[r][i] = x[r];
+        for (int tl = 0; tl < 3; ++tl) {
+            if (tl < ntile) {
+                const int tr = tl == 0 ? 0 : 64, tc = tl == 2 ? 64 : 0;
+#pragma unroll
+                for (int v = 0; v < 16 / VE; ++v) *reinterpret_cast<vec_t*>(&X[tr + lr][tc + lc + v * VE]) = buf[tl][v];
+            }
+        }
     }
     __syncthreads();
+
+    int bad = 0;
+    for (int p = 0; p < np; ++p) {
+        const int j0 = p * 16;
+        if (wave == 0) {
+            // the 16 x 16 diagonal block: lane l < 16 keeps row l of it (r) and
+            // column l of its inverse (x, by forward substitution folded into
+            // the same column sweep); column k of L goes to every lane through
+            // LDS. Lanes 16..63 and entries above the diagonal carry values
+            // that nothing reads.
+            R r[16], x[16];
 #pragma unroll
-    for (int c = 0; c < 64; ++c) Lb[(int64_t)i * mp + c] = T[i][c];
+            for (int c = 0; c < 16; ++c) {
+                r[c] = lane < 16 ? X[j0 + lane][j0 + c] : R(0);
+                x[c] = (c == lane) ? R(1) : R(0);
+            }
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                R pk = lane_value(r[k], k);
+                if (!(pk > R(0)) || !isfinite(pk)) {
+                    bad = 1;
+                    pk = R(1);
+                }
+                const R rs = rsqrt_of(pk);
+                r[k] = lane == k ? pk * rs : r[k] * rs;
+                if (lane < 16) colv[k & 1][lane] = r[k];
+                wave_sync();
+                R lc[16];
+#pragma unroll
+                for (int c = 0; c < 16; ++c) lc[c] = colv[k & 1][c];
+                // x_k = (e_l - sum_{i<k} L[k][i] x_i)_k / L[k][k], then the
+                // rows below take their L[.][k] x_k terms
+                x[k] = x[k] * rs;
+#pragma unroll
+                for (int c = k + 1; c < 16; ++c) {
+                    r[c] -= r[k] * lc[c];
+                    x[c] -= lc[c] * x[k];
+                }
+                wave_sync();
+            }
+            // the inverse block (zeros above its diagonal) over the block
+            if (lane < 16) {
+#pragma unroll
+                for (int c = 0; c < 16; ++c) X[j0 + c][j0 + lane] = x[c];
+            }
+        }
+        __syncthreads();
+        const int nt = np - 1 - p;  // 16-row tiles below the diagonal block
+        // panel rows below: L = A D^T (D the diagonal block's inverse), into S
+        for (int t = wave; t < nt; t += 4) {
+            acc_t acc = acc_t{0, 0, 0, 0};
+            const int ra = j0 + 16 + 16 * t;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                acc = M::mfma(X[ra + rl][j0 + kk * 4 + kl], X[j0 + rl][j0 + kk * 4 + kl], acc);
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) S[16 * t + M::row(lane, rr)][rl] = acc[rr];
+        }
+        __syncthreads();
+        // lower 16 x 16 tiles (a, b), a >= b, of the trailing block -= P P^T,
+        // and the panel rows back into X
+        const int ntl = nt * (nt + 1) / 2;
+        for (int q = wave; q < ntl; q += 4) {
+            int a = 0;
+            while ((a + 1) * (a + 2) / 2 <= q) ++a;
+            const int b = q - a * (a + 1) / 2;
+            const int ra = j0 + 16 + 16 * a, cb = j0 + 16 + 16 * b;
+            acc_t acc;
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) acc[rr] = X[ra + M::row(lane, rr)][cb + rl];
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                acc = M::mfma(-S[16 * a + rl][kk * 4 + kl], S[16 * b + rl][kk * 4 + kl], acc);
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) X[ra + M::row(lane, rr)][cb + rl] = acc[rr];
+        }
+        for (int e = tid; e < nt * 256; e += 256) X[j0 + 16 + (e >> 4)][j0 + (e & 15)] = S[e >> 4][e & 15];
+        __syncthreads();
+    }
+
+    // block columns right to left
+    for (int j = np - 2; j >= 0; --j) {
+        const int nt = np - 1 - j, rb = 16 * (j + 1);
+        for (int t = wave; t < nt; t += 4) {
+            acc_t acc = acc_t{0, 0, 0, 0};
+            for (int s = 0; s <= t; ++s)
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk)
+                    acc = M::mfma(X[rb + 16 * t + rl][rb + 16 * s + kk * 4 + kl],
+                                  X[rb + 16 * s + kk * 4 + kl][16 * j + rl], acc);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) S[16 * t + M::row(lane, r)][rl] = acc[r];
+        }
+        __syncthreads();
+        for (int t = wave; t < nt; t += 4) {
+            acc_t acc = acc_t{0, 0, 0, 0};
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                acc = M::mfma(-S[16 * t + rl][kk * 4 + kl], X[16 * j + kk * 4 + kl][16 * j + rl], acc);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) X[rb + 16 * t + M::row(lane, r)][16 * j + rl] = acc[r];
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int tl = 0; tl < 3; ++tl) {
+        if (tl < ntile) {
+            const int tr = tl == 0 ? 0 : 64, tc = tl == 2 ? 64 : 0;
+            vec_t* dst = reinterpret_cast<vec_t*>(Lb + (int64_t)(o + tr + lr) * mp + o + tc + lc);
+#pragma unroll
+            for (int v = 0; v < 16 / VE; ++v) {
+                vec_t w;
+#pragma unroll
+                for (int q = 0; q < VE; ++q) {
+                    const int r = tr + lr, c = tc + lc + v * VE + q;
+                    w[q] = (c <= r) ? X[r][c] : R(0);
+                }
+                dst[v] = w;
+            }
+        }
+    }
+    if (tid == 0 && bad) atomicOr(err, 2);
 }
 
 template <typename R>
@@ -344,12 +481,14 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
 }
 
 template <typename R>
-hipError_t launch_potrf_tile(R* A, R* Linv, int mp, int nbatch, int64_t bstride, int t, int* err, hipStream_t st) {
-    hipLaunchKernelGGL(k_potrf_diag<R>, dim3(nbatch), dim3(64), 0, st, A, Linv, mp, bstride, t, err);
+hipError_t launch_factor_node(R* A, R* Linv, int mp, int nbatch, int64_t bstride, int o, int n, int* err,
+                              hipStream_t st) {
+    if (n != 64 && n != 128) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_factor_node<R>, dim3(nbatch), dim3(256), 0, st, A, Linv, mp, bstride, o, n, err);
     return hipGetLastError();
 }
-template hipError_t launch_potrf_tile<double>(double*, double*, int, int, int64_t, int, int*, hipStream_t);
-template hipError_t launch_potrf_tile<float>(float*, float*, int, int, int64_t, int, int*, hipStream_t);
+template hipError_t launch_factor_node<double>(double*, double*, int, int, int64_t, int, int, int*, hipStream_t);
+template hipError_t launch_factor_node<float>(float*, float*, int, int, int64_t, int, int, int*, hipStream_t);
 
 template <typename R>
 hipError_t launch_zero_superdiag(R* M, int mp, int nbatch, int64_t bstride, hipStream_t st) {

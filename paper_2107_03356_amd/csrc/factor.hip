@@ -8,8 +8,9 @@
 //                A22 <- A22 - L21 L21^T                (GEMM, lower tiles)
 //                L22 L22^T = A22                      (recursion)
 //                L^-1 21 = -L22^-1 (L21 L11^-1)        (two GEMMs, triangular)
-// Leaves are 64 x 64 tiles factored and inverted by k_potrf_diag. L itself is
-// not kept: L21 lives in the (unused) upper block A12 while the node needs it,
+// Nodes of 64 or 128 are factored and inverted whole in one launch
+// (k_factor_node, in LDS). L itself is not kept: L21 lives in the (unused)
+// upper block A12 while the node needs it,
 // and L21 L11^-1 goes into A21, whose input values are consumed by then.
 // Every GEMM is batched over the matrices and skips the K-range its
 // triangular operand makes zero, so the flops are m^3/3 for the factor and
@@ -21,9 +22,10 @@ namespace mfac {
 
 // defined in chol.hip
 template <typename T>
-hipError_t launch_potrf_tile(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int t, int* err, hipStream_t st);
-template <typename T>
 hipError_t launch_zero_superdiag(T* M, int mp, int nbatch, int64_t bstride, hipStream_t st);
+template <typename T>
+hipError_t launch_factor_node(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int o, int n, int* err,
+                              hipStream_t st);
 
 namespace {
 
@@ -337,7 +339,7 @@ hipError_t gemm(bool ta, bool tb, const T* A, int a0r, int a0c, const T* B, int 
 // multiple of 64). U = L21^T (h x n2) is kept in the upper block A12.
 template <typename T>
 hipError_t factor_node(T* A, T* Linv, int o, int n, int mp, int nbatch, int64_t bstride, int* err, hipStream_t st) {
-    if (n == 64) return launch_potrf_tile(A, Linv, mp, nbatch, bstride, o / 64, err, st);
+    if (n <= 128) return launch_factor_node(A, Linv, mp, nbatch, bstride, o, n, err, st);
     const int h = (n / 128) * 64;  // split at a multiple of 64; n2 >= h
     const int n2 = n - h;
     const int p = o + h;

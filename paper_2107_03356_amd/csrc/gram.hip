@@ -208,19 +208,21 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
     // staging: 128 rows x 32 columns per operand, 8 floats per thread and operand
     const int sr = tid >> 2, sc = (tid & 3) * 8;
     const bool oka = ra0 + sr < m, okb = rb0 + sr < m;
-    const float* rowa = base + (int64_t)(ra0 + sr) * d;
-    const float* rowb = base + (int64_t)(rb0 + sr) * d;
+    // loads from clamped, in-bounds addresses (ncols is a positive multiple of
+    // 4), the values outside the tile replaced by zeros in registers
+    const float* rowa = base + (int64_t)min(ra0 + sr, m - 1) * d;
+    const float* rowb = base + (int64_t)min(rb0 + sr, m - 1) * d;
     float4 pa0, pa1, pb0, pb1;
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#define MFAC_GB_LOAD(K0_)                                                                              \
-    {                                                                                                  \
-        const int c_ = (K0_) + sc;                                                                     \
-        pa0 = (oka && c_ < ncols) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;                \
-        pa1 = (oka && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;        \
-        if (!diag_tile) {                                                                              \
-            pb0 = (okb && c_ < ncols) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;            \
-            pb1 = (okb && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero;    \
-        }                                                                                              \
+#define MFAC_GB_LOAD(K0_)                                                          \
+    {                                                                                    \
+        const int c_ = (K0_) + sc;                                                       \
+        const int ca_ = min(c_, ncols - 4), cb_ = min(c_ + 4, ncols - 4);                \
+        pa0 = keep4(oka && c_ < ncols, *reinterpret_cast<const float4*>(rowa + ca_));     \
+        pa1 = keep4(oka && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowa + cb_)); \
+        if (!diag_tile) {                                                                \
+            pb0 = keep4(okb && c_ < ncols, *reinterpret_cast<const float4*>(rowb + ca_)); \
+            pb1 = keep4(okb && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowb + cb_)); \
+        }                                                                                \
     }
 #define MFAC_GB_STORE(BUF_)                                                                            \
     {                                                                                                  \
@@ -359,7 +361,12 @@ __global__ __launch_bounds__(1024) void k_gram_blocks32(const float* __restrict_
     int ti, tj;
     tile_of(tile, ti, tj);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 2, wc = wave & 3;  // rows wr*64, columns wc*64
+    // wave -> 64 x 64 piece (rows wr*64, columns wc*64): a permutation under
+    // which the ten pieces on or below the diagonal of a diagonal tile fall
+    // 3, 2, 3, 2 on the four SIMDs whether waves go round-robin (wave & 3) or
+    // in runs of four (wave >> 2), so such a tile costs three waves per SIMD
+    const int code = (int)((0xbfed76ca98354021ull >> (4 * wave)) & 15u);
+    const int wr = code >> 2, wc = code & 3;
     const int rl = lane & 15, kl = lane >> 4;
     const bool diag_tile = ti == tj;
     const bool upper_wave = diag_tile && wr < wc;
@@ -370,19 +377,21 @@ __global__ __launch_bounds__(1024) void k_gram_blocks32(const float* __restrict_
     // staging: 256 rows x 32 columns per operand, 8 floats per thread and operand
     const int sr = tid >> 2, sc = (tid & 3) * 8;
     const bool oka = ra0 + sr < m, okb = rb0 + sr < m;
-    const float* rowa = base + (int64_t)(ra0 + sr) * d;
-    const float* rowb = base + (int64_t)(rb0 + sr) * d;
+    // loads from clamped, in-bounds addresses (ncols is a positive multiple of
+    // 4), the values outside the tile replaced by zeros in registers
+    const float* rowa = base + (int64_t)min(ra0 + sr, m - 1) * d;
+    const float* rowb = base + (int64_t)min(rb0 + sr, m - 1) * d;
     float4 pa0, pa1, pb0, pb1;
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#define MFAC_G32_LOAD(K0_)                                                                          \
-    {                                                                                               \
-        const int c_ = (K0_) + sc;                                                                  \
-        pa0 = (oka && c_ < ncols) ? *reinterpret_cast<const float4*>(rowa + c_) : zero;             \
-        pa1 = (oka && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowa + c_ + 4) : zero;     \
-        if (!diag_tile) {                                                                           \
-            pb0 = (okb && c_ < ncols) ? *reinterpret_cast<const float4*>(rowb + c_) : zero;         \
-            pb1 = (okb && c_ + 4 < ncols) ? *reinterpret_cast<const float4*>(rowb + c_ + 4) : zero; \
-        }                                                                                           \
+#define MFAC_G32_LOAD(K0_)                                                          \
+    {                                                                                    \
+        const int c_ = (K0_) + sc;                                                       \
+        const int ca_ = min(c_, ncols - 4), cb_ = min(c_ + 4, ncols - 4);                \
+        pa0 = keep4(oka && c_ < ncols, *reinterpret_cast<const float4*>(rowa + ca_));     \
+        pa1 = keep4(oka && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowa + cb_)); \
+        if (!diag_tile) {                                                                \
+            pb0 = keep4(okb && c_ < ncols, *reinterpret_cast<const float4*>(rowb + ca_)); \
+            pb1 = keep4(okb && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowb + cb_)); \
+        }                                                                                \
     }
 #define MFAC_G32_STORE(BUF_)                                                                        \
     {                                                                                               \

@@ -175,7 +175,11 @@ __global__ __launch_bounds__(512, 2) void k_trmm32(const LT* __restrict__ Linv, 
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     const int bl = lid / nslice, sl = lid - (lid / nslice) * nslice;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
+    // wave -> 32 x 64 piece (rows wr*32, columns wc*64). Waves w and w+4 share
+    // a SIMD (round-robin placement); pairing row pieces {0, 3} and {1, 2}
+    // there balances the chunks skipped in the diagonal 128-block below.
+    const int wr = (wave & 2) ? ((wave & 4) ? 2 : 1) : ((wave & 4) ? 3 : 0);
+    const int wc = wave & 1;
     const int rl = lane & 15, kl = lane >> 4;
     const int b = b0 + bl;
     const int c0 = sl * TN;
@@ -240,18 +244,21 @@ __global__ __launch_bounds__(512, 2) void k_trmm32(const LT* __restrict__ Linv, 
         for (int c = 0; c < nchunk; ++c) {
             const int buf = c & 1;
             if (c + 1 < nchunk) load(r * TM, (c + 1) * TK32);
+            // L^-1 is zero right of this wave's rows: chunks wholly there add nothing
+            if (c * TK32 < r * TM + wr * 32 + 32) {
 #pragma unroll
-            for (int kk = 0; kk < TK32 / 4; ++kk) {
-                float av[2], bv[4];
+                for (int kk = 0; kk < TK32 / 4; ++kk) {
+                    float av[2], bv[4];
 #pragma unroll
-                for (int x = 0; x < 2; ++x) av[x] = As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
+                    for (int x = 0; x < 2; ++x) av[x] = As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
 #pragma unroll
-                for (int y = 0; y < 4; ++y) bv[y] = Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
+                    for (int y = 0; y < 4; ++y) bv[y] = Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
 #pragma unroll
-                for (int x = 0; x < 2; ++x)
+                    for (int x = 0; x < 2; ++x)
 #pragma unroll
-                    for (int y = 0; y < 4; ++y)
-                        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+                        for (int y = 0; y < 4; ++y)
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
+                }
             }
             if (c + 1 < nchunk) store(buf ^ 1);
             __syncthreads();
