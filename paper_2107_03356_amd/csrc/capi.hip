@@ -116,6 +116,7 @@ struct mfac_static_s {
     float* A32;  // fast mode: the batch of fp32 Gram matrices, factored in place
     float* L32;  // fast mode: fp32 L^-1 of every block (the factor writes it here)
     unsigned int *band_count, *band_list;
+    double* band_work;  // fast mode: the wide band refinement's vectors
     hipStream_t st;
     int* err;
     double *A, *Linv, *gpart, *diag, *scores, *qpart;
@@ -729,12 +730,14 @@ size_t static_layout(int64_t d, int B, int m, bool fast, char* base, S* s) {
     float* xobs = c.take<float>((size_t)d);
     float *A32 = nullptr, *L32 = nullptr, *W = nullptr;
     unsigned int *bcount = nullptr, *blist = nullptr;
+    double* bwork = nullptr;
     if (fast) {
         A32 = c.take<float>((size_t)batch * mp * mp);
         L32 = c.take<float>((size_t)(d / B) * mp * mp);
         W = c.take<float>((size_t)m * d);
         bcount = c.take<unsigned int>(64);
         blist = c.take<unsigned int>((size_t)d);
+        bwork = c.take<double>((size_t)band_work_doubles(m, B));
     }
     if (s) {
         s->A32 = A32;
@@ -742,6 +745,7 @@ size_t static_layout(int64_t d, int B, int m, bool fast, char* base, S* s) {
         s->W = W;
         s->band_count = bcount;
         s->band_list = blist;
+        s->band_work = bwork;
         s->qpart = qpart;
         s->qcoef = qcoef;
         s->xobs = xobs;
@@ -871,7 +875,7 @@ MFAC_API mfac_status mfac_obs_mask(mfac_static s, const float* theta, int64_t ke
     HIPCHK(mark_begin(s));
     HIPCHK(launch_scores(theta, s->diag, s->d, sc, s->err, s->st));
     if (s->fast)
-        HIPCHK(launch_band_refine(sc, s->d, keep, s->sel, BAND_TAU, s->band_count, s->band_list, s->G, s->m, s->B,
+        HIPCHK(launch_band_refine(sc, s->d, keep, s->sel, BAND_TAU, s->band_count, s->band_list, s->band_work, s->G, s->m, s->B,
                                   s->L32, s->mp, (int64_t)s->mp * s->mp, s->lambda, theta, s->diag, sc, s->err,
                                   s->st));
     HIPCHK(launch_topk_mask(sc, s->d, keep, s->sel, keep_mask_out, s->st));

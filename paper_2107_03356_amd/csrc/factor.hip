@@ -29,18 +29,19 @@ hipError_t launch_factor_node(T* A, T* Linv, int mp, int nbatch, int64_t bstride
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 16;
+constexpr int BM = 128, BN = 128;
 
 // Per element type: the MFMA (16x16x4: fp64, or fp32 on twice the rate), its
-// accumulator, the row of an accumulator register, and the LDS pitches:
-// [row][k] chunks (the 16-row x 4-k read of one MFMA operand on distinct
-// banks) and [k][n] chunks (rows k .. k+3 on disjoint banks).
+// accumulator, the row of an accumulator register, the k-chunk depth (16 for
+// both: 32-deep fp32 chunks measured slower) and the LDS pitches: [row][k] chunks (the 16-row x 4-k read of one MFMA operand
+// on distinct banks) and [k][n] chunks (rows k .. k+3 on disjoint banks).
 template <typename T>
 struct Mf;
 template <>
 struct Mf<double> {
     typedef v4d acc;
     typedef double2 pair;
+    static constexpr int BK = 16;
     static constexpr int PA = BK + 2;
     static constexpr int PBN = BN + 16;
     static __device__ __forceinline__ acc mfma(double a, double b, acc c) {
@@ -52,6 +53,7 @@ template <>
 struct Mf<float> {
     typedef v4f acc;
     typedef float2 pair;
+    static constexpr int BK = 16;
     static constexpr int PA = BK + 4;
     static constexpr int PBN = BN + 16;
     static __device__ __forceinline__ acc mfma(float a, float b, acc c) {
@@ -136,7 +138,8 @@ template <typename T, bool TA, bool TB>
 __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
     using M = Mf<T>;
     using T2 = typename M::pair;
-    constexpr int PA = M::PA, PBN = M::PBN;
+    constexpr int PA = M::PA, PBN = M::PBN, BK = M::BK;
+    constexpr int NP = BM * BK / (512 * 2);  // operand pairs per thread and chunk
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
     __shared__ T As[2][TA ? BK : BM][TA ? PBN : PA];
     __shared__ T Bs[2][TB ? BN : BK][TB ? PA : PBN];
@@ -158,11 +161,11 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
         if (g.flags & KLO_COL) klo = J * BN;
         const int mrow0 = I * BM, ncol0 = J * BN;
 
-        // staging of 2048 doubles per operand and chunk, 4 per thread (two
-        // double2, kept in named registers):
-        //   [row][k] layout: row tid/4, k (tid%4)*4 .. +3 (32-byte row pieces)
-        //   [k][row] layout: k tid/64 and tid/64 + 8, row 2*(tid%64) .. +1 (a wave per 1 KB row)
-        const int sr = tid >> 2, sk = (tid & 3) * 4;
+        // staging of 128 x BK elements per operand and chunk, NP pairs per
+        // thread, kept in registers:
+        //   [row][k] layout: row tid/4, k (tid%4)*(BK/4) .. +BK/4-1 (row pieces)
+        //   [k][row] layout: k tid/64 + 8q, row 2*(tid%64) .. +1 (a wave per row)
+        const int sr = tid >> 2, sk = (tid & 3) * (BK / 4);
         const int tk = tid >> 6, tn = (tid & 63) * 2;
         // clamped source rows / columns (M, N are even, so a clamped pair stays
         // inside the operand)
@@ -172,21 +175,14 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
             TA ? A + (int64_t)g.a0r * ld + g.a0c + am : A + (int64_t)(g.a0r + am) * ld + g.a0c + sk;
         const T* __restrict__ bp =
             TB ? B + (int64_t)(g.b0r + bn) * ld + g.b0c + sk : B + (int64_t)g.b0r * ld + g.b0c + bn;
-        T2 pa0, pa1, pb0, pb1;
+        T2 pa[NP], pb[NP];
         auto load_chunk = [&](int k0) {
-            if constexpr (TA) {
-                pa0 = *reinterpret_cast<const T2*>(ap + (int64_t)(k0 + tk) * ld);
-                pa1 = *reinterpret_cast<const T2*>(ap + (int64_t)(k0 + tk + 8) * ld);
-            } else {
-                pa0 = *reinterpret_cast<const T2*>(ap + k0);
-                pa1 = *reinterpret_cast<const T2*>(ap + k0 + 2);
-            }
-            if constexpr (TB) {
-                pb0 = *reinterpret_cast<const T2*>(bp + k0);
-                pb1 = *reinterpret_cast<const T2*>(bp + k0 + 2);
-            } else {
-                pb0 = *reinterpret_cast<const T2*>(bp + (int64_t)(k0 + tk) * ld);
-                pb1 = *reinterpret_cast<const T2*>(bp + (int64_t)(k0 + tk + 8) * ld);
+#pragma unroll
+            for (int q = 0; q < NP; ++q) {
+                pa[q] = TA ? *reinterpret_cast<const T2*>(ap + (int64_t)(k0 + tk + 8 * q) * ld)
+                           : *reinterpret_cast<const T2*>(ap + k0 + 2 * q);
+                pb[q] = TB ? *reinterpret_cast<const T2*>(bp + k0 + 2 * q)
+                           : *reinterpret_cast<const T2*>(bp + (int64_t)(k0 + tk + 8 * q) * ld);
             }
         };
         auto put = [](T* dst, T2 v) {
@@ -194,19 +190,16 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
             dst[1] = v.y;
         };
         auto store_chunk = [&](int buf) {
-            if constexpr (TA) {
-                put(&As[buf][tk][tn], pa0);
-                put(&As[buf][tk + 8][tn], pa1);
-            } else {
-                put(&As[buf][sr][sk], pa0);
-                put(&As[buf][sr][sk + 2], pa1);
-            }
-            if constexpr (TB) {
-                put(&Bs[buf][sr][sk], pb0);
-                put(&Bs[buf][sr][sk + 2], pb1);
-            } else {
-                put(&Bs[buf][tk][tn], pb0);
-                put(&Bs[buf][tk + 8][tn], pb1);
+#pragma unroll
+            for (int q = 0; q < NP; ++q) {
+                if constexpr (TA)
+                    put(&As[buf][tk + 8 * q][tn], pa[q]);
+                else
+                    put(&As[buf][sr][sk + 2 * q], pa[q]);
+                if constexpr (TB)
+                    put(&Bs[buf][sr][sk + 2 * q], pb[q]);
+                else
+                    put(&Bs[buf][tk + 8 * q][tn], pb[q]);
             }
         };
 

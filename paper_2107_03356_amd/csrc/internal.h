@@ -146,9 +146,11 @@ SelectScratch select_scratch_carve(void* base, int64_t d);
 // lists the coordinates with |s - t| <= tau t (s != 0) and recomputes their
 // diagonal exactly (fp64 iterative refinement against G with the fp32 L^-1
 // as preconditioner), writing diag and scores of those coordinates.
-// list: d entries; count: one word. m <= 4096.
+// list: d entries; count: one word; work: band_work_doubles(m, B) doubles.
+// m <= 4096.
+int64_t band_work_doubles(int m, int B);
 hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, SelectScratch sc, double tau,
-                              unsigned int* count, unsigned int* list, const float* G, int m, int B,
+                              unsigned int* count, unsigned int* list, double* work, const float* G, int m, int B,
                               const float* L32, int mp, int64_t lstride, double lam, const float* theta,
                               double* diag, double* scores, int* err, hipStream_t st);
 hipError_t launch_topk_mask(const double* scores, int64_t d, int64_t keep, SelectScratch sc,

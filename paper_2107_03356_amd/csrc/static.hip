@@ -508,6 +508,287 @@ __device__ __forceinline__ double block_max_band(double x, double* sh) {
     return r;
 }
 
+// ------------------------------------------------------------------ band refinement, wide
+// The refinement of k_band_refine for up to BR_SLOTS band coordinates at once,
+// each of its steps a launch over the whole grid, so that every slot's passes
+// over G_b and L^-1 run on many work-groups at the HBM rate (one work-group
+// per coordinate streams a block at a small fraction of it). Slot c works on
+// list[c]; BR_ITERS steps are launched, and k_band_refine finishes a slot
+// that has not converged by then (from its x) and the coordinates past the
+// slots. Every sum has a fixed order.
+constexpr int BR_SLOTS = 64;
+constexpr int BR_ITERS = 6;
+constexpr int BR_CH = 4096;  // u columns staged in LDS by the residual pass
+
+struct BandWork {
+    double *x, *r, *z, *u;            // x, r, z: BR_SLOTS x mq; u: BR_SLOTS x B
+    unsigned long long *wmax, *xmax;  // BR_ITERS x BR_SLOTS: max |update|, max |x| (non-negative doubles' bits)
+    int mq;
+};
+
+__device__ __forceinline__ bool band_slot(const unsigned int* __restrict__ count,
+                                          const unsigned int* __restrict__ list, int c, int B, int64_t& j,
+                                          int64_t& b, int64_t& jj) {
+    if ((unsigned int)c >= *count) return false;
+    j = list[c];
+    b = j / B;
+    jj = j - b * B;
+    return true;
+}
+
+// Whether slot c met k_band_refine's stopping test at a step before `it`.
+__device__ __forceinline__ bool band_converged(const BandWork& w, int c, int it) {
+    for (int t = 1; t < it; ++t) {
+        const double wt = __longlong_as_double((long long)w.wmax[t * BR_SLOTS + c]);
+        const double wp = __longlong_as_double((long long)w.wmax[(t - 1) * BR_SLOTS + c]);
+        const double xt = __longlong_as_double((long long)w.xmax[t * BR_SLOTS + c]);
+        if (wt * (wt / wp) <= 1e-13 * xt) return true;
+    }
+    return false;
+}
+
+// x = r = 0 for every slot (r's padding must read as zeros), statistics cleared
+__global__ void k_br_init(BandWork w) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < BR_SLOTS * w.mq) {
+        w.x[i] = 0.0;
+        w.r[i] = 0.0;
+    }
+    if (i < BR_ITERS * BR_SLOTS) {
+        w.wmax[i] = 0ull;
+        w.xmax[i] = 0ull;
+    }
+}
+
+// u = G_b^T x. Grid (ceil(B / 256), BR_SLOTS), 16 waves: each lane four
+// columns, each wave a sixteenth of the rows; the waves' sums added in order.
+__global__ __launch_bounds__(1024) void k_br_u(const float* __restrict__ G, int m, int64_t d, int B,
+                                               const unsigned int* __restrict__ count,
+                                               const unsigned int* __restrict__ list, BandWork w, int it) {
+    const int c = blockIdx.y;
+    int64_t j, b, jj;
+    if (!band_slot(count, list, c, B, j, b, jj) || band_converged(w, c, it)) return;
+    __shared__ double xs[4096];
+    __shared__ double red[16][256];
+    const double* __restrict__ x = w.x + (int64_t)c * w.mq;
+    for (int i = threadIdx.x; i < m; i += 1024) xs[i] = x[i];
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = blockIdx.x * 256 + lane * 4;
+    const bool ok = col < B;  // B is a multiple of 4: the quad is whole
+    const int per = (m + 15) / 16;
+    const int i0 = min(m, wave * per), i1 = min(m, i0 + per);
+    const float* __restrict__ gp = G + b * B + (ok ? col : 0);
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    int i = i0;
+    for (; i + 8 <= i1; i += 8) {
+        float4 q[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) q[t] = *reinterpret_cast<const float4*>(gp + (int64_t)(i + t) * d);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const double xv = xs[i + t];
+            a0 += (double)q[t].x * xv;
+            a1 += (double)q[t].y * xv;
+            a2 += (double)q[t].z * xv;
+            a3 += (double)q[t].w * xv;
+        }
+    }
+    for (; i < i1; ++i) {
+        const float4 q = *reinterpret_cast<const float4*>(gp + (int64_t)i * d);
+        const double xv = xs[i];
+        a0 += (double)q.x * xv;
+        a1 += (double)q.y * xv;
+        a2 += (double)q.z * xv;
+        a3 += (double)q.w * xv;
+    }
+    red[wave][lane * 4 + 0] = a0;
+    red[wave][lane * 4 + 1] = a1;
+    red[wave][lane * 4 + 2] = a2;
+    red[wave][lane * 4 + 3] = a3;
+    __syncthreads();
+    if (threadIdx.x < 256) {
+        const int cc = blockIdx.x * 256 + threadIdx.x;
+        if (cc < B) {
+            double sum = 0.0;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sum += red[v][threadIdx.x];
+            w.u[(int64_t)c * B + cc] = sum;
+        }
+    }
+}
+
+// r = g - G_b u - mu x (r = g at the first step, x = 0). Grid (ceil(m / 16),
+// BR_SLOTS): four rows per wave, u staged through LDS in column chunks.
+__global__ __launch_bounds__(256) void k_br_r(const float* __restrict__ G, int m, int64_t d, int B,
+                                              const unsigned int* __restrict__ count,
+                                              const unsigned int* __restrict__ list, BandWork w, double mu, int it) {
+    const int c = blockIdx.y;
+    int64_t j, b, jj;
+    if (!band_slot(count, list, c, B, j, b, jj) || band_converged(w, c, it)) return;
+    __shared__ double us[BR_CH];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int rb = blockIdx.x * 16 + wave * 4;
+    const float* __restrict__ Gb = G + b * B;
+    double a[4] = {0.0, 0.0, 0.0, 0.0};
+    if (it > 0) {
+        const double* __restrict__ u = w.u + (int64_t)c * B;
+        for (int c0 = 0; c0 < B; c0 += BR_CH) {
+            const int nc = min(BR_CH, B - c0);
+            __syncthreads();
+            for (int t = threadIdx.x; t < nc; t += 256) us[t] = u[c0 + t];
+            __syncthreads();
+            for (int cc = lane * 4; cc < nc; cc += 256) {
+                float4 q[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    q[t] = keep4(rb + t < m,
+                                 *reinterpret_cast<const float4*>(Gb + (int64_t)min(rb + t, m - 1) * d + c0 + cc));
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    a[t] += (double)q[t].x * us[cc] + (double)q[t].y * us[cc + 1] + (double)q[t].z * us[cc + 2] +
+                            (double)q[t].w * us[cc + 3];
+            }
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) a[t] = wave_sum_dbl(a[t]);
+    if (lane == 0) {
+        const double* __restrict__ x = w.x + (int64_t)c * w.mq;
+        double* __restrict__ r = w.r + (int64_t)c * w.mq;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (rb + t < m) r[rb + t] = (double)Gb[(int64_t)(rb + t) * d + jj] - a[t] - mu * x[rb + t];
+    }
+}
+
+// z = L^-1 r. Grid (ceil(m / 16), BR_SLOTS): four rows per wave; row i reads
+// its whole quads up to (i + 4) & ~3 (zeros past i inside its diagonal tile).
+__global__ __launch_bounds__(256) void k_br_z(int m, int B, const float* __restrict__ L32, int mp, int64_t lstride,
+                                              const unsigned int* __restrict__ count,
+                                              const unsigned int* __restrict__ list, BandWork w, int it) {
+    const int c = blockIdx.y;
+    int64_t j, b, jj;
+    if (!band_slot(count, list, c, B, j, b, jj) || band_converged(w, c, it)) return;
+    __shared__ double rs[4096];
+    const double* __restrict__ r = w.r + (int64_t)c * w.mq;
+    for (int i = threadIdx.x; i < w.mq; i += 256) rs[i] = r[i];
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i0 = blockIdx.x * 16 + wave * 4;
+    if (i0 >= m) return;
+    const float* __restrict__ L = L32 + b * lstride;
+    double a[4] = {0.0, 0.0, 0.0, 0.0};
+    const int kend = (min(i0 + 3, m - 1) + 4) & ~3;
+    for (int k = lane * 4; k < kend; k += 256) {
+        float4 q[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            q[t] = keep4(i0 + t < m && k < ((i0 + t + 4) & ~3),
+                         *reinterpret_cast<const float4*>(L + (int64_t)min(i0 + t, m - 1) * mp + k));
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            a[t] += (double)q[t].x * rs[k] + (double)q[t].y * rs[k + 1] + (double)q[t].z * rs[k + 2] +
+                    (double)q[t].w * rs[k + 3];
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) a[t] = wave_sum_dbl(a[t]);
+    if (lane == 0) {
+        double* __restrict__ z = w.z + (int64_t)c * w.mq;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (i0 + t < m) z[i0 + t] = a[t];
+    }
+}
+
+// x += L^-T z and the step's statistics. Grid (ceil(m / 64), BR_SLOTS): lane
+// k of the 64 columns, each wave a quarter of the rows from the tile's first
+// column down (entries above the diagonal masked), summed in wave order.
+__global__ __launch_bounds__(256) void k_br_x(int m, int B, const float* __restrict__ L32, int mp, int64_t lstride,
+                                              const unsigned int* __restrict__ count,
+                                              const unsigned int* __restrict__ list, BandWork w, int it) {
+    const int c = blockIdx.y;
+    int64_t j, b, jj;
+    if (!band_slot(count, list, c, B, j, b, jj) || band_converged(w, c, it)) return;
+    __shared__ double zs[4096];
+    __shared__ double part[4][64];
+    const double* __restrict__ z = w.z + (int64_t)c * w.mq;
+    for (int i = threadIdx.x; i < m; i += 256) zs[i] = z[i];
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int k0 = blockIdx.x * 64, k = k0 + lane;
+    const bool okk = k < m;
+    const int per = (m - k0 + 3) / 4;
+    const int i0 = min(m, k0 + wave * per), i1 = min(m, i0 + per);
+    const float* __restrict__ lp = L32 + b * lstride + (okk ? k : 0);
+    double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+    int i = i0;
+    for (; i + 16 <= i1; i += 16) {
+        float q[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) q[t] = lp[(int64_t)(i + t) * mp];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) a[t & 7] += (i + t >= k) ? (double)q[t] * zs[i + t] : 0.0;
+    }
+    for (; i < i1; ++i) {
+        const float q = lp[(int64_t)i * mp];
+        a[0] += (i >= k) ? (double)q * zs[i] : 0.0;
+    }
+    part[wave][lane] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+    __syncthreads();
+    if (wave == 0) {
+        double wmax = 0.0, xmax = 0.0;
+        if (okk) {
+            const double upd = ((part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]));
+            double* __restrict__ x = w.x + (int64_t)c * w.mq;
+            const double xn = x[k] + upd;
+            x[k] = xn;
+            wmax = fabs(upd);
+            xmax = fabs(xn);
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            wmax = fmax(wmax, __shfl_xor(wmax, o, 64));
+            xmax = fmax(xmax, __shfl_xor(xmax, o, 64));
+        }
+        if (lane == 0) {
+            atomicMax(&w.wmax[it * BR_SLOTS + c], (unsigned long long)__double_as_longlong(wmax));
+            atomicMax(&w.xmax[it * BR_SLOTS + c], (unsigned long long)__double_as_longlong(xmax));
+        }
+    }
+}
+
+// The diagonal entry and score of every slot that converged within the
+// launched steps (k_band_refine finishes the others). Grid BR_SLOTS.
+__global__ __launch_bounds__(256) void k_br_final(const float* __restrict__ G, int m, int64_t d, int B,
+                                                  const unsigned int* __restrict__ count,
+                                                  const unsigned int* __restrict__ list, BandWork w, double lam,
+                                                  double tau, const float* __restrict__ theta,
+                                                  double* __restrict__ diag, double* __restrict__ scores,
+                                                  int* __restrict__ err) {
+    const int c = blockIdx.x;
+    int64_t j, b, jj;
+    if (!band_slot(count, list, c, B, j, b, jj) || !band_converged(w, c, BR_ITERS)) return;
+    __shared__ double red[4];
+    const double* __restrict__ x = w.x + (int64_t)c * w.mq;
+    const float* __restrict__ Gb = G + b * B;
+    double a = 0.0;
+    for (int i = threadIdx.x; i < m; i += 256) a += (double)Gb[(int64_t)i * d + jj] * x[i];
+    a = wave_sum_dbl(a);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const double S = (red[0] + red[1]) + (red[2] + red[3]);
+        const double dg = (1.0 - S) / lam;
+        diag[j] = dg;
+        const double th = (double)theta[j];
+        const double s_new = th * th / (2.0 * dg);
+        if (!(fabs(scores[j] - s_new) <= 0.25 * tau * s_new)) atomicOr(err, 64);
+        scores[j] = s_new;
+        if (!(dg > 0.0) || !isfinite(dg)) atomicOr(err, 8);
+    }
+}
+
 // The exact diagonal entry of one band coordinate j (block b, column g = G_b[:, j]):
 // x = A^-1 g for A = G_b G_b^T + m*lambda*I by iterative refinement in fp64,
 // x <- x + M (g - A x), where A x is applied matrix-free from the fp32 G
@@ -517,15 +798,17 @@ __device__ __forceinline__ double block_max_band(double x, double* sh) {
 // the order of that factor's relative error). It stops once the estimated
 // remaining error, rho |w| with rho = |w_k| / |w_(k-1)| (w the last update),
 // is below 1e-15 |x|; err |= 32 if that takes more than BAND_MAXIT steps.
-// Then [F_b^-1]_jj = (1 - g.x) / lambda and its score. One work-group of 16
+// Then [F_b^-1]_jj = (1 - g.x) / lambda and its score. One work-group of 8
 // waves per band coordinate, persistent over the band list; every sum has a
 // fixed order, so the results do not depend on the schedule. LDS: x, r, z (m
-// doubles each) and a chunk of G_b^T x.
+// doubles each) and a chunk of G_b^T x. Entries below BR_SLOTS were refined
+// by the wide kernels: the converged ones are skipped, the others resume from
+// their x.
 __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __restrict__ G, int m, int64_t d, int B,
                                                               const float* __restrict__ L32, int mp, int64_t lstride,
                                                               const unsigned int* __restrict__ count,
-                                                              const unsigned int* __restrict__ list, double lam,
-                                                              double tau, const float* __restrict__ theta,
+                                                              const unsigned int* __restrict__ list, BandWork bw,
+                                                              double lam, double tau, const float* __restrict__ theta,
                                                               double* __restrict__ diag, double* __restrict__ scores,
                                                               int* __restrict__ err) {
     extern __shared__ double sh[];
@@ -539,20 +822,22 @@ __global__ __launch_bounds__(BAND_THREADS) void k_band_refine(const float* __res
     const unsigned int n = *count;
     const double mu = (double)m * lam;
     for (unsigned int c = blockIdx.x; c < n; c += gridDim.x) {
+        const bool resume = c < (unsigned int)BR_SLOTS;
+        if (resume && band_converged(bw, (int)c, BR_ITERS)) continue;
         const int64_t j = list[c];
         const int64_t b = j / B;
         const int64_t jj = j - b * B;
         const float* __restrict__ Gb = G + b * B;
         const float* __restrict__ L = L32 + b * lstride;
-        for (int i = tid; i < m; i += BAND_THREADS) x[i] = 0.0;
+        for (int i = tid; i < m; i += BAND_THREADS) x[i] = resume ? bw.x[(int64_t)c * bw.mq + i] : 0.0;
         double wprev = 0.0;
         bool conv = false;
         for (int it = 0; it < BAND_MAXIT && !conv; ++it) {
             __syncthreads();
             for (int i = tid; i < mq; i += BAND_THREADS) r[i] = 0.0;
             __syncthreads();
-            // r = G_b (G_b^T x), column chunk by column chunk (x = 0 at the first step)
-            for (int c0 = 0; it > 0 && c0 < B; c0 += BAND_COLS) {
+            // r = G_b (G_b^T x), column chunk by column chunk (x = 0 at a fresh first step)
+            for (int c0 = 0; (it > 0 || resume) && c0 < B; c0 += BAND_COLS) {
                 const int nc = min(BAND_COLS, B - c0);
                 // u = G_b[:, chunk]^T x: wave w owns columns [128w, 128w + 128)
                 // of the chunk, two per lane; sixteen rows of loads in flight
@@ -765,8 +1050,13 @@ hipError_t select_kth(const double* scores, int64_t d, int64_t keep, SelectScrat
 }
 }  // namespace
 
+int64_t band_work_doubles(int m, int B) {
+    const int64_t mq = (m + 3) & ~3;
+    return (int64_t)BR_SLOTS * (3 * mq + B) + 2 * BR_ITERS * BR_SLOTS;
+}
+
 hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, SelectScratch sc, double tau,
-                              unsigned int* count, unsigned int* list, const float* G, int m, int B,
+                              unsigned int* count, unsigned int* list, double* work, const float* G, int m, int B,
                               const float* L32, int mp, int64_t lstride, double lam, const float* theta,
                               double* diag, double* scores, int* err, hipStream_t st) {
     if (d <= 0 || keep <= 0 || keep >= d) return hipSuccess;  // the mask needs no cut
@@ -777,6 +1067,32 @@ hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, 
                        tau, count, list);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+    BandWork w;
+    w.mq = (m + 3) & ~3;
+    w.x = work;
+    w.r = w.x + (int64_t)BR_SLOTS * w.mq;
+    w.z = w.r + (int64_t)BR_SLOTS * w.mq;
+    w.u = w.z + (int64_t)BR_SLOTS * w.mq;
+    w.wmax = reinterpret_cast<unsigned long long*>(w.u + (int64_t)BR_SLOTS * B);
+    w.xmax = w.wmax + BR_ITERS * BR_SLOTS;
+    const double mu = (double)m * lam;
+    const unsigned rows16 = (unsigned)ceil_div(m, 16);
+    const int64_t ninit = (int64_t)BR_SLOTS * w.mq > BR_ITERS * BR_SLOTS ? (int64_t)BR_SLOTS * w.mq : BR_ITERS * BR_SLOTS;
+    hipLaunchKernelGGL(k_br_init, dim3((unsigned)ceil_div(ninit, 256)), dim3(256), 0, st, w);
+    for (int it = 0; it < BR_ITERS; ++it) {
+        if (it > 0)
+            hipLaunchKernelGGL(k_br_u, dim3((unsigned)ceil_div(B, 256), BR_SLOTS), dim3(1024), 0, st, G, m, d, B,
+                               count, list, w, it);
+        hipLaunchKernelGGL(k_br_r, dim3(rows16, BR_SLOTS), dim3(256), 0, st, G, m, d, B, count, list, w, mu, it);
+        hipLaunchKernelGGL(k_br_z, dim3(rows16, BR_SLOTS), dim3(256), 0, st, m, B, L32, mp, lstride, count, list, w,
+                           it);
+        hipLaunchKernelGGL(k_br_x, dim3((unsigned)ceil_div(m, 64), BR_SLOTS), dim3(256), 0, st, m, B, L32, mp,
+                           lstride, count, list, w, it);
+    }
+    hipLaunchKernelGGL(k_br_final, dim3(BR_SLOTS), dim3(256), 0, st, G, m, d, B, count, list, w, lam, tau, theta,
+                       diag, scores, err);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     const size_t lds = (size_t)(3 * ((m + 3) & ~3) + BAND_COLS) * sizeof(double);
     if (lds > 65536) {
         e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_band_refine),
@@ -784,7 +1100,7 @@ hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, 
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(k_band_refine, dim3(256), dim3(BAND_THREADS), lds, st, G, m, d, B, L32, mp, lstride, count,
-                       list, lam, tau, theta, diag, scores, err);
+                       list, w, lam, tau, theta, diag, scores, err);
     return hipGetLastError();
 }
 

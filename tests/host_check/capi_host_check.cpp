@@ -269,10 +269,12 @@ hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int6
     if (Lsave) IN(Lsave, ((int64_t)(nb - 1) * sstride + (int64_t)mp * mp) * 4);
     return launched();
 }
+int64_t band_work_doubles(int m, int B) { return 64 * (3 * (int64_t)((m + 3) & ~3) + B) + 2 * 6 * 64; }
 hipError_t launch_band_refine(const double* scores_in, int64_t d, int64_t keep, SelectScratch sc, double tau,
-                              unsigned int* count, unsigned int* list, const float* G, int m, int B, const float* L32,
-                              int mp, int64_t lstride, double, const float* theta, double* diag, double* scores,
-                              int* err, hipStream_t) {
+                              unsigned int* count, unsigned int* list, double* work, const float* G, int m, int B,
+                              const float* L32, int mp, int64_t lstride, double, const float* theta, double* diag,
+                              double* scores, int* err, hipStream_t) {
+    IN(work, band_work_doubles(m, B) * 8);
     IN(scores_in, d * 8);
     IN(scores, d * 8);
     IN(diag, d * 8);
