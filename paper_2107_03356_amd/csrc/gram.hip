@@ -217,23 +217,24 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
     {                                                                                    \
         const int c_ = (K0_) + sc;                                                       \
         const int ca_ = min(c_, ncols - 4), cb_ = min(c_ + 4, ncols - 4);                \
-        pa0 = keep4(oka && c_ < ncols, *reinterpret_cast<const float4*>(rowa + ca_));     \
-        pa1 = keep4(oka && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowa + cb_)); \
+        pa0 = *reinterpret_cast<const float4*>(rowa + ca_);                              \
+        pa1 = *reinterpret_cast<const float4*>(rowa + cb_);                              \
         if (!diag_tile) {                                                                \
-            pb0 = keep4(okb && c_ < ncols, *reinterpret_cast<const float4*>(rowb + ca_)); \
-            pb1 = keep4(okb && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowb + cb_)); \
+            pb0 = *reinterpret_cast<const float4*>(rowb + ca_);                          \
+            pb1 = *reinterpret_cast<const float4*>(rowb + cb_);                          \
         }                                                                                \
     }
-#define MFAC_GB_STORE(BUF_)                                                                            \
-    {                                                                                                  \
-        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                                     \
-        a_[0] = pa0;                                                                                   \
-        a_[1] = pa1;                                                                                   \
-        if (!diag_tile) {                                                                              \
-            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                                 \
-            b_[0] = pb0;                                                                               \
-            b_[1] = pb1;                                                                               \
-        }                                                                                              \
+#define MFAC_GB_STORE(BUF_, K0_)                                                   \
+    {                                                                                    \
+        const int c_ = (K0_) + sc;                                                       \
+        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                       \
+        a_[0] = keep4(oka && c_ < ncols, pa0);                                           \
+        a_[1] = keep4(oka && c_ + 4 < ncols, pa1);                                       \
+        if (!diag_tile) {                                                                \
+            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                   \
+            b_[0] = keep4(okb && c_ < ncols, pb0);                                       \
+            b_[1] = keep4(okb && c_ + 4 < ncols, pb1);                                   \
+        }                                                                                \
     }
 
     v4d acc[2][4];
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
         for (int y = 0; y < 4; ++y) acc[x][y] = v4d{0.0, 0.0, 0.0, 0.0};
     const int nchunk = (ncols + KB - 1) / KB;
     MFAC_GB_LOAD(0)
-    MFAC_GB_STORE(0)
+    MFAC_GB_STORE(0, 0)
     __syncthreads();
     for (int c = 0; c < nchunk; ++c) {
         const int buf = c & 1;
@@ -265,7 +266,7 @@ __global__ __launch_bounds__(512, 4) void k_gram_blocks(const float* __restrict_
                         acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
         }
-        if (c + 1 < nchunk) MFAC_GB_STORE(buf ^ 1)
+        if (c + 1 < nchunk) MFAC_GB_STORE(buf ^ 1, (c + 1) * KB)
         __syncthreads();
     }
 #undef MFAC_GB_LOAD
@@ -386,23 +387,24 @@ __global__ __launch_bounds__(1024) void k_gram_blocks32(const float* __restrict_
     {                                                                                    \
         const int c_ = (K0_) + sc;                                                       \
         const int ca_ = min(c_, ncols - 4), cb_ = min(c_ + 4, ncols - 4);                \
-        pa0 = keep4(oka && c_ < ncols, *reinterpret_cast<const float4*>(rowa + ca_));     \
-        pa1 = keep4(oka && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowa + cb_)); \
+        pa0 = *reinterpret_cast<const float4*>(rowa + ca_);                              \
+        pa1 = *reinterpret_cast<const float4*>(rowa + cb_);                              \
         if (!diag_tile) {                                                                \
-            pb0 = keep4(okb && c_ < ncols, *reinterpret_cast<const float4*>(rowb + ca_)); \
-            pb1 = keep4(okb && c_ + 4 < ncols, *reinterpret_cast<const float4*>(rowb + cb_)); \
+            pb0 = *reinterpret_cast<const float4*>(rowb + ca_);                          \
+            pb1 = *reinterpret_cast<const float4*>(rowb + cb_);                          \
         }                                                                                \
     }
-#define MFAC_G32_STORE(BUF_)                                                                        \
-    {                                                                                               \
-        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                                  \
-        a_[0] = pa0;                                                                                \
-        a_[1] = pa1;                                                                                \
-        if (!diag_tile) {                                                                           \
-            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                              \
-            b_[0] = pb0;                                                                            \
-            b_[1] = pb1;                                                                            \
-        }                                                                                           \
+#define MFAC_G32_STORE(BUF_, K0_)                                                   \
+    {                                                                                    \
+        const int c_ = (K0_) + sc;                                                       \
+        float4* a_ = reinterpret_cast<float4*>(&As[BUF_][sr][sc]);                       \
+        a_[0] = keep4(oka && c_ < ncols, pa0);                                           \
+        a_[1] = keep4(oka && c_ + 4 < ncols, pa1);                                       \
+        if (!diag_tile) {                                                                \
+            float4* b_ = reinterpret_cast<float4*>(&Bs[BUF_][sr][sc]);                   \
+            b_[0] = keep4(okb && c_ < ncols, pb0);                                       \
+            b_[1] = keep4(okb && c_ + 4 < ncols, pb1);                                   \
+        }                                                                                \
     }
 
     v4f acc[4][4];
@@ -412,7 +414,7 @@ __global__ __launch_bounds__(1024) void k_gram_blocks32(const float* __restrict_
         for (int y = 0; y < 4; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
     const int nchunk = (ncols + KB32 - 1) / KB32;
     MFAC_G32_LOAD(0)
-    MFAC_G32_STORE(0)
+    MFAC_G32_STORE(0, 0)
     __syncthreads();
     for (int c = 0; c < nchunk; ++c) {
         const int buf = c & 1;
@@ -434,7 +436,7 @@ __global__ __launch_bounds__(1024) void k_gram_blocks32(const float* __restrict_
                         acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y], 0, 0, 0);
             }
         }
-        if (c + 1 < nchunk) MFAC_G32_STORE(buf ^ 1)
+        if (c + 1 < nchunk) MFAC_G32_STORE(buf ^ 1, (c + 1) * KB32)
         __syncthreads();
     }
 #undef MFAC_G32_LOAD

@@ -24,6 +24,9 @@ __device__ __forceinline__ int xcd_remap(int p, int n) {
     return (p % 8) * (n / 8) + p / 8;
 }
 
+// Component t (a compile-time constant after unrolling) of a float4.
+__device__ __forceinline__ float f4_at(const float4& v, int t) { return t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w; }
+
 // v where ok, else zeros; element-wise so the value stays in registers.
 __device__ __forceinline__ float4 keep4(bool ok, float4 v) {
     return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
