@@ -840,8 +840,7 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
         if (ef != hipSuccess) return fail();
         if (mark_end(s, 1) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
         const hipError_t et =
-            fast ? launch_trmm32(nullptr, L32b, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, nullptr,
-                                 nullptr, 0, s->st)
+            fast ? launch_trmm32(L32b, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, nullptr, s->st)
                  : launch_trmm_diag(s->Linv, s->mp, bstride, G, m, d, block, b0, nb, lambda, s->diag, s->st);
         if (et != hipSuccess) return fail();
         if (mark_end(s, 2) != hipSuccess) return fail();
@@ -889,8 +888,8 @@ namespace {
 mfac_status ensure_w(mfac_static s) {
     if (!s->fast || s->w_ready) return MFAC_OK;
     const int64_t bstride = (int64_t)s->mp * s->mp;
-    HIPCHK(launch_trmm32(nullptr, s->L32, s->mp, bstride, s->G, s->m, s->d, s->B, 0, s->nblocks, s->lambda, nullptr,
-                         s->W, nullptr, 0, s->st));
+    HIPCHK(launch_trmm32(s->L32, s->mp, bstride, s->G, s->m, s->d, s->B, 0, s->nblocks, s->lambda, nullptr, s->W,
+                         s->st));
     s->w_ready = true;
     return MFAC_OK;
 }

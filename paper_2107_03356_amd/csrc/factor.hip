@@ -222,21 +222,30 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
         if (nchunk > 0) load_chunk(klo);
         // beta C enters as the accumulator's start value (scaled by 1/alpha), so
         // its loads issue together with the first chunk's
+        // (the test is uniform and outside the loops, so all 32 loads issue
+        // before the first wait)
         typename M::acc acc[2][4];
         const T cs = (T)(g.beta / g.alpha);
+        if (g.beta != 0.0 && !idle) {
     #pragma unroll
-        for (int x = 0; x < 2; ++x)
+            for (int x = 0; x < 2; ++x)
     #pragma unroll
-            for (int y = 0; y < 4; ++y)
+                for (int y = 0; y < 4; ++y)
     #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    T v = 0;
-                    if (g.beta != 0.0 && !idle) {
+                    for (int r = 0; r < 4; ++r) {
                         const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
-                        v = cs * C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
+                        acc[x][y][r] = C[(int64_t)(g.cm0 + row) * ld + g.cn0 + col];
                     }
-                    acc[x][y][r] = v;
-                }
+    #pragma unroll
+            for (int x = 0; x < 2; ++x)
+    #pragma unroll
+                for (int y = 0; y < 4; ++y) acc[x][y] *= cs;
+        } else {
+    #pragma unroll
+            for (int x = 0; x < 2; ++x)
+    #pragma unroll
+                for (int y = 0; y < 4; ++y) acc[x][y] = typename M::acc{0, 0, 0, 0};
+        }
         if (nchunk > 0) {
             store_chunk(0);
             __syncthreads();

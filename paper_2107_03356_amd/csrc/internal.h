@@ -122,14 +122,12 @@ hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double*
 hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* G, int m,
                             int64_t d, int B, int b0, int nb, double lam, double* diag,
                             hipStream_t st);
-// W_b = Linv_b G_b on fp32 MFMA for blocks [b0, b0+nb): Linv from Linv64
-// (fp64, the factor's output) or Linv32 (fp32), batch stride lstride; G is
-// read only. diag (or nullptr): (1 - colsum(W^2)) / lam in fp64 from the fp32
-// W. Wout (or nullptr): W, row stride d. Lsave (or nullptr): the fp32 L^-1
-// elements the pass reads, per block at stride sstride.
-hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
-                         int64_t d, int B, int b0, int nb, double lam, double* diag, float* Wout, float* Lsave,
-                         int64_t sstride, hipStream_t st);
+// W_b = Linv_b G_b on fp32 MFMA for blocks [b0, b0+nb): Linv the fp32 L^-1
+// of each block at batch stride lstride; G is read only. diag (or nullptr):
+// (1 - colsum(W^2)) / lam in fp64 from the fp32 W. Wout (or nullptr): W, row
+// stride d.
+hipError_t launch_trmm32(const float* Linv, int mp, int64_t lstride, const float* G, int m, int64_t d, int B, int b0,
+                         int nb, double lam, double* diag, float* Wout, hipStream_t st);
 hipError_t launch_diag_to_f32(const double* diag, int64_t d, float* out, hipStream_t st);
 hipError_t launch_scores(const float* theta, const double* diag, int64_t d, double* scores,
                          int* err, hipStream_t st);

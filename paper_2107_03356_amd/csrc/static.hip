@@ -152,23 +152,17 @@ __global__ __launch_bounds__(512, 4) void k_trmm_diag(const double* __restrict__
 // same walk as k_trmm_diag, 32-deep k-chunks of fp32 operands in LDS ([row][k]
 // for L^-1 with a 36-float pitch, [k][column] for G with a 144-float pitch:
 // the 16-row x 4-k and 4-k x 16-column read patterns of one MFMA operand hit
-// distinct banks). L^-1 is read in fp64 (from the factor; LT = double) and
-// rounded when staged, or in fp32 (LT = float). With Lsave, the work-groups
-// of slice 0 also store every L^-1 element they stage, rounded to fp32, to
-// Lsave (which then holds the lower triangle and the zero upper parts of the
-// diagonal 128-blocks: all that a later pass reads). G is only read. W is
+// distinct banks), L^-1 the fp32 factor's output. G is only read. W is
 // stored (fp32, row stride d) when Wout is set; the column sums of squares of
 // the fp32 W values are summed in fp64 and give the diagonal when diag is set.
 constexpr int TK32 = 32;
 constexpr int PA32 = TK32 + 4;   // [row][k] pitch (floats)
 constexpr int PB32 = TN + 16;    // [k][column] pitch (floats)
 
-template <typename LT>
-__global__ __launch_bounds__(512, 2) void k_trmm32(const LT* __restrict__ Linv, int mp, int64_t lstride,
+__global__ __launch_bounds__(512, 2) void k_trmm32(const float* __restrict__ Linv, int mp, int64_t lstride,
                                                    const float* __restrict__ G, int m, int64_t d, int B, int b0,
                                                    int nslice, double inv_lam, double* __restrict__ diag,
-                                                   float* __restrict__ Wout, float* __restrict__ Lsave,
-                                                   int64_t sstride) {
+                                                   float* __restrict__ Wout) {
     __shared__ float As[2][TM][PA32];
     __shared__ float Bs[2][TK32][PB32];
     __shared__ double red[4][TN];
@@ -184,8 +178,7 @@ __global__ __launch_bounds__(512, 2) void k_trmm32(const LT* __restrict__ Linv, 
     const int b = b0 + bl;
     const int c0 = sl * TN;
     const int ncol = (B - c0) < TN ? (B - c0) : TN;
-    const LT* __restrict__ Lb = Linv + (int64_t)bl * lstride;
-    float* __restrict__ Ls = (Lsave && sl == 0) ? Lsave + (int64_t)bl * sstride : nullptr;
+    const float* __restrict__ Lb = Linv + (int64_t)bl * lstride;
     const float* __restrict__ Gb = G + (int64_t)b * B + c0;
     const int T = (mp + TM - 1) / TM;
 
@@ -201,21 +194,9 @@ __global__ __launch_bounds__(512, 2) void k_trmm32(const LT* __restrict__ Linv, 
     float4 ra0, ra1, rb0, rb1;
     auto load = [&](int r0, int k0) {
         const int64_t arow = (int64_t)min(r0 + ar, mp - 1) * mp + k0 + ac;
-        if constexpr (sizeof(LT) == 8) {
-            const double2* p = reinterpret_cast<const double2*>(Lb + arow);
-            const double2 x0 = p[0], x1 = p[1], x2 = p[2], x3 = p[3];
-            ra0 = make_float4((float)x0.x, (float)x0.y, (float)x1.x, (float)x1.y);
-            ra1 = make_float4((float)x2.x, (float)x2.y, (float)x3.x, (float)x3.y);
-        } else {
-            const float4* p = reinterpret_cast<const float4*>(Lb + arow);
-            ra0 = p[0];
-            ra1 = p[1];
-        }
-        if (Ls && r0 + ar < mp) {
-            float4* q = reinterpret_cast<float4*>(Ls + arow);
-            q[0] = ra0;
-            q[1] = ra1;
-        }
+        const float4* p = reinterpret_cast<const float4*>(Lb + arow);
+        ra0 = p[0];
+        ra1 = p[1];
         const float* gp = Gb + (int64_t)min(k0 + br, m - 1) * d;
         rb0 = *reinterpret_cast<const float4*>(gp + bc0);
         rb1 = *reinterpret_cast<const float4*>(gp + bc1);
@@ -991,16 +972,11 @@ hipError_t launch_trmm_diag(const double* Linv, int mp, int64_t bstride, float* 
     return hipGetLastError();
 }
 
-hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
-                         int64_t d, int B, int b0, int nb, double lam, double* diag, float* Wout, float* Lsave,
-                         int64_t sstride, hipStream_t st) {
+hipError_t launch_trmm32(const float* Linv, int mp, int64_t lstride, const float* G, int m, int64_t d, int B, int b0,
+                         int nb, double lam, double* diag, float* Wout, hipStream_t st) {
     const int nslice = (int)ceil_div(B, TN);
-    if (Linv64)
-        hipLaunchKernelGGL(k_trmm32<double>, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv64, mp, lstride, G,
-                           m, d, B, b0, nslice, 1.0 / lam, diag, Wout, Lsave, sstride);
-    else
-        hipLaunchKernelGGL(k_trmm32<float>, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv32, mp, lstride, G,
-                           m, d, B, b0, nslice, 1.0 / lam, diag, Wout, Lsave, sstride);
+    hipLaunchKernelGGL(k_trmm32, dim3((unsigned)(nslice * nb)), dim3(512), 0, st, Linv, mp, lstride, G, m, d, B, b0,
+                       nslice, 1.0 / lam, diag, Wout);
     return hipGetLastError();
 }
 

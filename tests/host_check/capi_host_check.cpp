@@ -257,16 +257,12 @@ hipError_t launch_gram_blocks32(const float* G, int m, int64_t d, int B, int b0,
     if (gram_blocks32_part_doubles(nb, mp, B)) IN(part, gram_blocks32_part_doubles(nb, mp, B) * 8);
     return launched();
 }
-hipError_t launch_trmm32(const double* Linv64, const float* Linv32, int mp, int64_t lstride, const float* G, int m,
-                         int64_t d, int B, int b0, int nb, double, double* diag, float* Wout, float* Lsave,
-                         int64_t sstride, hipStream_t) {
-    CHECK((Linv64 != nullptr) != (Linv32 != nullptr));
-    if (Linv64) IN(Linv64, ((int64_t)(nb - 1) * lstride + (int64_t)mp * mp) * 8);
-    if (Linv32) IN(Linv32, ((int64_t)(nb - 1) * lstride + (int64_t)mp * mp) * 4);
+hipError_t launch_trmm32(const float* Linv, int mp, int64_t lstride, const float* G, int m, int64_t d, int B, int b0,
+                         int nb, double, double* diag, float* Wout, hipStream_t) {
+    IN(Linv, ((int64_t)(nb - 1) * lstride + (int64_t)mp * mp) * 4);
     IN(G, ((int64_t)(m - 1) * d + (int64_t)(b0 + nb) * B) * 4);
     if (diag) IN(diag + (int64_t)b0 * B, (int64_t)nb * B * 8);
     if (Wout) IN(Wout, ((int64_t)(m - 1) * d + (int64_t)(b0 + nb) * B) * 4);
-    if (Lsave) IN(Lsave, ((int64_t)(nb - 1) * sstride + (int64_t)mp * mp) * 4);
     return launched();
 }
 int64_t band_work_doubles(int m, int B) { return 64 * (3 * (int64_t)((m + 3) & ~3) + B) + 2 * 6 * 64; }
