@@ -719,9 +719,11 @@ def main():
     del_rows = win.get_rows(0, calib_rows)
     del del_rows
 
-    # ---- timed region: K steps, HIP events on the library's stream (torch's current stream)
+    # ---- timed region: K steps, HIP events on the library's stream (torch's
+    # current stream); the library's stage tracing stays off here (each of its
+    # marks costs a few microseconds of queue time between launches)
+    win.trace(False)
     win.trace_read()   # drop any earlier marks
-    win.trace(True)
     stream = torch.cuda.current_stream(dev)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -732,14 +734,20 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    win.trace(False)
     ms_total = e0.elapsed_time(e1)
-    ph_ms, ph_cnt = win.trace_read()
     st = win.status()
     if st != 0:
         log(f"device error after the timed steps: {P.status_string(st)}")
         sys.exit(1)
     log(f"timed {args.steps} steps: {ms_total:.1f} ms (wall {wall * 1e3:.1f} ms)")
+    # the same K steps once more with stage tracing on, outside the timed
+    # region: per-phase times and the pass kernels' own durations (roofline)
+    win.trace(True)
+    for t in range(args.warmup, nsteps):
+        step(t, out=y)
+    torch.cuda.synchronize()
+    win.trace(False)
+    ph_ms, ph_cnt = win.trace_read()
 
     # The periodic full refactor (every R replaces, R = max(m, 1024) by
     # default) falls outside a 200-step window; its cost is measured here on

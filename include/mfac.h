@@ -200,7 +200,8 @@ mfac_status mfac_window_set_stream(mfac_window w, hipStream_t stream);
  * enable != 0 starts recording around every replace, replace_seq and ihvp;
  * 0 stops (recorded events are kept until read). In mfac_window_replace_seq
  * phase 2 is the fused pass (G^T c of one step with G x of the next) for all
- * but the last step, and phase 0 runs once, for the first gradient. */
+ * but the last step, and phase 0 runs once, for the first gradient. Each
+ * recorded event costs a few microseconds of queue time between launches. */
 #define MFAC_NPHASES 4
 mfac_status mfac_window_trace(mfac_window w, int32_t enable);
 

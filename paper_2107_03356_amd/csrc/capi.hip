@@ -278,6 +278,23 @@ mfac_status window_slot_update(mfac_window w, int pstride, int k) {
     return MFAC_OK;
 }
 
+// window_slot_update followed by the coefficients coef[i*nv + c] = scale_c
+// (Ainv rhs_c)_i (see launch_coef_from_inv); the O(m^2) update forms them in
+// the same pass over Ainv.
+mfac_status window_slot_update_coef(mfac_window w, int pstride, int k, const double* rhs, int rstride, int nv, int kc,
+                                    double s0, double s1) {
+    if (w->period == 0 || w->since_refactor + 1 >= w->period) {
+        mfac_status rc = window_factor(w, w->p, pstride, k);
+        if (rc != MFAC_OK) return rc;
+        HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, rhs, rstride, nv, kc, s0, s1, w->coef, w->err, w->st));
+        return MFAC_OK;
+    }
+    HIPCHK(launch_inv_replace_coef(w->K, w->m, w->p, pstride, k, (double)w->m * w->lambda, w->Ainv, w->mp, w->zv,
+                                   w->zv + w->mp, rhs, rstride, nv, kc, s0, s1, w->coef, w->err, w->st));
+    w->since_refactor += 1;
+    return MFAC_OK;
+}
+
 }  // namespace
 
 // ====================================================================== misc
@@ -411,8 +428,6 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
     HIPCHK(launch_reduce_partials(w->part, grid, w->m, nv, w->p, w->st));
-    mfac_status rc = window_slot_update(w, nv, k);
-    if (rc != MFAC_OK) return rc;
 
     if (y_out || n > 0) {
         // column 0: c' = -m A^-1 e_k, so y = -G^T c' = m G^T A^-1 e_k;
@@ -427,19 +442,17 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
             vout.y[nv2] = v == 0 ? y_out : Y + (int64_t)(v - 1) * d;
             vout.alpha[nv2] = v == 0 ? 0.0f : (float)inv_lam;
         }
-        if (v0 == 0) {
-            HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p, nv, nv, k, -(double)w->m, inv_lam, w->coef,
-                                        w->err, w->st));
-        } else {
-            // no y_out: coefficients of the queries only (columns 1..n of p)
-            HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, w->m, w->p + 1, nv, nv2, -1, inv_lam, inv_lam, w->coef,
-                                        w->err, w->st));
-        }
+        // no y_out: coefficients of the queries only (columns 1..n of p)
+        const mfac_status rc = v0 == 0 ? window_slot_update_coef(w, nv, k, w->p, nv, nv, k, -(double)w->m, inv_lam)
+                                       : window_slot_update_coef(w, nv, k, w->p + 1, nv, nv2, -1, inv_lam, inv_lam);
+        if (rc != MFAC_OK) return rc;
         HIPCHK(mark_end(w, 1));
         HIPCHK(mark_begin(w));
         HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, nv2, w->coef, vout, al, w->st));
         HIPCHK(mark_end(w, 2));
     } else {
+        const mfac_status rc = window_slot_update(w, nv, k);
+        if (rc != MFAC_OK) return rc;
         HIPCHK(mark_end(w, 1));
     }
     if (slot < 0) w->head = (k + 1) % w->m;
@@ -458,10 +471,7 @@ MFAC_API mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const flo
 
     // coefficients of gradient t once its Gram column is in p (slot k)
     auto coefficients = [&](int k) -> mfac_status {
-        mfac_status rc = window_slot_update(w, 1, k);
-        if (rc != MFAC_OK) return rc;
-        HIPCHK(launch_coef_from_inv(w->Ainv, w->mp, m, w->p, 1, 1, k, -(double)m, inv_lam, w->coef, w->err, w->st));
-        return MFAC_OK;
+        return window_slot_update_coef(w, 1, k, w->p, 1, 1, k, -(double)m, inv_lam);
     };
 
     int k = w->head;

@@ -437,6 +437,59 @@ __global__ __launch_bounds__(256) void k_inv_update(const double* __restrict__ p
     }
 }
 
+// k_inv_update and k_coef_from_inv in one pass over Ainv: one wave per row i
+// updates the row (the same expression per entry) and, for i < m, forms the
+// row's coefficients from the new values (the same per-lane order and wave
+// sums), so both results are those of the two kernels. The column k of the
+// coefficient matrix (kc >= 0) is the new Ainv[i][kc]; the other columns take
+// rhs[j*rstride + c]. grid ceil(mp / 4).
+__global__ __launch_bounds__(256) void k_inv_update_coef(const double* __restrict__ p, int pstride, int k, int m,
+                                                         double mu, const double* __restrict__ z,
+                                                         const double* __restrict__ v, double* __restrict__ Ainv,
+                                                         int mp, const double* __restrict__ rhs, int rstride, int nv,
+                                                         int kc, double s0, double s1, double* __restrict__ coef,
+                                                         int* __restrict__ err) {
+    __shared__ double sh[4];
+    double t, zk, s;
+    inv_update_scalars(p, pstride, k, m, mu, z, v, sh, t, zk, s);
+    if (blockIdx.x == 0 && threadIdx.x == 0 && (!(s > 0.0) || !isfinite(s) || !(t > 0.0))) atomicOr(err, 16);
+    const int lane = threadIdx.x & 63;
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= mp) return;
+    const double r = zk / t, it = 1.0 / t, is = 1.0 / s;
+    const double vi = v[i], wi = z[i] - v[i] * r - (i == k ? 1.0 : 0.0);
+    double* row = Ainv + (int64_t)i * mp;
+    double acc[MAXNV];
+#pragma unroll
+    for (int c = 0; c < MAXNV; ++c) acc[c] = 0.0;
+    const int c0 = kc >= 0 ? 1 : 0;
+    double akc = 0.0;
+    for (int j = lane; j < mp; j += 64) {
+        const double wj = z[j] - v[j] * r - (j == k ? 1.0 : 0.0);
+        const double a = row[j] - vi * v[j] * it + wi * wj * is;
+        row[j] = a;
+        if (j == kc) akc = a;
+        if (j < m) {
+#pragma unroll
+            for (int c = 0; c < MAXNV; ++c)
+                if (c >= c0 && c < nv) acc[c] += a * rhs[(int64_t)j * rstride + c];
+        }
+    }
+    if (i >= m) return;
+    if (c0) akc = wave_sum_d(akc);  // the one lane holding it, exact
+#pragma unroll
+    for (int c = 0; c < MAXNV; ++c) {
+        if (c < nv) {
+            double x = (c < c0) ? akc : wave_sum_d(acc[c]);
+            x *= (c == 0 ? s0 : s1);
+            if (lane == 0) {
+                if (!isfinite(x)) atomicOr(err, 4);
+                coef[i * nv + c] = x;
+            }
+        }
+    }
+}
+
 // coef[i*nv + c] = scale_c * (Ainv rhs_c)_i with rhs_0 = e_k when k >= 0,
 // the other columns p[j*pstride + c]; one wave per row i, lanes along the row.
 __global__ __launch_bounds__(256) void k_coef_from_inv(const double* __restrict__ Ainv, int mp, int m,
@@ -514,6 +567,16 @@ hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, in
     if (e != hipSuccess) return e;
     const int T = mp / 64;
     hipLaunchKernelGGL(k_inv_update, dim3(T * T), dim3(256), 0, st, p, pstride, k, m, mu, z, v, Ainv, mp, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_inv_replace_coef(double* K, int m, const double* p, int pstride, int k, double mu, double* Ainv,
+                                  int mp, double* z, double* v, const double* rhs, int rstride, int nv, int kc,
+                                  double s0, double s1, double* coef, int* err, hipStream_t st) {
+    hipLaunchKernelGGL(k_inv_gemv, dim3((unsigned)ceil_div(mp, 4)), dim3(256), 0, st, K, m, p, pstride, k, Ainv, mp,
+                       z, v, err);
+    hipLaunchKernelGGL(k_inv_update_coef, dim3((unsigned)ceil_div(mp, 4)), dim3(256), 0, st, p, pstride, k, m, mu, z,
+                       v, Ainv, mp, rhs, rstride, nv, kc, s0, s1, coef, err);
     return hipGetLastError();
 }
 

@@ -112,6 +112,12 @@ hipError_t launch_lauum(const double* Linv, double* Ainv, int mp, int nbatch, in
 // replaced)^-1; z, v: mp-double scratch vectors.
 hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, int k, double mu, double* Ainv,
                               int mp, double* z, double* v, int* err, hipStream_t st);
+// launch_inv_replace, then the coefficients of launch_coef_from_inv (rhs at
+// stride rstride, nv columns, column kc the new Ainv's column if kc >= 0)
+// formed in the same pass over Ainv.
+hipError_t launch_inv_replace_coef(double* K, int m, const double* p, int pstride, int k, double mu, double* Ainv,
+                                  int mp, double* z, double* v, const double* rhs, int rstride, int nv, int kc,
+                                  double s0, double s1, double* coef, int* err, hipStream_t st);
 // coef[i*nv+c] = scale_c (Ainv rhs_c)_i: rhs_0 = e_k if k >= 0 (scale s0); the
 // other columns rhs_c[j] = p[j*pstride + c] (scale s1; also column 0 if k < 0).
 hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double* p, int pstride, int nv, int k,

@@ -322,6 +322,20 @@ hipError_t launch_inv_replace(double* K, int m, const double* p, int pstride, in
     CHECK(k >= 0 && k < m);
     return launched();
 }
+hipError_t launch_inv_replace_coef(double* K, int m, const double* p, int pstride, int k, double, double* Ainv, int mp,
+                                  double* z, double* v, const double* rhs, int rstride, int nv, int kc, double, double,
+                                  double* coef, int* err, hipStream_t) {
+    IN(K, (int64_t)m * m * 8);
+    IN(p, ((int64_t)(m - 1) * pstride + 1) * 8);
+    IN(Ainv, (int64_t)mp * mp * 8);
+    IN(z, (int64_t)mp * 8);
+    IN(v, (int64_t)mp * 8);
+    IN(rhs, ((int64_t)(m - 1) * rstride + nv) * 8);
+    IN(coef, (int64_t)m * nv * 8);
+    IN(err, 4);
+    CHECK(k >= 0 && k < m && kc < m && nv >= 1 && nv <= 17);
+    return launched();
+}
 hipError_t launch_coef_from_inv(const double* Ainv, int mp, int m, const double* p, int pstride, int nv, int k, double,
                                 double, double* coef, int* err, hipStream_t) {
     IN(Ainv, (int64_t)mp * mp * 8);
