@@ -381,6 +381,7 @@ __global__ __launch_bounds__(256) void k_inv_gemv(double* __restrict__ K, int m,
     if (i >= mp) return;
     const double* row = Ainv + (int64_t)i * mp;
     double s = 0.0;
+#pragma unroll 4
     for (int j = lane; j < m; j += 64)
         if (j != k) s += row[j] * p[(int64_t)j * pstride];
     s = wave_sum_d(s);
@@ -464,6 +465,7 @@ __global__ __launch_bounds__(256) void k_inv_update_coef(const double* __restric
     for (int c = 0; c < MAXNV; ++c) acc[c] = 0.0;
     const int c0 = kc >= 0 ? 1 : 0;
     double akc = 0.0;
+#pragma unroll 4
     for (int j = lane; j < mp; j += 64) {
         const double wj = z[j] - v[j] * r - (j == k ? 1.0 : 0.0);
         const double a = row[j] - vi * v[j] * it + wi * wj * is;
@@ -504,6 +506,7 @@ __global__ __launch_bounds__(256) void k_coef_from_inv(const double* __restrict_
 #pragma unroll
     for (int c = 0; c < MAXNV; ++c) acc[c] = 0.0;
     const int c0 = k >= 0 ? 1 : 0;
+#pragma unroll 4
     for (int j = lane; j < m; j += 64) {
         const double a = row[j];
 #pragma unroll

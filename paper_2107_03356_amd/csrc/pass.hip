@@ -168,7 +168,15 @@ __global__ __launch_bounds__(256) void k_reduce_partials(const double* __restric
         const int g = row / pg.mg;
         const int64_t stride = (int64_t)pg.mg * nv;
         const double* src = part + (int64_t)g * pg.gx * stride + (int64_t)(row - g * pg.mg) * nv + v;
-        for (int b = bg; b < pg.gx; b += 16) s += src[b * stride];
+        // eight loads in flight, added in the order of b
+        for (int b = bg; b < pg.gx; b += 16 * 8) {
+            double q[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) q[u] = b + 16 * u < pg.gx ? src[(int64_t)(b + 16 * u) * stride] : 0.0;
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (b + 16 * u < pg.gx) s += q[u];
+        }
     }
     red[bg][to] = s;
     __syncthreads();
