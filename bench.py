@@ -61,21 +61,23 @@ def pass_src_sha():
 
 
 def read_counters(workload, kernel):
-    """HBM traffic per launch from the committed rocprofv3 --pmc summary, if it
-    was taken on this workload and the current streaming-kernel sources (else
-    None)."""
-    if not os.path.exists(COUNTERS):
-        return None
-    text = open(COUNTERS).read()
-    sha = pass_src_sha()
-    m = re.search(r"pass_src_sha256_16:\s*(\w+)", text)
-    if not m or m.group(1) != sha:
-        return None
-    m = re.search(r"counters_workload:\s*(\S+)", text)
-    if not m or m.group(1) != workload:
-        return None
-    m = re.search(rf"{kernel}_traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    return float(m.group(1)) if m else None
+    """HBM traffic per launch from a committed rocprofv3 --pmc summary (the
+    workload's own profiles/<workload>_counters.md, else the headline
+    window's), if it was taken on this workload and the current
+    streaming-kernel sources (else None)."""
+    for path in (os.path.join(ROOT, "profiles", f"{workload}_counters.md"), COUNTERS):
+        if not os.path.exists(path):
+            continue
+        text = open(path).read()
+        m = re.search(r"pass_src_sha256_16:\s*(\w+)", text)
+        if not m or m.group(1) != pass_src_sha():
+            continue
+        m = re.search(r"counters_workload:\s*(\S+)", text)
+        if not m or m.group(1) != workload:
+            continue
+        m = re.search(rf"{kernel}_traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+        return float(m.group(1)) if m else None
+    return None
 
 
 STATIC_SRC = [os.path.join(ROOT, "paper_2107_03356_amd", "csrc", f)
