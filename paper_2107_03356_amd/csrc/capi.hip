@@ -295,6 +295,16 @@ mfac_status window_slot_update_coef(mfac_window w, int pstride, int k, const dou
     return MFAC_OK;
 }
 
+// The coefficient phase of a replace whose pass 1 left its partials in
+// w->part (shape grid, nv vectors): p, then the slot update (or refactor) and,
+// with nvc > 0, the coefficients (see window_slot_update_coef).
+mfac_status window_coef_phase(mfac_window w, const Pass1Grid& grid, int nv, int k, const double* rhs, int rstride,
+                              int nvc, int kc, double s0, double s1) {
+    HIPCHK(launch_reduce_partials(w->part, grid, w->m, nv, w->p, w->st));
+    if (nvc > 0) return window_slot_update_coef(w, nv, k, rhs, rstride, nvc, kc, s0, s1);
+    return window_slot_update(w, nv, k);
+}
+
 }  // namespace
 
 // ====================================================================== misc
@@ -427,7 +437,6 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
     HIPCHK(launch_pass1(w->G, w->m, d, w->nslab, nv, vin, al, w->part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_reduce_partials(w->part, grid, w->m, nv, w->p, w->st));
 
     if (y_out || n > 0) {
         // column 0: c' = -m A^-1 e_k, so y = -G^T c' = m G^T A^-1 e_k;
@@ -443,15 +452,15 @@ MFAC_API mfac_status mfac_window_replace(mfac_window w, int32_t slot, const floa
             vout.alpha[nv2] = v == 0 ? 0.0f : (float)inv_lam;
         }
         // no y_out: coefficients of the queries only (columns 1..n of p)
-        const mfac_status rc = v0 == 0 ? window_slot_update_coef(w, nv, k, w->p, nv, nv, k, -(double)w->m, inv_lam)
-                                       : window_slot_update_coef(w, nv, k, w->p + 1, nv, nv2, -1, inv_lam, inv_lam);
+        const mfac_status rc = v0 == 0 ? window_coef_phase(w, grid, nv, k, w->p, nv, nv, k, -(double)w->m, inv_lam)
+                                       : window_coef_phase(w, grid, nv, k, w->p + 1, nv, nv2, -1, inv_lam, inv_lam);
         if (rc != MFAC_OK) return rc;
         HIPCHK(mark_end(w, 1));
         HIPCHK(mark_begin(w));
         HIPCHK(launch_pass2(w->G, w->m, d, w->nslab, nv2, w->coef, vout, al, w->st));
         HIPCHK(mark_end(w, 2));
     } else {
-        const mfac_status rc = window_slot_update(w, nv, k);
+        const mfac_status rc = window_coef_phase(w, grid, nv, k, w->p, nv, 0, -1, 0.0, 0.0);
         if (rc != MFAC_OK) return rc;
         HIPCHK(mark_end(w, 1));
     }
@@ -470,8 +479,8 @@ MFAC_API mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const flo
     const bool fused = m <= PASS21_MAX_M;
 
     // coefficients of gradient t once its Gram column is in p (slot k)
-    auto coefficients = [&](int k) -> mfac_status {
-        return window_slot_update_coef(w, 1, k, w->p, 1, 1, k, -(double)m, inv_lam);
+    auto coefficients = [&](const Pass1Grid& grid, int k) -> mfac_status {
+        return window_coef_phase(w, grid, 1, k, w->p, 1, 1, k, -(double)m, inv_lam);
     };
 
     int k = w->head;
@@ -485,10 +494,9 @@ MFAC_API mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const flo
     HIPCHK(launch_pass1(w->G, m, d, w->nslab, 1, vin, al, w->part, &grid, w->st));
     HIPCHK(mark_end(w, 0));
     HIPCHK(mark_begin(w));
-    HIPCHK(launch_reduce_partials(w->part, grid, m, 1, w->p, w->st));
     w->head = (k + 1) % m;
     w->steps += 1;
-    mfac_status rc = coefficients(k);
+    mfac_status rc = coefficients(grid, k);
     if (rc != MFAC_OK) return rc;
     HIPCHK(mark_end(w, 1));
 
@@ -527,10 +535,9 @@ MFAC_API mfac_status mfac_window_replace_seq(mfac_window w, int32_t n, const flo
             HIPCHK(mark_end(w, 0));
         }
         HIPCHK(mark_begin(w));
-        HIPCHK(launch_reduce_partials(w->part, grid, m, 1, w->p, w->st));
         w->head = (knext + 1) % m;
         w->steps += 1;
-        rc = coefficients(knext);
+        rc = coefficients(grid, knext);
         if (rc != MFAC_OK) return rc;
         HIPCHK(mark_end(w, 1));
         k = knext;
