@@ -87,6 +87,7 @@ struct mfac_window_s {
     hipStream_t st;
     int* err;
     double *K, *A, *Linv, *Ainv, *part, *p, *zv, *gpart, *coef;
+    int64_t gpart_elems;  // the window Gram's partials, and the factor's K segments
     int head;
     int64_t steps;
     // coefficient policy: 0 = refactor from K on every replace; R > 0 = O(m^2)
@@ -120,6 +121,7 @@ struct mfac_static_s {
     hipStream_t st;
     int* err;
     double *A, *Linv, *gpart, *diag, *scores, *qpart;
+    int64_t gpart_elems;  // the Gram's partials, and the factor's K segments when a batch is small
     double* qcoef;
     float* xobs;
     SelectScratch sel;
@@ -152,7 +154,9 @@ size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
     double* p = c.take<double>((size_t)m * nvmax);
     double* zv = c.take<double>((size_t)mp * 2);
     double* coef = c.take<double>((size_t)m * nvmax);
-    double* gpart = c.take<double>((size_t)gram_window_part_doubles(m, nslab_of(d)));
+    // the init Gram's partials and, later, the refactor's split-K segments
+    const int64_t gw = gram_window_part_doubles(m, nslab_of(d)), gk = splitk_part_doubles(mp);
+    double* gpart = c.take<double>((size_t)(gw > gk ? gw : gk));
     if (w) {
         w->err = err;
         w->K = K;
@@ -164,6 +168,7 @@ size_t window_layout(int64_t d, int m, int max_q, char* base, W* w) {
         w->zv = zv;
         w->coef = coef;
         w->gpart = gpart;
+        w->gpart_elems = gw > gk ? gw : gk;
     }
     return c.off;
 }
@@ -262,7 +267,7 @@ void marks_free(H* h) {
 // A = K + m*lambda*I, A = L L^T, Linv = L^-1, Ainv = Linv^T Linv.
 mfac_status window_factor(mfac_window w, const double* p, int pstride, int k) {
     HIPCHK(launch_assemble(w->K, w->m, p, pstride, k, (double)w->m * w->lambda, w->A, w->mp, w->err, w->st));
-    HIPCHK(launch_factor_invert(w->A, w->Linv, w->mp, 1, 0, w->err, w->st));
+    HIPCHK(launch_factor_invert(w->A, w->Linv, w->mp, 1, 0, w->err, w->st, w->gpart, w->gpart_elems));
     HIPCHK(launch_lauum(w->Linv, w->Ainv, w->mp, 1, 0, w->st));
     w->since_refactor = 0;
     return MFAC_OK;
@@ -741,7 +746,11 @@ size_t static_layout(int64_t d, int B, int m, bool fast, char* base, S* s) {
     // the fp32 L^-1 of every block, W and the band list
     double* A = fast ? nullptr : c.take<double>((size_t)batch * mp * mp);
     double* Linv = fast ? nullptr : c.take<double>((size_t)batch * mp * mp);
-    double* gpart = c.take<double>((size_t)static_gram_part(d / B, batch, mp, B, fast));
+    // the Gram's partials and, in the fp64 mode with small batches (few
+    // GEMM tasks), the factor's split-K segments
+    const int64_t ggp = static_gram_part(d / B, batch, mp, B, fast);
+    const int64_t gsk = (!fast && batch < 256) ? splitk_part_doubles(mp) : 0;
+    double* gpart = c.take<double>((size_t)(ggp > gsk ? ggp : gsk));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
     double* qcoef = c.take<double>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
@@ -773,6 +782,7 @@ size_t static_layout(int64_t d, int B, int m, bool fast, char* base, S* s) {
         s->A = A;
         s->Linv = Linv;
         s->gpart = gpart;
+        s->gpart_elems = ggp > gsk ? ggp : gsk;
         s->batch = batch;
     }
     return c.off;
@@ -853,7 +863,8 @@ MFAC_API mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t
         if (eg != hipSuccess) return fail();
         if (mark_end(s, 0) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
         const hipError_t ef = fast ? launch_factor_invert32(s->A32, L32b, s->mp, nb, bstride, s->err, s->st)
-                                   : launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st);
+                                   : launch_factor_invert(s->A, s->Linv, s->mp, nb, bstride, s->err, s->st, s->gpart,
+                                                          s->gpart_elems);
         if (ef != hipSuccess) return fail();
         if (mark_end(s, 1) != hipSuccess || mark_begin(s) != hipSuccess) return fail();
         const hipError_t et =
@@ -1007,7 +1018,9 @@ size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* b
     char* sel = c.take<char>((size_t)select_scratch_bytes(d));
     double* A = c.take<double>((size_t)pl.pb * mp * mp);
     double* Linv = c.take<double>((size_t)pl.pb * mp * mp);
-    double* gpart = c.take<double>((size_t)(pa > pb2 ? pa : pb2));
+    const int64_t gpp = pa > pb2 ? pa : pb2;
+    const int64_t gsk = pl.pb < 256 ? splitk_part_doubles(mp) : 0;
+    double* gpart = c.take<double>((size_t)(gpp > gsk ? gpp : gsk));
     double* qpart = c.take<double>((size_t)static_query_part_doubles(d, B, m));
     double* qcoef = c.take<double>((size_t)(d / B) * m * 4);
     float* xobs = c.take<float>((size_t)d);
@@ -1021,6 +1034,7 @@ size_t static_paged_layout(int64_t d, int B, int m, const PagedPlan& pl, char* b
         s->A = A;
         s->Linv = Linv;
         s->gpart = gpart;
+        s->gpart_elems = gpp > gsk ? gpp : gsk;
         s->qpart = qpart;
         s->qcoef = qcoef;
         s->xobs = xobs;
@@ -1086,7 +1100,7 @@ bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
             PCHK(launch_gram_blocks(s->page[b], m, pl.pc, B, 0, nbp, mu, s->A, mp, s->gpart, st));
             PCHK(mark_end(s, 0));
             PCHK(mark_begin(s));
-            PCHK(launch_factor_invert(s->A, s->Linv, mp, nbp, bstride, s->err, st));
+            PCHK(launch_factor_invert(s->A, s->Linv, mp, nbp, bstride, s->err, st, s->gpart, s->gpart_elems));
             PCHK(mark_end(s, 1));
             PCHK(mark_begin(s));
             PCHK(launch_trmm_diag(s->Linv, mp, bstride, s->page[b], m, pl.pc, B, 0, nbp, s->lambda, s->diag + c0, st));
@@ -1107,7 +1121,7 @@ bool paged_run(mfac_static s, const PagedPlan& pl, double mu) {
             PCHK(hipEventRecord(E[6 + b], st));
         }
         PCHK(mark_begin(s));
-        PCHK(launch_factor_invert(s->A, s->Linv, mp, 1, bstride, s->err, st));
+        PCHK(launch_factor_invert(s->A, s->Linv, mp, 1, bstride, s->err, st, s->gpart, s->gpart_elems));
         PCHK(mark_end(s, 1));
         PCHK(hipEventRecord(E[1], st));
         PCHK(hipStreamWaitEvent(s->up, E[1], 0));

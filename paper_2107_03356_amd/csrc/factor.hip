@@ -85,6 +85,12 @@ struct GemmArgs {
     int tiles_m, tiles_n;
     int mode;   // task layout, see task_tiles
     int ntask;  // tasks per batch item
+    // split K: nsplit > 1 gives each task nsplit work-groups, work-group s
+    // summing segment s of each tile's K range into part (unscaled, one
+    // BM x BN tile per segment, batch item and tile); k_bgemm_reduce then
+    // forms C from the segments
+    int nsplit, nbatch;
+    T* part;
 };
 
 enum : int {
@@ -143,7 +149,9 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
     __shared__ T As[2][TA ? BK : BM][TA ? PBN : PA];
     __shared__ T Bs[2][TB ? BN : BK][TB ? PA : PBN];
-    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int lid0 = xcd_remap(blockIdx.x, gridDim.x);
+    const int seg = lid0 % g.nsplit;
+    const int lid = lid0 / g.nsplit;
     const int bt = lid / g.ntask;
     int I0, J0, I1, J1;
     task_tiles(g, lid - bt * g.ntask, I0, J0, I1, J1);
@@ -159,6 +167,13 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
         if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BM);
         if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BN);
         if (g.flags & KLO_COL) klo = J * BN;
+        if (g.nsplit > 1) {
+            // this work-group's segment of the tile's K range (whole chunks; may be empty)
+            const int kc = ((khi - klo + g.nsplit - 1) / g.nsplit + BK - 1) / BK * BK;
+            const int a = min(khi, klo + seg * kc), b = min(khi, a + kc);
+            klo = a;
+            khi = b;
+        }
         const int mrow0 = I * BM, ncol0 = J * BN;
 
         // staging of 128 x BK elements per operand and chunk, NP pairs per
@@ -226,7 +241,7 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
         // before the first wait)
         typename M::acc acc[2][4];
         const T cs = (T)(g.beta / g.alpha);
-        if (g.beta != 0.0 && !idle) {
+        if (g.beta != 0.0 && !idle && g.nsplit == 1) {
     #pragma unroll
             for (int x = 0; x < 2; ++x)
     #pragma unroll
@@ -275,6 +290,19 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
             __syncthreads();
         }
         if (idle) return;
+        if (g.nsplit > 1) {
+            T* P = g.part + ((((int64_t)seg * g.nbatch + bt) * g.tiles_m + I) * g.tiles_n + J) * (BM * BN);
+    #pragma unroll
+            for (int x = 0; x < 2; ++x)
+    #pragma unroll
+                for (int y = 0; y < 4; ++y)
+    #pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int row = crow(x, r), col = ccol(y);
+                        if (row < g.M && col < g.N) P[(row - mrow0) * BN + (col - ncol0)] = acc[x][y][r];
+                    }
+            return;
+        }
     #pragma unroll
         for (int x = 0; x < 2; ++x)
     #pragma unroll
@@ -292,10 +320,46 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
     }
 }
 
+// C = alpha * (sum of the K segments, in segment order) + beta * C over the
+// elements k_bgemm would write (inside M x N, not in the idle upper pieces of
+// a lower-triangle product's diagonal tiles). One work-group per 1024-element
+// chunk of each task's tiles, four adjacent columns a thread, every segment
+// loaded before the sum so that the loads overlap.
+template <typename T>
+__global__ __launch_bounds__(256) void k_bgemm_reduce(GemmArgs<T> g) {
+    typedef T v4 __attribute__((ext_vector_type(4)));
+    constexpr int CH = BM * BN / 1024;
+    const int ch = blockIdx.x % CH, q = (blockIdx.x / CH) & 1, lid = blockIdx.x / (2 * CH);
+    const int bt = lid / g.ntask;
+    int I0, J0, I1, J1;
+    task_tiles(g, lid - bt * g.ntask, I0, J0, I1, J1);
+    const int I = q == 0 ? I0 : I1, J = q == 0 ? J0 : J1;
+    if (I < 0) return;
+    const int e = ch * 1024 + threadIdx.x * 4;
+    const int r = e / BN, c = e - r * BN;
+    const int row = I * BM + r, col = J * BN + c;
+    if (row >= g.M || col >= g.N) return;
+    if ((g.flags & LOWER_ONLY) && I == J && (r / 32) * 32 + 31 < (c / 64) * 64) return;
+    const int64_t sstride = (int64_t)g.nbatch * g.tiles_m * g.tiles_n * (BM * BN);
+    const T* P = g.part + (((int64_t)bt * g.tiles_m + I) * g.tiles_n + J) * (BM * BN) + e;
+    v4 s[8];
+#pragma unroll
+    for (int sg = 0; sg < 8; ++sg)
+        if (sg < g.nsplit) s[sg] = *reinterpret_cast<const v4*>(P + sg * sstride);
+    v4 v = s[0];
+#pragma unroll
+    for (int sg = 1; sg < 8; ++sg)
+        if (sg < g.nsplit) v += s[sg];
+    T* dst = g.C + (int64_t)bt * g.bstride + (int64_t)(g.cm0 + row) * g.ld + g.cn0 + col;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        if (col + k < g.N) dst[k] = g.beta != 0.0 ? (T)g.alpha * v[k] + (T)g.beta * dst[k] : (T)g.alpha * v[k];
+}
+
 template <typename T>
 hipError_t gemm(bool ta, bool tb, const T* A, int a0r, int a0c, const T* B, int b0r, int b0c, T* C, int cm0, int cn0,
                 int M, int N, int K, double alpha, double beta, int flags, int mp, int nbatch, int64_t bstride,
-                hipStream_t st) {
+                T* part, int64_t part_elems, hipStream_t st) {
     GemmArgs<T> g;
     g.A = A;
     g.B = B;
@@ -329,61 +393,91 @@ hipError_t gemm(bool ta, bool tb, const T* A, int a0r, int a0c, const T* B, int 
         g.mode = TASK_PLAIN;
         g.ntask = g.tiles_m * g.tiles_n;
     }
-    const int64_t grid = (int64_t)g.ntask * nbatch;
+    // Few tasks (one matrix, or a handful) leave most CUs idle and make each
+    // work-group walk its whole K range chunk after chunk: split K over up to
+    // 8 work-groups per task, as far as part holds the segments.
+    const int64_t tasks = (int64_t)g.ntask * nbatch;
+    g.nsplit = 1;
+    g.nbatch = nbatch;
+    g.part = part;
+    if (part && tasks < 256 && K >= 4 * Mf<T>::BK) {
+        int ns = (int)(256 / tasks < 8 ? 256 / tasks : 8);
+        if (ns > K / (2 * Mf<T>::BK)) ns = K / (2 * Mf<T>::BK);
+        while (ns > 1 && (int64_t)ns * nbatch * g.tiles_m * g.tiles_n * (BM * BN) > part_elems) --ns;
+        g.nsplit = ns < 1 ? 1 : ns;
+    }
+    const int64_t grid = tasks * g.nsplit;
     if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<T, false, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
     if (!ta && tb) hipLaunchKernelGGL((k_bgemm<T, false, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
     if (ta && !tb) hipLaunchKernelGGL((k_bgemm<T, true, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
     if (ta && tb) hipLaunchKernelGGL((k_bgemm<T, true, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || g.nsplit == 1) return e;
+    hipLaunchKernelGGL((k_bgemm_reduce<T>), dim3((unsigned)(tasks * 2 * (BM * BN / 1024))), dim3(256), 0, st, g);
     return hipGetLastError();
 }
 
 // Factor and invert the diagonal block [o, o+n) of every batch item (n a
 // multiple of 64). U = L21^T (h x n2) is kept in the upper block A12.
 template <typename T>
-hipError_t factor_node(T* A, T* Linv, int o, int n, int mp, int nbatch, int64_t bstride, int* err, hipStream_t st) {
+hipError_t factor_node(T* A, T* Linv, int o, int n, int mp, int nbatch, int64_t bstride, int* err, T* part,
+                       int64_t part_elems, hipStream_t st) {
     if (n <= 128) return launch_factor_node(A, Linv, mp, nbatch, bstride, o, n, err, st);
     const int h = (n / 128) * 64;  // split at a multiple of 64; n2 >= h
     const int n2 = n - h;
     const int p = o + h;
-    hipError_t e = factor_node(A, Linv, o, h, mp, nbatch, bstride, err, st);
+    hipError_t e = factor_node(A, Linv, o, h, mp, nbatch, bstride, err, part, part_elems, st);
     if (e != hipSuccess) return e;
     // U = Linv11 A21^T (h x n2) -> A12; Linv11 lower: k < (I+1) BM
-    e = gemm(false, true, Linv, o, o, A, p, o, A, o, p, h, n2, h, 1.0, 0.0, KHI_ROW, mp, nbatch, bstride, st);
+    e = gemm(false, true, Linv, o, o, A, p, o, A, o, p, h, n2, h, 1.0, 0.0, KHI_ROW, mp, nbatch, bstride, part,
+             part_elems, st);
     if (e != hipSuccess) return e;
     // A22 -= U^T U (lower tiles)
-    e = gemm(true, false, A, o, p, A, o, p, A, p, p, n2, n2, h, -1.0, 1.0, LOWER_ONLY, mp, nbatch, bstride, st);
+    e = gemm(true, false, A, o, p, A, o, p, A, p, p, n2, n2, h, -1.0, 1.0, LOWER_ONLY, mp, nbatch, bstride, part,
+             part_elems, st);
     if (e != hipSuccess) return e;
-    e = factor_node(A, Linv, p, n2, mp, nbatch, bstride, err, st);
+    e = factor_node(A, Linv, p, n2, mp, nbatch, bstride, err, part, part_elems, st);
     if (e != hipSuccess) return e;
     // T = U^T Linv11 (n2 x h) -> A21; Linv11 lower: op(B)[k][j] = 0 for k < j
-    e = gemm(true, false, A, o, p, Linv, o, o, A, p, o, n2, h, h, 1.0, 0.0, KLO_COL, mp, nbatch, bstride, st);
+    e = gemm(true, false, A, o, p, Linv, o, o, A, p, o, n2, h, h, 1.0, 0.0, KLO_COL, mp, nbatch, bstride, part,
+             part_elems, st);
     if (e != hipSuccess) return e;
     // Linv21 = -Linv22 T; Linv22 lower
     return gemm(false, false, Linv, p, p, A, p, o, Linv, p, o, n2, h, n2, -1.0, 0.0, KHI_ROW, mp, nbatch, bstride,
-                st);
+                part, part_elems, st);
 }
 
 }  // namespace
 
 template <typename T>
-hipError_t factor_invert(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int* err, hipStream_t st) {
+hipError_t factor_invert(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int* err, T* part, int64_t part_elems,
+                         hipStream_t st) {
     // The trimmed K ranges read Linv only in the lower triangle and in the
     // first superdiagonal of 64 x 64 tiles (upper halves of 128-wide diagonal
     // blocks at 64-aligned origins); the leaves write zeros above their own
     // diagonals, so only that superdiagonal needs clearing.
     hipError_t e = launch_zero_superdiag(Linv, mp, nbatch, bstride, st);
     if (e != hipSuccess) return e;
-    return factor_node(A, Linv, 0, mp, mp, nbatch, bstride, err, st);
+    return factor_node(A, Linv, 0, mp, mp, nbatch, bstride, err, part, part_elems, st);
+}
+
+int64_t splitk_part_doubles(int mp) {
+    if (mp <= 128) return 0;  // a single node: no GEMMs
+    // segments x tiles <= 8 x (all 128 x 128 tiles of the largest product) and
+    // <= 512 tiles (split only below 256 tasks, at most two tiles a task)
+    const int64_t t = ceil_div(mp, BM) * ceil_div(mp, BM);
+    const int64_t tiles = 8 * t < 512 ? 8 * t : 512;
+    return tiles * (BM * BN);
 }
 
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
-                                hipStream_t st) {
-    return factor_invert<double>(A, Linv, mp, nbatch, bstride, err, st);
+                                hipStream_t st, double* part, int64_t part_elems) {
+    return factor_invert<double>(A, Linv, mp, nbatch, bstride, err, part, part_elems, st);
 }
 
 hipError_t launch_factor_invert32(float* A, float* Linv, int mp, int nbatch, int64_t bstride, int* err,
                                   hipStream_t st) {
-    return factor_invert<float>(A, Linv, mp, nbatch, bstride, err, st);
+    return factor_invert<float>(A, Linv, mp, nbatch, bstride, err, nullptr, 0, st);
 }
 
 }  // namespace mfac

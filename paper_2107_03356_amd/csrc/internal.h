@@ -101,8 +101,12 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
 // upper tiles are left unspecified: readers use the lower triangle only). A is
 // consumed (its contents afterwards are scratch). err |= 2 on a non-positive
 // pivot. Recursive blocked algorithm on batched fp64 MFMA GEMMs.
+// part (part_elems doubles, or nullptr): room for the K segments of GEMMs
+// with few tasks (one matrix), which then split K over more work-groups;
+// splitk_part_doubles(mp) covers every GEMM of an mp factor.
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
-                                hipStream_t st);
+                                hipStream_t st, double* part = nullptr, int64_t part_elems = 0);
+int64_t splitk_part_doubles(int mp);
 // The same in fp32 (fp32 matrix cores and leaves), for the fast static mode.
 hipError_t launch_factor_invert32(float* A, float* Linv, int mp, int nbatch, int64_t bstride, int* err,
                                   hipStream_t st);

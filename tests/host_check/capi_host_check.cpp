@@ -292,10 +292,15 @@ hipError_t launch_assemble(double* K, int m, const double* p, int pstride, int k
     IN(err, 4);
     return launched();
 }
-hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err, hipStream_t) {
+int64_t splitk_part_doubles(int mp) { return mp <= 128 ? 0 : (int64_t)512 * 128 * 128; }
+hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err, hipStream_t,
+                                double* part, int64_t part_elems) {
     IN(A, ((int64_t)(nbatch - 1) * bstride + (int64_t)mp * mp) * 8);
     IN(Linv, ((int64_t)(nbatch - 1) * bstride + (int64_t)mp * mp) * 8);
     IN(err, 4);
+    if (part) IN(part, part_elems * 8);
+    // one matrix (the refactor, the one-block precompute) brings room for its split-K segments
+    if (nbatch == 1 && mp > 128) CHECK(part && part_elems >= splitk_part_doubles(mp));
     CHECK(mp % NB == 0);
     return launched();
 }
