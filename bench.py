@@ -60,6 +60,11 @@ def pass_src_sha():
     return h.hexdigest()[:16]
 
 
+# timed steps per workload when --steps is not given: about 0.3 s or more of
+# timed work
+DEFAULT_STEPS = {"dyn_d1m_m256": 1000}
+
+
 def read_counters(workload, kernel):
     """HBM traffic per launch from a committed rocprofv3 --pmc summary (the
     workload's own profiles/<workload>_counters.md, else the headline
@@ -623,7 +628,9 @@ def cpu_optimizer_baseline(wl, seed, nsteps):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 20; 1000 for the d = 1M window, whose 20 steps "
+                         "would time only ~6 ms of work while the clocks ramp)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dyn_resnet50_d25.6m_m1024")
     ap.add_argument("--seed", type=int, default=0)
@@ -649,6 +656,8 @@ def main():
     from synth import GradientStream, get_workload
 
     wl = get_workload(args.workload)
+    if args.steps is None:
+        args.steps = DEFAULT_STEPS.get(wl.name, 20)
     dev = torch.device("cuda:0")
     if wl.kind == "static":
         return bench_static(args, wl, dev)
