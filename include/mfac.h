@@ -248,10 +248,13 @@ mfac_status mfac_static_precompute(mfac_static* out, int64_t d, int32_t block, i
 #define MFAC_STATIC_TRACE 1u /* record HIP events around the precompute's stages and
                                 mfac_obs_mask; read with mfac_static_trace_read */
 /* Fast mode (mfac_static_precompute only; m <= 4096, block <= 65536): the
- * Gram matrices and W on fp32 matrix cores (fp32 products, sums of up to 512
- * products in fp32 then fp64; the factor stays fp64). The inverse diagonal then
- * carries the fp32 rounding (about 1e-8 relative on gradient-like data with a
- * well-conditioned G_b G_b^T + m*lambda*I). G is left intact: the fp32 L^-1 of
+ * Gram matrices, their Cholesky factors and inverses, and W on fp32 matrix
+ * cores (fp32 products and sums: a Gram entry over at most 2048 columns,
+ * wider blocks adding their 2048-column splits in fp64; W over the m rows;
+ * the squares of W summed in fp64 for the diagonal). The inverse diagonal then
+ * carries the fp32 rounding (on gradient-like data with a well-conditioned
+ * G_b G_b^T + m*lambda*I, a largest entry error of 4.1e-6 relative measured
+ * at d = 4.19M, B = 2048, m = 1024). G is left intact: the fp32 L^-1 of
  * every block is kept in the workspace, and W is formed into the workspace by
  * the first query that reads it (mfac_static_ihvp, mfac_static_element,
  * mfac_obs_update). mfac_obs_mask stays exact: coordinates whose fp64 score
