@@ -1,6 +1,6 @@
 """GPU parity of the fast static mode (MFAC_STATIC_FP32) against the fp64 oracle.
 
-The Gram matrices and W run on fp32 matrix cores; the inverse diagonal then
+The Gram matrices, their factors and W run on fp32 matrix cores; the inverse diagonal then
 carries fp32 rounding, while the keep-mask must still equal the oracle's bit
 for bit (its band at the cut is recomputed in fp64). Each case checks:
 the diagonal and every score against the oracle (the measured score error
