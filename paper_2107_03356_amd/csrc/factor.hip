@@ -29,7 +29,7 @@ hipError_t launch_factor_node(T* A, T* Linv, int mp, int nbatch, int64_t bstride
 
 namespace {
 
-constexpr int BM = 128, BN = 128;
+constexpr int TILE = 128;  // the large GEMM tile (k_bgemm's BT; small products take 64)
 
 // Per element type: the MFMA (16x16x4: fp64, or fp32 on twice the rate), its
 // accumulator, the row of an accumulator register, the k-chunk depth (16 for
@@ -43,7 +43,6 @@ struct Mf<double> {
     typedef double2 pair;
     static constexpr int BK = 16;
     static constexpr int PA = BK + 2;
-    static constexpr int PBN = BN + 16;
     static __device__ __forceinline__ acc mfma(double a, double b, acc c) {
         return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
     }
@@ -55,7 +54,6 @@ struct Mf<float> {
     typedef float2 pair;
     static constexpr int BK = 16;
     static constexpr int PA = BK + 4;
-    static constexpr int PBN = BN + 16;
     static __device__ __forceinline__ acc mfma(float a, float b, acc c) {
         return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
     }
@@ -63,9 +61,9 @@ struct Mf<float> {
 };
 
 enum : int {
-    KHI_ROW = 1,   // A lower triangular: k < (I+1)*BM for output row tile I
-    KHI_COL = 2,   // op(B) upper triangular: k < (J+1)*BN for output column tile J
-    KLO_COL = 4,   // op(B) lower triangular: k >= J*BN
+    KHI_ROW = 1,   // A lower triangular: k < (I+1)*BT for output row tile I
+    KHI_COL = 2,   // op(B) upper triangular: k < (J+1)*BT for output column tile J
+    KLO_COL = 4,   // op(B) lower triangular: k >= J*BT
     LOWER_ONLY = 8 // only output tiles with I >= J
 };
 
@@ -87,7 +85,7 @@ struct GemmArgs {
     int ntask;  // tasks per batch item
     // split K: nsplit > 1 gives each task nsplit work-groups, work-group s
     // summing segment s of each tile's K range into part (unscaled, one
-    // BM x BN tile per segment, batch item and tile); k_bgemm_reduce then
+    // BT x BT tile per segment, batch item and tile); k_bgemm_reduce then
     // forms C from the segments
     int nsplit, nbatch;
     T* part;
@@ -132,23 +130,27 @@ __device__ __forceinline__ void task_tiles(const GemmArgs<T>& g, int t, int& I0,
 // C = alpha * op(A) op(B) + beta * C on sub-matrices of every batch item:
 //   op(A)[m][k] = TA ? A[a0r+k][a0c+m] : A[a0r+m][a0c+k]
 //   op(B)[k][n] = TB ? B[b0r+n][b0c+k] : B[b0r+k][b0c+n]
-// One work-group per task of one or two 128 x 128 output tiles (a long and a
+// One work-group per task of one or two BT x BT output tiles (a long and a
 // short tile of a triangular product together, so tasks take equal time;
 // lower-triangle products launch only their lower tiles), 16-deep k-chunks
-// through double-buffered LDS with the next chunk's loads in flight. Eight
-// waves per work-group, each owning 32 x 64 of a tile as 2 x 4 MFMA tiles, and
-// two work-groups per CU. Rows/columns past M/N (a half tile when M or N is an odd multiple
-// of 64) load clamped, in-bounds data and are never stored. The elements C
+// through double-buffered LDS with the next chunk's loads in flight. BT / 16
+// waves per work-group, each owning 32 x BT/2 of a tile as 2 x BT/32 MFMA
+// tiles: BT = 128 (eight waves, two work-groups per CU) or 64 (four waves,
+// four per CU). Rows/columns past M/N (a half tile when M or N is an odd
+// multiple of 64) load clamped, in-bounds data and are never stored. The elements C
 // writes are disjoint from the ones A and B read (they may share a buffer).
-template <typename T, bool TA, bool TB>
-__global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
+template <typename T, bool TA, bool TB, int BT>
+__global__ __launch_bounds__(4 * BT, 4) void k_bgemm(GemmArgs<T> g) {
     using M = Mf<T>;
     using T2 = typename M::pair;
-    constexpr int PA = M::PA, PBN = M::PBN, BK = M::BK;
-    constexpr int NP = BM * BK / (512 * 2);  // operand pairs per thread and chunk
+    constexpr int NT = 4 * BT;       // threads: BT / 16 waves of 32 x BT/2
+    constexpr int HW = BT / 2;       // a wave's column extent
+    constexpr int NY = BT / 32;      // its 16-column MFMA tiles
+    constexpr int PA = M::PA, PBN = BT + 16, BK = M::BK;
+    constexpr int NP = BT * BK / (NT * 2);  // operand pairs per thread and chunk
     // [m][k] chunks for a non-transposed A / transposed B, [k][m] otherwise
-    __shared__ T As[2][TA ? BK : BM][TA ? PBN : PA];
-    __shared__ T Bs[2][TB ? BN : BK][TB ? PA : PBN];
+    __shared__ T As[2][TA ? BK : BT][TA ? PBN : PA];
+    __shared__ T Bs[2][TB ? BT : BK][TB ? PA : PBN];
     const int lid0 = xcd_remap(blockIdx.x, gridDim.x);
     const int seg = lid0 % g.nsplit;
     const int lid = lid0 / g.nsplit;
@@ -160,13 +162,13 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
     T* __restrict__ C = g.C + (int64_t)bt * g.bstride;
     const int ld = g.ld;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*64
+    const int wr = wave >> 1, wc = wave & 1;  // rows wr*32, columns wc*HW
     const int rl = lane & 15, kl = lane >> 4;
     auto tile = [&](int I, int J) {
         int klo = 0, khi = g.K;
-        if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BM);
-        if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BN);
-        if (g.flags & KLO_COL) klo = J * BN;
+        if (g.flags & KHI_ROW) khi = min(khi, (I + 1) * BT);
+        if (g.flags & KHI_COL) khi = min(khi, (J + 1) * BT);
+        if (g.flags & KLO_COL) klo = J * BT;
         if (g.nsplit > 1) {
             // this work-group's segment of the tile's K range (whole chunks; may be empty)
             const int kc = ((khi - klo + g.nsplit - 1) / g.nsplit + BK - 1) / BK * BK;
@@ -174,14 +176,14 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
             klo = a;
             khi = b;
         }
-        const int mrow0 = I * BM, ncol0 = J * BN;
+        const int mrow0 = I * BT, ncol0 = J * BT;
 
-        // staging of 128 x BK elements per operand and chunk, NP pairs per
+        // staging of BT x BK elements per operand and chunk, NP pairs per
         // thread, kept in registers:
         //   [row][k] layout: row tid/4, k (tid%4)*(BK/4) .. +BK/4-1 (row pieces)
-        //   [k][row] layout: k tid/64 + 8q, row 2*(tid%64) .. +1 (a wave per row)
+        //   [k][row] layout: k tid/HW + 8q, row 2*(tid%HW) .. +1 (HW threads per k)
         const int sr = tid >> 2, sk = (tid & 3) * (BK / 4);
-        const int tk = tid >> 6, tn = (tid & 63) * 2;
+        const int tk = tid / HW, tn = (tid % HW) * 2;
         // clamped source rows / columns (M, N are even, so a clamped pair stays
         // inside the operand)
         const int am = min(mrow0 + (TA ? tn : sr), g.M - (TA ? 2 : 1));
@@ -221,31 +223,31 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
         // C tile coordinates of accumulator (x, y, r): the MFMA result's row
         // of register r of this lane, column lane % 16
         auto crow = [&](int x, int r) { return mrow0 + wr * 32 + x * 16 + M::row(lane, r); };
-        auto ccol = [&](int y) { return ncol0 + wc * 64 + y * 16 + rl; };
+        auto ccol = [&](int y) { return ncol0 + wc * HW + y * 16 + rl; };
         const int nchunk = (khi - klo) / BK;
         // This wave's own K range: a triangular operand is zero outside it, so
         // the wave skips the MFMAs of chunks that lie wholly outside (the
-        // trimmed K range above is per 128-tile; this is per 32 rows / 64
+        // trimmed K range above is per tile; this is per 32 rows / HW
         // columns). A wave whose rows or columns all lie past M / N, or that
         // sits above the diagonal of a diagonal tile of a lower-triangle
         // product, computes and stores nothing.
         int wkhi = khi, wklo = klo;
         if (g.flags & KHI_ROW) wkhi = min(wkhi, mrow0 + wr * 32 + 32);
-        if (g.flags & KLO_COL) wklo = max(wklo, ncol0 + wc * 64);
-        const bool idle = mrow0 + wr * 32 >= g.M || ncol0 + wc * 64 >= g.N ||
-                          ((g.flags & LOWER_ONLY) && I == J && wr * 32 + 31 < wc * 64);
+        if (g.flags & KLO_COL) wklo = max(wklo, ncol0 + wc * HW);
+        const bool idle = mrow0 + wr * 32 >= g.M || ncol0 + wc * HW >= g.N ||
+                          ((g.flags & LOWER_ONLY) && I == J && wr * 32 + 31 < wc * HW);
         if (nchunk > 0) load_chunk(klo);
         // beta C enters as the accumulator's start value (scaled by 1/alpha), so
         // its loads issue together with the first chunk's
         // (the test is uniform and outside the loops, so all 32 loads issue
         // before the first wait)
-        typename M::acc acc[2][4];
+        typename M::acc acc[2][NY];
         const T cs = (T)(g.beta / g.alpha);
         if (g.beta != 0.0 && !idle && g.nsplit == 1) {
     #pragma unroll
             for (int x = 0; x < 2; ++x)
     #pragma unroll
-                for (int y = 0; y < 4; ++y)
+                for (int y = 0; y < NY; ++y)
     #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int row = min(crow(x, r), g.M - 1), col = min(ccol(y), g.N - 1);
@@ -254,12 +256,12 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
     #pragma unroll
             for (int x = 0; x < 2; ++x)
     #pragma unroll
-                for (int y = 0; y < 4; ++y) acc[x][y] *= cs;
+                for (int y = 0; y < NY; ++y) acc[x][y] *= cs;
         } else {
     #pragma unroll
             for (int x = 0; x < 2; ++x)
     #pragma unroll
-                for (int y = 0; y < 4; ++y) acc[x][y] = typename M::acc{0, 0, 0, 0};
+                for (int y = 0; y < NY; ++y) acc[x][y] = typename M::acc{0, 0, 0, 0};
         }
         if (nchunk > 0) {
             store_chunk(0);
@@ -272,17 +274,17 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
             if (!idle && k0 + BK > wklo && k0 < wkhi) {
     #pragma unroll
             for (int kk = 0; kk < BK / 4; ++kk) {
-                T av[2], bv[4];
+                T av[2], bv[NY];
     #pragma unroll
                 for (int x = 0; x < 2; ++x)
                     av[x] = TA ? As[buf][kk * 4 + kl][wr * 32 + x * 16 + rl] : As[buf][wr * 32 + x * 16 + rl][kk * 4 + kl];
     #pragma unroll
-                for (int y = 0; y < 4; ++y)
-                    bv[y] = TB ? Bs[buf][wc * 64 + y * 16 + rl][kk * 4 + kl] : Bs[buf][kk * 4 + kl][wc * 64 + y * 16 + rl];
+                for (int y = 0; y < NY; ++y)
+                    bv[y] = TB ? Bs[buf][wc * HW + y * 16 + rl][kk * 4 + kl] : Bs[buf][kk * 4 + kl][wc * HW + y * 16 + rl];
     #pragma unroll
                 for (int x = 0; x < 2; ++x)
     #pragma unroll
-                    for (int y = 0; y < 4; ++y)
+                    for (int y = 0; y < NY; ++y)
                         acc[x][y] = M::mfma(av[x], bv[y], acc[x][y]);
             }
             }
@@ -291,22 +293,22 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
         }
         if (idle) return;
         if (g.nsplit > 1) {
-            T* P = g.part + ((((int64_t)seg * g.nbatch + bt) * g.tiles_m + I) * g.tiles_n + J) * (BM * BN);
+            T* P = g.part + ((((int64_t)seg * g.nbatch + bt) * g.tiles_m + I) * g.tiles_n + J) * (BT * BT);
     #pragma unroll
             for (int x = 0; x < 2; ++x)
     #pragma unroll
-                for (int y = 0; y < 4; ++y)
+                for (int y = 0; y < NY; ++y)
     #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int row = crow(x, r), col = ccol(y);
-                        if (row < g.M && col < g.N) P[(row - mrow0) * BN + (col - ncol0)] = acc[x][y][r];
+                        if (row < g.M && col < g.N) P[(row - mrow0) * BT + (col - ncol0)] = acc[x][y][r];
                     }
             return;
         }
     #pragma unroll
         for (int x = 0; x < 2; ++x)
     #pragma unroll
-            for (int y = 0; y < 4; ++y)
+            for (int y = 0; y < NY; ++y)
     #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int row = crow(x, r), col = ccol(y);
@@ -325,10 +327,10 @@ __global__ __launch_bounds__(512, 4) void k_bgemm(GemmArgs<T> g) {
 // a lower-triangle product's diagonal tiles). One work-group per 1024-element
 // chunk of each task's tiles, four adjacent columns a thread, every segment
 // loaded before the sum so that the loads overlap.
-template <typename T>
+template <typename T, int BT>
 __global__ __launch_bounds__(256) void k_bgemm_reduce(GemmArgs<T> g) {
     typedef T v4 __attribute__((ext_vector_type(4)));
-    constexpr int CH = BM * BN / 1024;
+    constexpr int CH = BT * BT / 1024;
     const int ch = blockIdx.x % CH, q = (blockIdx.x / CH) & 1, lid = blockIdx.x / (2 * CH);
     const int bt = lid / g.ntask;
     int I0, J0, I1, J1;
@@ -336,12 +338,12 @@ __global__ __launch_bounds__(256) void k_bgemm_reduce(GemmArgs<T> g) {
     const int I = q == 0 ? I0 : I1, J = q == 0 ? J0 : J1;
     if (I < 0) return;
     const int e = ch * 1024 + threadIdx.x * 4;
-    const int r = e / BN, c = e - r * BN;
-    const int row = I * BM + r, col = J * BN + c;
+    const int r = e / BT, c = e - r * BT;
+    const int row = I * BT + r, col = J * BT + c;
     if (row >= g.M || col >= g.N) return;
-    if ((g.flags & LOWER_ONLY) && I == J && (r / 32) * 32 + 31 < (c / 64) * 64) return;
-    const int64_t sstride = (int64_t)g.nbatch * g.tiles_m * g.tiles_n * (BM * BN);
-    const T* P = g.part + (((int64_t)bt * g.tiles_m + I) * g.tiles_n + J) * (BM * BN) + e;
+    if ((g.flags & LOWER_ONLY) && I == J && (r / 32) * 32 + 31 < (c / (BT / 2)) * (BT / 2)) return;
+    const int64_t sstride = (int64_t)g.nbatch * g.tiles_m * g.tiles_n * (BT * BT);
+    const T* P = g.part + (((int64_t)bt * g.tiles_m + I) * g.tiles_n + J) * (BT * BT) + e;
     v4 s[8];
 #pragma unroll
     for (int sg = 0; sg < 8; ++sg)
@@ -354,6 +356,14 @@ __global__ __launch_bounds__(256) void k_bgemm_reduce(GemmArgs<T> g) {
 #pragma unroll
     for (int k = 0; k < 4; ++k)
         if (col + k < g.N) dst[k] = g.beta != 0.0 ? (T)g.alpha * v[k] + (T)g.beta * dst[k] : (T)g.alpha * v[k];
+}
+
+template <typename T, int BT>
+void launch_bgemm(bool ta, bool tb, int64_t grid, const GemmArgs<T>& g, hipStream_t st) {
+    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<T, false, false, BT>), dim3((unsigned)grid), dim3(4 * BT), 0, st, g);
+    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<T, false, true, BT>), dim3((unsigned)grid), dim3(4 * BT), 0, st, g);
+    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<T, true, false, BT>), dim3((unsigned)grid), dim3(4 * BT), 0, st, g);
+    if (ta && tb) hipLaunchKernelGGL((k_bgemm<T, true, true, BT>), dim3((unsigned)grid), dim3(4 * BT), 0, st, g);
 }
 
 template <typename T>
@@ -378,8 +388,13 @@ hipError_t gemm(bool ta, bool tb, const T* A, int a0r, int a0c, const T* B, int 
     g.alpha = alpha;
     g.beta = beta;
     g.flags = flags;
-    g.tiles_m = (int)ceil_div(M, BM);
-    g.tiles_n = (int)ceil_div(N, BN);
+    // 64 x 64 tiles (four waves, four work-groups per CU) for products of at
+    // most 256 x 256, the recursion's short levels, where 128 x 128 tiles
+    // leave one or four tiles per matrix: 7-8% off the 256 x 256 level in
+    // fp64 and off a single-matrix factor; no change at 128 x 128
+    const int bt = (M <= 256 && N <= 256) ? 64 : 128;
+    g.tiles_m = (int)ceil_div(M, bt);
+    g.tiles_n = (int)ceil_div(N, bt);
     if (flags & LOWER_ONLY) {
         g.mode = TASK_LOWER;  // square: tiles_m == tiles_n
         g.ntask = g.tiles_m * (g.tiles_m + 1) / 2;
@@ -403,17 +418,21 @@ hipError_t gemm(bool ta, bool tb, const T* A, int a0r, int a0c, const T* B, int 
     if (part && tasks < 256 && K >= 4 * Mf<T>::BK) {
         int ns = (int)(256 / tasks < 8 ? 256 / tasks : 8);
         if (ns > K / (2 * Mf<T>::BK)) ns = K / (2 * Mf<T>::BK);
-        while (ns > 1 && (int64_t)ns * nbatch * g.tiles_m * g.tiles_n * (BM * BN) > part_elems) --ns;
+        while (ns > 1 && (int64_t)ns * nbatch * g.tiles_m * g.tiles_n * (bt * bt) > part_elems) --ns;
         g.nsplit = ns < 1 ? 1 : ns;
     }
     const int64_t grid = tasks * g.nsplit;
-    if (!ta && !tb) hipLaunchKernelGGL((k_bgemm<T, false, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
-    if (!ta && tb) hipLaunchKernelGGL((k_bgemm<T, false, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
-    if (ta && !tb) hipLaunchKernelGGL((k_bgemm<T, true, false>), dim3((unsigned)grid), dim3(512), 0, st, g);
-    if (ta && tb) hipLaunchKernelGGL((k_bgemm<T, true, true>), dim3((unsigned)grid), dim3(512), 0, st, g);
+    if (bt == 64)
+        launch_bgemm<T, 64>(ta, tb, grid, g, st);
+    else
+        launch_bgemm<T, 128>(ta, tb, grid, g, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || g.nsplit == 1) return e;
-    hipLaunchKernelGGL((k_bgemm_reduce<T>), dim3((unsigned)(tasks * 2 * (BM * BN / 1024))), dim3(256), 0, st, g);
+    if (bt == 64)
+        hipLaunchKernelGGL((k_bgemm_reduce<T, 64>), dim3((unsigned)(tasks * 2 * (64 * 64 / 1024))), dim3(256), 0, st, g);
+    else
+        hipLaunchKernelGGL((k_bgemm_reduce<T, 128>), dim3((unsigned)(tasks * 2 * (128 * 128 / 1024))), dim3(256), 0,
+                           st, g);
     return hipGetLastError();
 }
 
@@ -428,7 +447,7 @@ hipError_t factor_node(T* A, T* Linv, int o, int n, int mp, int nbatch, int64_t 
     const int p = o + h;
     hipError_t e = factor_node(A, Linv, o, h, mp, nbatch, bstride, err, part, part_elems, st);
     if (e != hipSuccess) return e;
-    // U = Linv11 A21^T (h x n2) -> A12; Linv11 lower: k < (I+1) BM
+    // U = Linv11 A21^T (h x n2) -> A12; Linv11 lower: k < (I+1) BT
     e = gemm(false, true, Linv, o, o, A, p, o, A, o, p, h, n2, h, 1.0, 0.0, KHI_ROW, mp, nbatch, bstride, part,
              part_elems, st);
     if (e != hipSuccess) return e;
@@ -464,10 +483,11 @@ hipError_t factor_invert(T* A, T* Linv, int mp, int nbatch, int64_t bstride, int
 int64_t splitk_part_doubles(int mp) {
     if (mp <= 128) return 0;  // a single node: no GEMMs
     // segments x tiles <= 8 x (all 128 x 128 tiles of the largest product) and
-    // <= 512 tiles (split only below 256 tasks, at most two tiles a task)
-    const int64_t t = ceil_div(mp, BM) * ceil_div(mp, BM);
+    // <= 512 tiles (split only below 256 tasks, at most two tiles a task); 64 x
+    // 64 tiles cover the same area, and 512 of them a quarter of it
+    const int64_t t = ceil_div(mp, TILE) * ceil_div(mp, TILE);
     const int64_t tiles = 8 * t < 512 ? 8 * t : 512;
-    return tiles * (BM * BN);
+    return tiles * (TILE * TILE);
 }
 
 hipError_t launch_factor_invert(double* A, double* Linv, int mp, int nbatch, int64_t bstride, int* err,
