@@ -277,6 +277,38 @@ def test_refactor_policies(dev, period):
     assert win.status() == 0
 
 
+@pytest.mark.parametrize("m", [150, 300, 448, 520, 700, 1030])
+def test_refactor_every_replace_across_gemm_tile_paths(dev, m):
+    """A refactor on every replace at window sizes whose factor takes each
+    GEMM path of one matrix: 64 x 64 tiles only (m = 150, 300: padded to
+    192, 320), a product exactly 256 wide (448), 128 x 128 tiles with half
+    tiles beside 64 x 64 ones (520 -> 576, 700 -> 704), and m > 1024
+    (1030 -> 1088); one matrix always splits K over several work-groups."""
+    from paper_2107_03356_amd import Window
+    base = get_workload("dyn_d1m_m256")
+    wl = base.scaled(d=12000 + 37, m=m, scale_d=base.d)
+    gs = GradientStream(wl, seed=21)
+    G0 = gs.window()
+    say("refactor every replace, m", m)
+    win = Window(wl.d, wl.m, wl.lam, max_queries=1, G0=G0.to(dev), device=dev)
+    win.set_refactor_period(0)
+    orc = WindowOracle(wl.d, wl.m, wl.lam, G0=G0.numpy())
+    worst = 0.0
+    for t in range(3):
+        g = gs.row(wl.m + t)
+        X = gs.queries(t, 1)
+        y, Y = win.replace(g.to(dev), X=X.to(dev))
+        yo = orc.slide(g.numpy())
+        Yo = orc.ihvp(X.numpy())
+        worst = max(worst, rel_l2(y.cpu().numpy(), yo), rel_l2(Y[0].cpu().numpy(), Yo[0]))
+    say("worst rel L2", f"{worst:.2e}")
+    assert win.status() == 0
+    # well conditioned (m < d, lambda = 1e-4) with fp64 coefficients: what is
+    # left is the fp32 rounding of the data (~3e-8), so a factor that is off
+    # in any tile shows far below the general 1e-4 bar
+    assert worst < 1e-6
+
+
 def test_long_run_inverse_updates_do_not_drift(dev):
     """400 O(m^2) inverse updates (over six trips round a 64-slot ring) without a refactor."""
     from paper_2107_03356_amd import Window
