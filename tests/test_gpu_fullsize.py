@@ -188,7 +188,9 @@ def _pool_size():
 
 def test_static_pruning_full_size_setup(dev):
     """Draw G and theta on the GPU, keep the oracle's host copy, run the
-    library's precompute + inverse diagonal + scores + mask."""
+    library's precompute + inverse diagonal + scores + mask: first in the fast
+    mode (fp32 matrix cores, G left intact), then in the fp64 mode (which
+    writes W over G)."""
     from paper_2107_03356_amd import StaticBlocks
     wl = get_workload("static_d4.19m_b2048_m1024")
     d, m, B = wl.d, wl.m, wl.block
@@ -200,6 +202,15 @@ def test_static_pruning_full_size_setup(dev):
     theta = gs.theta()
     Gh = G.cpu().numpy()       # the oracle's copy, taken before the library runs
     keep = d // 2
+    fast = StaticBlocks(G, B, wl.lam, fp32=True)
+    fdiag = fast.inv_diag(fp64=True)
+    fmask, _ = fast.obs_mask(theta, keep)
+    torch.cuda.synchronize()
+    assert fast.status() == 0
+    fdiag, fmask = fdiag.cpu().numpy(), fmask.cpu().numpy()
+    fast.close()
+    del fast
+    torch.cuda.empty_cache()
     sb = StaticBlocks(G, B, wl.lam)
     diag = sb.inv_diag(fp64=True)
     mask, scores = sb.obs_mask(theta, keep)
@@ -207,7 +218,7 @@ def test_static_pruning_full_size_setup(dev):
     assert sb.status() == 0
     _log(f"static full size on GPU in {time.perf_counter() - t0:.1f} s")
     _S["st"] = dict(wl=wl, G=Gh, theta=theta.cpu().numpy(), keep=keep, diag=diag.cpu().numpy(),
-                    scores=scores.cpu().numpy(), mask=mask.cpu().numpy(),
+                    scores=scores.cpu().numpy(), mask=mask.cpu().numpy(), fdiag=fdiag, fmask=fmask,
                     dref=np.full(d, np.nan), parts_done=0)
     sb.close()
     del G, sb
@@ -242,7 +253,8 @@ def test_static_pruning_full_size_oracle_part(dev, part):
 def test_static_pruning_full_size_matches_oracle(dev):
     """Inverse diagonal over all d coordinates (fp64, 1e-11 relative L2 and
     per block), the fp64 scores, and the global top-50% keep-mask bit for bit
-    against the oracle's (Section 4.1: global OBD pruning, ties by index)."""
+    against the oracle's (Section 4.1: global OBD pruning, ties by index);
+    the fast mode's keep-mask bit for bit against the same oracle mask."""
     st = _S.get("st")
     if st is None or st["parts_done"] != _ORACLE_PARTS:
         pytest.skip("oracle incomplete")
@@ -265,6 +277,14 @@ def test_static_pruning_full_size_matches_oracle(dev):
     assert int(mask.sum()) == keep
     diff = np.flatnonzero(mask != mref)
     assert diff.size == 0, (diff.size, diff[:10])
+    # the fast mode: fp32 rounding in its diagonal, the same mask bit for bit
+    # (its band at the cut decided in fp64)
+    fdiag, fmask = st["fdiag"], st["fmask"]
+    frel = np.abs(fdiag - dref) / np.abs(dref)
+    _log(f"fast mode: diag rel L2 {rel_l2(fdiag, dref):.2e}, max rel err {frel.max():.2e}")
+    assert rel_l2(fdiag, dref) < 1e-6
+    fdiff = np.flatnonzero(fmask != mref)
+    assert fdiff.size == 0, (fdiff.size, fdiff[:10])
 
 
 def test_static_pruning_full_size_release(dev):
